@@ -1,0 +1,264 @@
+#!/usr/bin/env python3
+"""Benchmark of the EMU Split/Merge reshard on one MI355X.
+
+One step is one pass of the whole hot path over the 8B decoder's state (Llama-3.1-8B shapes, bf16,
+synthetic seeded weights): reshard TP2 PP2 -> TP4 PP1 (all 4 source and 4 destination shard sets
+resident in HBM), pack the destination shards into 2^28-byte contiguous buckets, and unpack the
+buckets into a second, receiver-side destination set. The copy map is compiled once before timing
+(its compile time is reported separately). Inputs are resident in HBM before the timed region.
+
+Prints one JSON line. ``value`` is the step's HBM traffic rate: algorithmic bytes read + written by the
+three kernels (2 x destination bytes each) divided by the step time. Per-kernel times come from HIP
+events recorded on the stream the kernels run on. The ``cpu_baseline`` leg times the CPU oracle on a
+bounded sample of the same workload (embedding + the first 16 layers).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+EIGHT_B = (32, 4096, 32, 128, 8, 14336, 128256)  # L, H, nH, hd, G, I, V
+PMC_SUMMARY = os.path.join(ROOT, "profiles", "reshard_8b_tp2pp2_tp4pp1_pmc.txt")
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_34645_amd", "csrc", "emu_exec.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_hash():
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per reshard launch from the committed rocprofv3 --pmc summary, if it was taken on the
+    current kernel source; else None."""
+    if not os.path.exists(PMC_SUMMARY):
+        return None
+    vals = {}
+    with open(PMC_SUMMARY) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256_16") != kernel_hash():
+        return None
+    try:
+        return float(vals["reshard_hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(seed, layers):
+    """Time the CPU oracle on embedding + the first `layers` layers of the same transition."""
+    import numpy as np
+
+    import oracle
+
+    m = oracle.Model(*EIGHT_B)
+    src, dst = oracle.Layout(m, 2, 2), oracle.Layout(m, 4, 1)
+    groups = ["embed"] + list(range(layers))
+    rng = np.random.default_rng(seed)
+    shards = {}
+    for r, specs in enumerate(oracle.rank_inventory(src)):
+        for j, s in enumerate(specs):
+            g = "embed" if s.kind == "embed" else ("final" if s.kind in ("final_norm", "lm_head") else s.layer)
+            if g in groups:
+                shards[(r, j)] = rng.integers(0, 1 << 16, size=s.shape, dtype=np.uint16)
+    t = time.perf_counter()
+    out_bytes = 0
+    for g in groups:
+        out = oracle.reshard_group(lambda r, j: shards[(r, j)], src, dst, g)
+        out_bytes += sum(a.nbytes for a in out.values())
+        del out
+    dt = time.perf_counter() - t
+    alg = 2 * out_bytes
+    return {"value": round(alg / dt / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "seconds": round(dt, 3), "algorithmic_bytes": alg,
+            "host_cores_available": len(os.sched_getaffinity(0)),
+            "sample": f"TP2PP2->TP4PP1 reshard of the embedding + layers 0-{layers - 1} of the 8B decoder "
+                      f"(bf16, {alg / 2 / 1e9:.2f} GB of destination shards), NumPy single-threaded, "
+                      f"input generation excluded"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--bucket-bytes", type=int, default=1 << 28)
+    ap.add_argument("--seed", type=int, default=1234)
+    ap.add_argument("--cpu-layers", type=int, default=16)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--tile-vecs", type=int, default=None)
+    ap.add_argument("--wg-per-cu", type=int, default=None)
+    ap.add_argument("--nontemporal", type=int, default=None)
+    ap.add_argument("--lds", type=int, default=None)
+    ap.add_argument("--bucket-wg-per-cu", type=int, default=None)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the reshard is the local step each rank runs, and this build "
+              "has no multi-GPU path. Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_34645_amd import emu
+    from synthetic import device_fill
+
+    emu.load()
+    for opt, v in ((emu.OPT_TILE_VECS, args.tile_vecs), (emu.OPT_WG_PER_CU, args.wg_per_cu),
+                   (emu.OPT_NONTEMPORAL, args.nontemporal), (emu.OPT_LDS_STAGING, args.lds),
+                   (emu.OPT_BUCKET_WG_PER_CU, args.bucket_wg_per_cu)):
+        if v is not None:
+            emu.set_option(opt, v)
+
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda", 0)
+    props = torch.cuda.get_device_properties(dev)
+    model = emu.Model(*EIGHT_B)
+    src, dst = emu.Layout(model, 2, 2), emu.Layout(model, 4, 1)
+    B = args.bucket_bytes
+
+    t = time.perf_counter()
+    plan = emu.Plan(src, dst)
+    plan_ms = (time.perf_counter() - t) * 1e3
+    info = plan.info
+    log(f"plan: {info['n_segments']} segments, {info['n_tiles']} tiles, {plan_ms:.2f} ms")
+
+    ws = plan.workspace(dev)
+    S = plan.alloc(0, dev)
+    D = plan.alloc(1, dev)
+    R = plan.alloc(1, dev)
+    bufs, bptrs = plan.alloc_buckets(1, B, dev)
+    sdesc = plan.tensors(0)
+    device_fill(S.tensors, args.seed, ["norm" if d["kind"].endswith("norm") else "weight" for d in sdesc], "bf16")
+    torch.cuda.synchronize()
+    log(f"resident: {(sum(b.numel() for b in S.bufs + D.bufs + R.bufs) + sum(b.numel() for b in bufs)) / 1e9:.1f} GB")
+
+    reshard_bytes = info["bytes_read"] + info["bytes_written"]
+    _, stream_bytes = plan.bucket_layout(1, B, -1)
+    bucket_bytes_rw = 2 * stream_bytes
+    step_bytes = reshard_bytes + 2 * bucket_bytes_rw
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        plan.reshard(ws, S.ptrs, D.ptrs)
+        if ev:
+            ev[1].record()
+        plan.pack(ws, 1, B, D.ptrs, bptrs)
+        if ev:
+            ev[2].record()
+        plan.unpack(ws, 1, B, bptrs, R.ptrs)
+        if ev:
+            ev[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    r_ms = sorted(e[0].elapsed_time(e[1]) for e in evs)
+    p_ms = sorted(e[1].elapsed_time(e[2]) for e in evs)
+    u_ms = sorted(e[2].elapsed_time(e[3]) for e in evs)
+    mean = lambda x: sum(x) / len(x)
+    med = lambda x: x[len(x) // 2]
+    ok = all(torch.equal(a, b) for a, b in zip(D.bufs, R.bufs))
+
+    # plain device copy of the same destination bytes (torch copy_), as a practical ceiling
+    cev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for b_src, b_dst in zip(D.bufs, R.bufs):
+        b_dst.copy_(b_src)
+    cev[0].record()
+    reps = 5
+    for _ in range(reps):
+        for b_src, b_dst in zip(D.bufs, R.bufs):
+            b_dst.copy_(b_src)
+    cev[1].record()
+    torch.cuda.synchronize()
+    copy_ms = cev[0].elapsed_time(cev[1]) / reps
+    copy_bytes = 2 * sum(b.numel() for b in D.bufs)
+
+    ms_per_step = wall * 1e3 / args.steps
+    reshard_avg = mean(r_ms)
+    achieved = reshard_bytes / (reshard_avg * 1e-3) / 1e9
+    traffic = measured_traffic()
+    out = {
+        "metric": "reshard HBM GB/s (bytes read+written) and ms per 8B transition, % of HBM peak",
+        "value": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic (seeded N(0,0.02) bf16 weights, 1+N(0,0.02) norms; Llama-3.1-8B shapes)",
+        "config": {
+            "workload": "8B decoder bf16: reshard TP2PP2->TP4PP1 + pack into 2^28-byte buckets + unpack",
+            "model": "L32 H4096 32x128 heads 8 KV MLP14336 V128256",
+            "src_layout": "TP2PP2", "dst_layout": "TP4PP1", "bucket_bytes": B,
+            "bytes_per_step": step_bytes, "parallelism": "none (1 GPU holds all ranks' shards)",
+        },
+        "reshard_ms": round(reshard_avg, 4),
+        "reshard_ms_median": round(med(r_ms), 4),
+        "reshard_ms_min_max": [round(r_ms[0], 4), round(r_ms[-1], 4)],
+        "reshard_GBps": round(achieved, 1),
+        "reshard_pct_of_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
+        "pack_ms": round(mean(p_ms), 4),
+        "unpack_ms": round(mean(u_ms), 4),
+        "pack_GBps": round(bucket_bytes_rw / (mean(p_ms) * 1e-3) / 1e9, 1),
+        "unpack_GBps": round(bucket_bytes_rw / (mean(u_ms) * 1e-3) / 1e9, 1),
+        "transition_ms": round(reshard_avg + mean(p_ms) + mean(u_ms), 4),
+        "plan_compile_ms": round(plan_ms, 3),
+        "copy_ceiling_GBps": round(copy_bytes / (copy_ms * 1e-3) / 1e9, 1),
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_reshard",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": reshard_bytes,
+        },
+        "options": {k: emu.get_option(v) for k, v in (("tile_vecs", emu.OPT_TILE_VECS),
+                                                      ("wg_per_cu", emu.OPT_WG_PER_CU),
+                                                      ("nontemporal", emu.OPT_NONTEMPORAL),
+                                                      ("lds_staging", emu.OPT_LDS_STAGING),
+                                                      ("bucket_wg_per_cu", emu.OPT_BUCKET_WG_PER_CU))},
+        "device": {"name": props.name, "cus": props.multi_processor_count,
+                   "hbm_GB": round(props.total_memory / 1e9, 1)},
+        "outputs_consistent": ok,
+        "seed": args.seed,
+    }
+    del S, D, R, bufs
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample ...")
+        out["cpu_baseline"] = cpu_baseline(args.seed, args.cpu_layers)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,207 @@
+/*
+ * emu.h -- C ABI of the MI355X (gfx950) EMU Split/Merge reshard library (libemu.so).
+ *
+ * An Elastic Model Unit (EMU) is one model-stage replica <M, T_tp x pp, R, theta, omega> whose parameter
+ * shards theta_i (i = 1..tp*pp) and optimizer shards omega share one TP/PP layout and are not sharded
+ * across data-parallel replicas (paper, section 5, EMU definition). Split and Merge reshard that state
+ * between two compatible layouts without changing it (section 5.2, primitives (a) and (b); section 6.2,
+ * preserving training semantics). Layout changes run locally after the collectives, and every shard
+ * travels as one contiguous buffer (section 6.2, transport and resharding-transport interplay).
+ *
+ * This library implements that local step on one GPU:
+ *   emu_plan            compile a shard-to-shard copy map between two layouts (host only)
+ *   emu_reshard         execute the map: source shard set -> destination shard set
+ *   emu_pack_buckets    concatenate one side's shards per rank into fixed-size contiguous buckets
+ *   emu_unpack_buckets  the inverse, on the receiver side
+ *
+ * Conventions (the paper fixes none of them; these are the readings the library implements):
+ *   - Megatron-style sharding: q/k/v and gate/up column-parallel, o and down row-parallel,
+ *     embedding and LM head vocab-parallel, RMSNorm weights replicated on every TP rank.
+ *   - Fused QKV (EMU_QKV_HEAD_INTERLEAVED): per rank, for each local KV group g, the rows of g's query
+ *     heads, then k_g, then v_g. tp must divide the KV-head count (tp > KV heads: EMU_ERR_UNSUPPORTED).
+ *   - Fused gate/up (EMU_GATE_UP_BLOCK): per rank, [gate rows of the rank; up rows of the rank].
+ *   - PP stage p holds layers [p*L/pp, (p+1)*L/pp); the embedding is on stage 0, the final norm and
+ *     LM head on stage pp-1; embeddings are untied.
+ *   - Rank inside a unit: r = p*tp + t. Per-rank tensor order ("canonical order"): embed (p == 0);
+ *     per local layer attn_norm, qkv (or q, k, v), o, mlp_norm, gate_up (or gate, up), down;
+ *     final_norm, lm_head (p == pp-1). Tensor index tables list rank 0's tensors first, then rank 1's...
+ *   - Vocabulary padding: pad multiple m > 0 pads V to ceil(V/(tp*m))*tp*m rows; m == 0 means no
+ *     padding and tp must divide V. Destination pad rows are written with zeros; source pad rows are
+ *     never read. Replicated norms are read from TP rank 0 of their stage.
+ *   - Buckets: a rank's stream is its tensors' bytes in canonical order with no padding; bucket k of
+ *     the rank holds stream bytes [k*B, (k+1)*B); the last bucket is short and bytes past its end are
+ *     not touched. Bucket pointer tables list rank 0's buckets first, then rank 1's, ...
+ *
+ * Ownership and execution:
+ *   - The caller allocates and owns every device buffer (tensors, buckets, pointer tables, workspace)
+ *     and every stream. The library allocates host memory for plans only: it never calls hipMalloc or
+ *     hipFree and never synchronizes a device or stream.
+ *   - Pointer tables are DEVICE arrays of 64-bit device addresses. Every tensor and bucket base must be
+ *     16-byte aligned. Source and destination buffers must not overlap (undefined behaviour).
+ *   - Execute calls only enqueue work on the given stream (a hipStream_t; NULL = default stream) on the
+ *     current device, and return. Device faults surface at the caller's next synchronization. Buffers
+ *     and the plan must stay alive until that work has completed.
+ *   - Every function returns an emu_status (0 = EMU_OK); none aborts or throws. On error,
+ *     emu_last_error() returns a thread-local message.
+ *   - A plan is immutable after emu_plan and may be used from several threads; an uploaded workspace
+ *     is only read by the kernels and may serve concurrent launches on several streams.
+ */
+#ifndef EMU_H
+#define EMU_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EMU_ABI_VERSION 1
+
+typedef enum {
+  EMU_OK = 0,
+  EMU_ERR_NULL = -1,        /* a required pointer argument is NULL */
+  EMU_ERR_LAYOUT = -2,      /* a layout does not divide its model (invalid EMU layout) */
+  EMU_ERR_MISMATCH = -3,    /* source and destination describe different models or element types */
+  EMU_ERR_UNSUPPORTED = -4, /* valid by definition but not implemented (tp > KV heads, > 2048 tensors
+                               on one rank) */
+  EMU_ERR_WORKSPACE = -5,   /* workspace too small or not 256-byte aligned */
+  EMU_ERR_BUCKET = -6,      /* bucket size zero or not a multiple of the element size */
+  EMU_ERR_ALIGN = -7,       /* a device pointer argument is not 16-byte aligned */
+  EMU_ERR_HIP = -8,         /* the HIP runtime reported an error (message in emu_last_error) */
+  EMU_ERR_HANDLE = -9,      /* not a live plan handle (NULL, freed, or foreign) */
+  EMU_ERR_RANGE = -10,      /* an index or side argument is out of range */
+  EMU_ERR_ARG = -11         /* another argument is invalid (message in emu_last_error) */
+} emu_status;
+
+typedef enum { EMU_BF16 = 0, EMU_FP32 = 1 } emu_dtype;                       /* 2 / 4 bytes */
+typedef enum { EMU_QKV_HEAD_INTERLEAVED = 0, EMU_QKV_SEPARATE = 1 } emu_qkv_format;
+typedef enum { EMU_GATE_UP_BLOCK = 0, EMU_GATE_UP_SEPARATE = 1 } emu_mlp_format;
+
+typedef enum {
+  EMU_T_EMBED = 0, EMU_T_ATTN_NORM = 1, EMU_T_QKV = 2, EMU_T_Q = 3, EMU_T_K = 4, EMU_T_V = 5,
+  EMU_T_O = 6, EMU_T_MLP_NORM = 7, EMU_T_GATE_UP = 8, EMU_T_GATE = 9, EMU_T_UP = 10,
+  EMU_T_DOWN = 11, EMU_T_FINAL_NORM = 12, EMU_T_LM_HEAD = 13
+} emu_tensor_kind;
+
+/* Llama-style decoder shape: L layers, hidden H, nH query heads of head_dim, KV heads, MLP width, V. */
+typedef struct {
+  int32_t num_layers, hidden, num_heads, num_kv_heads, head_dim, ffn_hidden, vocab;
+} emu_model_t;
+
+/* One EMU layout T_tp x pp plus its storage conventions (paper section 5, EMU definition). */
+typedef struct {
+  emu_model_t model;
+  int32_t tp, pp;
+  int32_t vocab_pad_multiple; /* m; 0 = no padding */
+  int32_t dtype;              /* emu_dtype */
+  int32_t qkv_format;         /* emu_qkv_format */
+  int32_t mlp_format;         /* emu_mlp_format */
+} emu_layout_t;
+
+typedef struct emu_plan_s* emu_plan_t;
+
+typedef struct {
+  int32_t n_src_ranks, n_dst_ranks;
+  int32_t n_src_tensors, n_dst_tensors;
+  int64_t n_segments;        /* copy segments + zero-fill segments */
+  int64_t n_zero_segments;
+  int64_t n_tiles;           /* work tiles of one emu_reshard launch */
+  uint64_t tile_bytes;       /* destination bytes per full tile */
+  uint64_t bytes_read;       /* bytes emu_reshard reads: destination bytes minus zero-filled bytes */
+  uint64_t bytes_written;    /* bytes emu_reshard writes: all destination bytes */
+  uint64_t zero_fill_bytes;
+  uint64_t src_bytes, dst_bytes;
+  uint64_t workspace_bytes;  /* device workspace emu_plan_upload needs */
+  int32_t src_vocab_padded, dst_vocab_padded;
+  int32_t n_general_segments; /* segments not on the 16-byte vector path (misaligned runs) */
+  int32_t reserved;
+} emu_plan_info_t;
+
+typedef struct {
+  int32_t rank;        /* r = p*tp + t */
+  int32_t kind;        /* emu_tensor_kind */
+  int32_t layer;       /* -1 for embed, final_norm, lm_head */
+  int32_t ndim;        /* 1 for norms (rows == 1), else 2 */
+  int64_t rows, cols;  /* row-major shape */
+  uint64_t bytes;
+  uint64_t stream_offset; /* byte offset inside its rank's bucket stream */
+} emu_tensor_desc_t;
+
+/* One entry of the copy map: rows x run bytes copied from the source tensor (src_tensor < 0: zeros)
+ * at src_offset + i*src_stride to the destination tensor at dst_offset + i*dst_stride, i < rows. */
+typedef struct {
+  int32_t src_tensor, dst_tensor;   /* global tensor indices (pointer-table positions) */
+  uint64_t src_offset, dst_offset;  /* bytes */
+  uint64_t src_stride, dst_stride;  /* bytes between consecutive rows */
+  uint64_t rows, run;
+} emu_segment_t;
+
+/* Tuning knobs (process-wide; change them only while no emu call is running). */
+typedef enum {
+  EMU_OPT_TILE_VECS = 0,     /* 16-byte vectors per thread per tile: 4, 8 or 16 (default 8); read by
+                                emu_plan, so a plan keeps the value it was compiled with */
+  EMU_OPT_WG_PER_CU = 1,     /* reshard grid: workgroups per compute unit; 0 = one workgroup per tile
+                                (default 0) */
+  EMU_OPT_NONTEMPORAL = 2,   /* 1 = streaming (non-temporal) loads and stores (default 1) */
+  EMU_OPT_LDS_STAGING = 3,   /* 1 = stage each tile through LDS between load and store (default 0) */
+  EMU_OPT_BUCKET_WG_PER_CU = 4 /* pack/unpack grid: workgroups per compute unit (default 8) */
+} emu_option;
+
+/* Library version (EMU_ABI_VERSION). */
+int emu_version(void);
+/* Human-readable name of a status code. Never NULL. */
+const char* emu_status_str(int status);
+/* Thread-local detail of the last error returned on this thread ("" if none). Never NULL. */
+const char* emu_last_error(void);
+int emu_set_option(int32_t option, int64_t value);
+int emu_get_option(int32_t option, int64_t* value);
+
+/* Validate one layout (section 5.2: Split/Merge are defined between compatible layouts for any
+ * integer factor). Returns EMU_OK, EMU_ERR_LAYOUT or EMU_ERR_UNSUPPORTED. Host only. */
+int emu_layout_check(const emu_layout_t* layout);
+
+/* Compile the copy map from layout *src to layout *dst of the same model and element type
+ * (section 5.2, Split and Merge; the call is direction-free and covers both and their compositions).
+ * Destination-driven: every destination byte is covered by exactly one segment (zero-fill for
+ * destination vocabulary pad rows). Host only: no GPU call. *out receives a new plan. */
+int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out);
+/* Free a plan. Work enqueued with it must have completed. */
+int emu_plan_free(emu_plan_t plan);
+int emu_plan_info(emu_plan_t plan, emu_plan_info_t* out);
+/* Shape of tensor `index` (global, rank-major canonical order) on side 0 (source) or 1 (dest). */
+int emu_tensor_info(emu_plan_t plan, int32_t side, int32_t index, emu_tensor_desc_t* out);
+/* Copy `count` segments starting at `first` (in execution order) into out[]. */
+int emu_plan_segments(emu_plan_t plan, int64_t first, int64_t count, emu_segment_t* out);
+
+/* Enqueue the host-to-device copy of the plan's tables into the caller's workspace (at least
+ * info.workspace_bytes, 256-byte aligned). The plan must outlive the copy. */
+int emu_plan_upload(emu_plan_t plan, void* d_workspace, uint64_t workspace_bytes, void* hip_stream);
+
+/* Execute the reshard (section 5.2 (a)/(b), the local layout change of section 6.2):
+ * d_src_ptrs[i] is the device address of source tensor i, d_dst_ptrs[j] of destination tensor j
+ * (both device arrays of n_src_tensors / n_dst_tensors entries). Reads only the source, writes every
+ * destination byte exactly once. d_workspace holds the uploaded plan tables. */
+int emu_reshard(emu_plan_t plan, const void* d_workspace, const uint64_t* d_src_ptrs,
+                const uint64_t* d_dst_ptrs, void* hip_stream);
+
+/* Bucket geometry of one rank (rank >= 0) or of all ranks together (rank == -1) of one side, for
+ * bucket size bucket_bytes (section 6.2: each shard sent once as a contiguous buffer). Host only. */
+int emu_bucket_layout(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, int32_t rank,
+                      uint64_t* n_buckets, uint64_t* stream_bytes);
+
+/* Pack one side's tensors into buckets: bucket k of rank r receives bytes [k*B, (k+1)*B) of r's
+ * stream. d_tensor_ptrs lists that side's tensors (as for emu_reshard); d_bucket_ptrs lists all
+ * buckets, rank 0 first (emu_bucket_layout(..., -1, ...) of them). Tensor stream offsets are computed
+ * on the device from the tensor sizes held in the workspace. bucket_bytes must be a positive multiple
+ * of the element size. */
+int emu_pack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, uint64_t bucket_bytes,
+                     const uint64_t* d_tensor_ptrs, const uint64_t* d_bucket_ptrs, void* hip_stream);
+/* The inverse of emu_pack_buckets: buckets -> that side's tensors. */
+int emu_unpack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, uint64_t bucket_bytes,
+                       const uint64_t* d_bucket_ptrs, const uint64_t* d_tensor_ptrs, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EMU_H */

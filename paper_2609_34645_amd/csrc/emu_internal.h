@@ -1,0 +1,89 @@
+// Internal structures shared by the host plan compiler (emu_plan.cpp) and the HIP executor
+// (emu_exec.hip). Not part of the public ABI.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "emu.h"
+
+namespace emu {
+
+constexpr uint32_t kPlanMagic = 0x454d5550u;  // "EMUP"
+constexpr int kThreads = 256;                 // workgroup size of every kernel (4 wave64s)
+constexpr int kMaxRankTensors = 2048;         // per-rank tensor offsets live in LDS during pack/unpack
+constexpr uint64_t kChunkBytes = 65536;       // pack/unpack work unit, in stream bytes
+constexpr uint64_t kWsAlign = 256;
+
+// Segment execution modes. Every "vec" mode needs src/dst offsets, strides and the run to be
+// multiples of 16 bytes (and 16-byte aligned tensor bases, an ABI requirement).
+enum SegMode : uint32_t {
+  SEG_VEC_1D = 0,        // one contiguous run; a tile is a fixed slice of it
+  SEG_VEC_ROWS = 1,      // rows shorter than a tile; a tile is `param` whole rows
+  SEG_VEC_ROWCHUNK = 2,  // rows longer than a tile; a tile is one slice of one row
+  SEG_GENERAL = 3,       // any byte alignment; a tile is one slice of one row, copied bytewise
+};
+constexpr uint32_t SEG_MODE_MASK = 0xff;
+constexpr uint32_t SEG_ZERO = 0x100;  // no source: write zeros
+
+// Device copy of one segment. 80 bytes, read with scalar loads by the reshard kernel.
+struct alignas(16) DevSeg {
+  uint64_t src_off, dst_off;
+  uint64_t src_stride, dst_stride;
+  uint64_t rows, run;
+  int32_t src_idx, dst_idx;
+  uint32_t mode;   // SegMode | SEG_ZERO
+  uint32_t param;  // SEG_VEC_ROWS: rows per tile; SEG_VEC_ROWCHUNK / SEG_GENERAL: tiles per row
+  uint32_t rv;     // SEG_VEC_ROWS: 16-byte vectors per row
+  uint32_t magic;  // SEG_VEC_ROWS: ceil(2^32 / rv) for rv > 1 (n / rv == umulhi(n, magic) for n*rv < 2^32)
+  uint64_t tile0;  // index of the segment's first tile
+};
+static_assert(sizeof(DevSeg) == 80, "DevSeg layout");
+
+// Byte offsets of the tables inside the device workspace.
+struct SideTables {
+  uint64_t off_sizes;        // uint64[n_tensors]   tensor byte sizes, global order
+  uint64_t off_rank_first;   // uint32[n_ranks + 1] first global tensor index of each rank
+  uint64_t off_rank_bytes;   // uint64[n_ranks]     stream length of each rank
+  uint64_t off_chunk_first;  // uint64[n_ranks + 1] first pack/unpack chunk of each rank
+};
+
+struct WsLayout {
+  uint64_t off_segs;     // DevSeg[n_segments]
+  uint64_t off_tilemap;  // uint32[n_tiles]  segment index of every tile
+  SideTables side[2];
+  uint64_t total;
+};
+
+struct SideInfo {
+  emu_layout_t lay{};
+  int64_t vp = 0;
+  int32_t nranks = 0;
+  uint64_t total_bytes = 0;
+  std::vector<emu_tensor_desc_t> tensors;
+  std::vector<uint32_t> rank_first;   // nranks + 1
+  std::vector<uint64_t> rank_bytes;   // nranks
+  std::vector<uint64_t> chunk_first;  // nranks + 1
+};
+
+struct Plan {
+  uint32_t magic = kPlanMagic;
+  SideInfo side[2];
+  std::vector<emu_segment_t> segs;  // execution order
+  std::vector<DevSeg> dsegs;
+  int tile_vecs = 8;                // 16-byte vectors per thread per tile
+  uint64_t tile_bytes = 0;
+  uint64_t ntiles = 0;
+  emu_plan_info_t info{};
+  WsLayout ws{};
+  std::vector<uint8_t> host_ws;     // workspace image uploaded by emu_plan_upload
+};
+
+// errors.cpp-style helpers (defined in emu_plan.cpp)
+int fail(int code, const char* fmt, ...);
+void clear_error();
+bool plan_live(const Plan* p);
+int64_t option(int32_t key);
+
+}  // namespace emu

@@ -1,0 +1,561 @@
+// Host side of the EMU reshard library: layout validation, shard inventory, copy-map compilation,
+// bucket geometry, plan queries, options and error reporting. No GPU calls in this file.
+//
+// The copy map is destination-driven. Every shard tensor is described by "blocks": rectangles of one
+// logical tensor (row range x column range) placed at a row/column position of the shard. A
+// destination block is intersected with the source blocks of the same logical tensor; each non-empty
+// intersection is one 2D copy segment (rows x run bytes, with source and destination row strides).
+// Destination rows that no block covers (vocabulary padding) become zero-fill segments. This one rule
+// covers the column-parallel, row-parallel and vocab-parallel cuts, the fused QKV and gate/up
+// permutations, PP regrouping (a layer's blocks live on the stage that owns it) and changes of the
+// fused format, for Split, Merge and their compositions (paper section 5.2, primitives (a) and (b)).
+#include <algorithm>
+#include <atomic>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <unordered_set>
+
+#include "emu_internal.h"
+
+namespace emu {
+
+// ------------------------------------------------------------------------------------------------
+// errors, handles, options
+// ------------------------------------------------------------------------------------------------
+
+static thread_local char g_err[512];
+
+int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+void clear_error() { g_err[0] = 0; }
+
+static std::mutex g_plans_mu;
+static std::unordered_set<const Plan*> g_plans;
+
+bool plan_live(const Plan* p) {
+  if (!p) return false;
+  std::lock_guard<std::mutex> lk(g_plans_mu);
+  return g_plans.count(p) && p->magic == kPlanMagic;
+}
+
+static std::atomic<int64_t> g_opt[5] = {{8}, {0}, {1}, {0}, {8}};
+
+int64_t option(int32_t key) { return g_opt[key].load(std::memory_order_relaxed); }
+
+// ------------------------------------------------------------------------------------------------
+// layouts and inventory
+// ------------------------------------------------------------------------------------------------
+
+// Logical tensor ids: 0 = embedding; 1 + 9*l + k for layer l (k: 0 attn_norm, 1 q, 2 k, 3 v, 4 o,
+// 5 mlp_norm, 6 gate, 7 up, 8 down); 1 + 9*L = final norm; 2 + 9*L = LM head.
+enum { LK_ATTN_NORM = 0, LK_Q, LK_K, LK_V, LK_O, LK_MLP_NORM, LK_GATE, LK_UP, LK_DOWN };
+
+struct Block {
+  int32_t lt;             // logical tensor id
+  int64_t lrow0, nrows;   // logical rows covered
+  int64_t lcol0, ncols;   // logical columns covered
+  int64_t row0, col0;     // position inside the shard tensor
+};
+
+static int elem_size(int32_t dtype) { return dtype == EMU_BF16 ? 2 : dtype == EMU_FP32 ? 4 : 0; }
+
+static int check_layout(const emu_layout_t* l) {
+  if (!l) return fail(EMU_ERR_NULL, "layout is NULL");
+  const emu_model_t& m = l->model;
+  if (m.num_layers <= 0 || m.hidden <= 0 || m.num_heads <= 0 || m.num_kv_heads <= 0 ||
+      m.head_dim <= 0 || m.ffn_hidden <= 0 || m.vocab <= 0)
+    return fail(EMU_ERR_LAYOUT, "model dimensions must be positive");
+  if (l->tp <= 0 || l->pp <= 0 || l->vocab_pad_multiple < 0)
+    return fail(EMU_ERR_LAYOUT, "tp and pp must be positive, the pad multiple non-negative");
+  if (!elem_size(l->dtype)) return fail(EMU_ERR_LAYOUT, "unknown dtype %d", l->dtype);
+  if (l->qkv_format != EMU_QKV_HEAD_INTERLEAVED && l->qkv_format != EMU_QKV_SEPARATE)
+    return fail(EMU_ERR_LAYOUT, "unknown qkv format %d", l->qkv_format);
+  if (l->mlp_format != EMU_GATE_UP_BLOCK && l->mlp_format != EMU_GATE_UP_SEPARATE)
+    return fail(EMU_ERR_LAYOUT, "unknown mlp format %d", l->mlp_format);
+  if (m.num_heads % m.num_kv_heads)
+    return fail(EMU_ERR_LAYOUT, "query heads (%d) not a multiple of KV heads (%d)", m.num_heads, m.num_kv_heads);
+  if (l->tp > m.num_kv_heads)
+    return fail(EMU_ERR_UNSUPPORTED, "tp=%d exceeds the KV-head count %d (KV replication)", l->tp, m.num_kv_heads);
+  if (m.num_kv_heads % l->tp) return fail(EMU_ERR_LAYOUT, "tp=%d does not divide %d KV heads", l->tp, m.num_kv_heads);
+  if (m.ffn_hidden % l->tp) return fail(EMU_ERR_LAYOUT, "tp=%d does not divide the MLP width %d", l->tp, m.ffn_hidden);
+  if (m.num_layers % l->pp) return fail(EMU_ERR_LAYOUT, "pp=%d does not divide %d layers", l->pp, m.num_layers);
+  if (l->vocab_pad_multiple == 0 && m.vocab % l->tp)
+    return fail(EMU_ERR_LAYOUT, "tp=%d does not divide the unpadded vocabulary %d", l->tp, m.vocab);
+  return EMU_OK;
+}
+
+static int64_t padded_vocab(const emu_layout_t& l) {
+  int64_t V = l.model.vocab;
+  if (l.vocab_pad_multiple == 0) return V;
+  int64_t q = int64_t(l.tp) * l.vocab_pad_multiple;
+  return (V + q - 1) / q * q;
+}
+
+// Build one side's tensor list (global, rank-major canonical order) and each tensor's blocks.
+static int build_side(const emu_layout_t& lay, SideInfo& s, std::vector<std::vector<Block>>& blocks) {
+  int rc = check_layout(&lay);
+  if (rc) return rc;
+  const emu_model_t& m = lay.model;
+  const int tp = lay.tp, pp = lay.pp, es = elem_size(lay.dtype);
+  const int64_t H = m.hidden, hd = m.head_dim, G = m.num_kv_heads, nH = m.num_heads, I = m.ffn_hidden;
+  const int64_t qpg = nH / G, gl = G / tp, V = m.vocab;
+  const int L = m.num_layers, per_stage = L / pp;
+  s.lay = lay;
+  s.vp = padded_vocab(lay);
+  s.nranks = tp * pp;
+  const int64_t vr = s.vp / tp;
+  s.tensors.clear();
+  s.rank_first.assign(s.nranks + 1, 0);
+  blocks.clear();
+
+  auto add = [&](int r, int kind, int layer, int ndim, int64_t rows, int64_t cols) {
+    emu_tensor_desc_t d{};
+    d.rank = r; d.kind = kind; d.layer = layer; d.ndim = ndim; d.rows = rows; d.cols = cols;
+    d.bytes = uint64_t(rows) * uint64_t(cols) * uint64_t(es);
+    s.tensors.push_back(d);
+    blocks.emplace_back();
+    return &blocks.back();
+  };
+  auto lt_layer = [&](int l, int k) { return 1 + 9 * l + k; };
+  auto vocab_block = [&](std::vector<Block>* b, int lt, int t) {
+    int64_t real = std::max<int64_t>(0, std::min<int64_t>(vr, V - t * vr));
+    if (real > 0) b->push_back({lt, t * vr, real, 0, H, 0, 0});
+  };
+
+  for (int p = 0; p < pp; ++p) {
+    for (int t = 0; t < tp; ++t) {
+      const int r = p * tp + t;
+      s.rank_first[r] = uint32_t(s.tensors.size());
+      if (p == 0) vocab_block(add(r, EMU_T_EMBED, -1, 2, vr, H), 0, t);
+      for (int l = p * per_stage; l < (p + 1) * per_stage; ++l) {
+        add(r, EMU_T_ATTN_NORM, l, 1, 1, H)->push_back({lt_layer(l, LK_ATTN_NORM), 0, 1, 0, H, 0, 0});
+        if (lay.qkv_format == EMU_QKV_HEAD_INTERLEAVED) {
+          auto* b = add(r, EMU_T_QKV, l, 2, (nH / tp + 2 * gl) * hd, H);
+          for (int64_t j = 0; j < gl; ++j) {
+            const int64_t g = t * gl + j, base = j * (qpg + 2) * hd;
+            b->push_back({lt_layer(l, LK_Q), g * qpg * hd, qpg * hd, 0, H, base, 0});
+            b->push_back({lt_layer(l, LK_K), g * hd, hd, 0, H, base + qpg * hd, 0});
+            b->push_back({lt_layer(l, LK_V), g * hd, hd, 0, H, base + (qpg + 1) * hd, 0});
+          }
+        } else {
+          add(r, EMU_T_Q, l, 2, nH / tp * hd, H)->push_back({lt_layer(l, LK_Q), t * (nH / tp) * hd, nH / tp * hd, 0, H, 0, 0});
+          add(r, EMU_T_K, l, 2, gl * hd, H)->push_back({lt_layer(l, LK_K), t * gl * hd, gl * hd, 0, H, 0, 0});
+          add(r, EMU_T_V, l, 2, gl * hd, H)->push_back({lt_layer(l, LK_V), t * gl * hd, gl * hd, 0, H, 0, 0});
+        }
+        const int64_t oc = nH * hd / tp;
+        add(r, EMU_T_O, l, 2, H, oc)->push_back({lt_layer(l, LK_O), 0, H, t * oc, oc, 0, 0});
+        add(r, EMU_T_MLP_NORM, l, 1, 1, H)->push_back({lt_layer(l, LK_MLP_NORM), 0, 1, 0, H, 0, 0});
+        const int64_t il = I / tp;
+        if (lay.mlp_format == EMU_GATE_UP_BLOCK) {
+          auto* b = add(r, EMU_T_GATE_UP, l, 2, 2 * il, H);
+          b->push_back({lt_layer(l, LK_GATE), t * il, il, 0, H, 0, 0});
+          b->push_back({lt_layer(l, LK_UP), t * il, il, 0, H, il, 0});
+        } else {
+          add(r, EMU_T_GATE, l, 2, il, H)->push_back({lt_layer(l, LK_GATE), t * il, il, 0, H, 0, 0});
+          add(r, EMU_T_UP, l, 2, il, H)->push_back({lt_layer(l, LK_UP), t * il, il, 0, H, 0, 0});
+        }
+        add(r, EMU_T_DOWN, l, 2, H, il)->push_back({lt_layer(l, LK_DOWN), 0, H, t * il, il, 0, 0});
+      }
+      if (p == pp - 1) {
+        add(r, EMU_T_FINAL_NORM, -1, 1, 1, H)->push_back({1 + 9 * L, 0, 1, 0, H, 0, 0});
+        vocab_block(add(r, EMU_T_LM_HEAD, -1, 2, vr, H), 2 + 9 * L, t);
+      }
+      if (s.tensors.size() - s.rank_first[r] > size_t(kMaxRankTensors))
+        return fail(EMU_ERR_UNSUPPORTED, "rank %d holds more than %d tensors", r, kMaxRankTensors);
+    }
+  }
+  s.rank_first[s.nranks] = uint32_t(s.tensors.size());
+  s.rank_bytes.assign(s.nranks, 0);
+  s.chunk_first.assign(s.nranks + 1, 0);
+  s.total_bytes = 0;
+  for (int r = 0; r < s.nranks; ++r) {
+    uint64_t off = 0;
+    for (uint32_t i = s.rank_first[r]; i < s.rank_first[r + 1]; ++i) {
+      s.tensors[i].stream_offset = off;
+      off += s.tensors[i].bytes;
+    }
+    s.rank_bytes[r] = off;
+    s.total_bytes += off;
+    s.chunk_first[r + 1] = s.chunk_first[r] + (off + kChunkBytes - 1) / kChunkBytes;
+  }
+  return EMU_OK;
+}
+
+// ------------------------------------------------------------------------------------------------
+// copy map
+// ------------------------------------------------------------------------------------------------
+
+static bool is_norm(int kind) {
+  return kind == EMU_T_ATTN_NORM || kind == EMU_T_MLP_NORM || kind == EMU_T_FINAL_NORM;
+}
+
+struct SrcRef {
+  int32_t tensor;
+  Block b;
+};
+
+static void push_segment(std::vector<emu_segment_t>& out, const emu_segment_t& s) {
+  if (!out.empty()) {
+    emu_segment_t& p = out.back();
+    // append to the previous run when both are single runs, same tensors, contiguous on both sides
+    if (p.rows == 1 && s.rows == 1 && p.src_tensor == s.src_tensor && p.dst_tensor == s.dst_tensor &&
+        p.src_tensor >= 0 && p.src_offset + p.run == s.src_offset && p.dst_offset + p.run == s.dst_offset) {
+      p.run += s.run;
+      p.src_stride = p.dst_stride = p.run;
+      return;
+    }
+  }
+  out.push_back(s);
+}
+
+static int compile(Plan& P, const std::vector<std::vector<Block>>& sb, const std::vector<std::vector<Block>>& db) {
+  const SideInfo& S = P.side[0];
+  const SideInfo& D = P.side[1];
+  const int es = elem_size(S.lay.dtype);
+  const int nlt = 3 + 9 * S.lay.model.num_layers;
+
+  // source blocks per logical tensor; replicated norms are read from TP rank 0 of their stage
+  std::vector<std::vector<SrcRef>> by_lt(nlt);
+  for (size_t i = 0; i < S.tensors.size(); ++i) {
+    const emu_tensor_desc_t& t = S.tensors[i];
+    if (is_norm(t.kind) && t.rank % S.lay.tp != 0) continue;
+    for (const Block& b : sb[i]) by_lt[b.lt].push_back({int32_t(i), b});
+  }
+  for (auto& v : by_lt)
+    std::sort(v.begin(), v.end(), [](const SrcRef& a, const SrcRef& b) {
+      return a.b.lrow0 != b.b.lrow0 ? a.b.lrow0 < b.b.lrow0 : a.b.lcol0 < b.b.lcol0;
+    });
+
+  P.segs.clear();
+  for (size_t j = 0; j < D.tensors.size(); ++j) {
+    const emu_tensor_desc_t& dt = D.tensors[j];
+    int64_t covered_rows = 0;
+    for (const Block& b : db[j]) {
+      for (const SrcRef& sr : by_lt[b.lt]) {
+        const Block& s = sr.b;
+        const int64_t r0 = std::max(b.lrow0, s.lrow0), r1 = std::min(b.lrow0 + b.nrows, s.lrow0 + s.nrows);
+        const int64_t c0 = std::max(b.lcol0, s.lcol0), c1 = std::min(b.lcol0 + b.ncols, s.lcol0 + s.ncols);
+        if (r0 >= r1 || c0 >= c1) continue;
+        const emu_tensor_desc_t& st = S.tensors[sr.tensor];
+        emu_segment_t g{};
+        g.src_tensor = sr.tensor;
+        g.dst_tensor = int32_t(j);
+        g.src_offset = uint64_t((s.row0 + r0 - s.lrow0) * st.cols + (s.col0 + c0 - s.lcol0)) * es;
+        g.dst_offset = uint64_t((b.row0 + r0 - b.lrow0) * dt.cols + (b.col0 + c0 - b.lcol0)) * es;
+        g.src_stride = uint64_t(st.cols) * es;
+        g.dst_stride = uint64_t(dt.cols) * es;
+        g.rows = uint64_t(r1 - r0);
+        g.run = uint64_t(c1 - c0) * es;
+        if (g.rows == 1 || (g.run == g.src_stride && g.run == g.dst_stride)) {
+          g.run *= g.rows;
+          g.rows = 1;
+          g.src_stride = g.dst_stride = g.run;
+        }
+        push_segment(P.segs, g);
+      }
+      covered_rows += b.nrows * (b.ncols == dt.cols ? 1 : 0);
+    }
+    if ((dt.kind == EMU_T_EMBED || dt.kind == EMU_T_LM_HEAD) && covered_rows < dt.rows) {
+      // destination vocabulary pad rows: no source, written with zeros
+      emu_segment_t z{};
+      z.src_tensor = -1;
+      z.dst_tensor = int32_t(j);
+      z.dst_offset = uint64_t(covered_rows) * dt.cols * es;
+      z.run = uint64_t(dt.rows - covered_rows) * dt.cols * es;
+      z.rows = 1;
+      z.src_stride = z.dst_stride = z.run;
+      P.segs.push_back(z);
+    }
+  }
+  return EMU_OK;
+}
+
+// Device segments, tiles and the workspace image.
+static int finalize(Plan& P) {
+  const int U = P.tile_vecs;
+  const uint64_t TV = uint64_t(kThreads) * U;  // vectors per tile
+  const uint64_t TB = TV * 16;                 // bytes per tile
+  P.tile_bytes = TB;
+  P.dsegs.clear();
+  std::vector<uint32_t> tilemap;
+  uint64_t tiles = 0, zero_bytes = 0, written = 0;
+  int64_t nzero = 0;
+  int32_t ngeneral = 0;
+  for (size_t i = 0; i < P.segs.size(); ++i) {
+    const emu_segment_t& g = P.segs[i];
+    DevSeg d{};
+    d.src_off = g.src_offset; d.dst_off = g.dst_offset;
+    d.src_stride = g.src_stride; d.dst_stride = g.dst_stride;
+    d.rows = g.rows; d.run = g.run;
+    d.src_idx = g.src_tensor; d.dst_idx = g.dst_tensor;
+    d.tile0 = tiles;
+    const bool zero = g.src_tensor < 0;
+    const bool vec = ((g.dst_offset | g.run) % 16 == 0) && (g.rows == 1 || g.dst_stride % 16 == 0) &&
+                     (zero || (g.src_offset % 16 == 0 && (g.rows == 1 || g.src_stride % 16 == 0)));
+    uint64_t nt;
+    if (!vec) {
+      d.mode = SEG_GENERAL;
+      const uint64_t tpr = (g.run + TB - 1) / TB;
+      if (tpr > 0xffffffffull) return fail(EMU_ERR_UNSUPPORTED, "row of %llu bytes too long", (unsigned long long)g.run);
+      d.param = uint32_t(tpr);
+      nt = g.rows * tpr;
+      ++ngeneral;
+    } else if (g.rows == 1) {
+      d.mode = SEG_VEC_1D;
+      nt = (g.run + TB - 1) / TB;
+    } else if (g.run <= TB) {
+      d.mode = SEG_VEC_ROWS;
+      d.rv = uint32_t(g.run / 16);
+      d.param = uint32_t(TB / g.run);
+      d.magic = d.rv > 1 ? uint32_t(((1ull << 32) + d.rv - 1) / d.rv) : 0u;
+      nt = (g.rows + d.param - 1) / d.param;
+    } else {
+      d.mode = SEG_VEC_ROWCHUNK;
+      const uint64_t tpr = (g.run + TB - 1) / TB;
+      d.param = uint32_t(tpr);
+      nt = g.rows * tpr;
+    }
+    if (zero) {
+      d.mode |= SEG_ZERO;
+      zero_bytes += g.rows * g.run;
+      ++nzero;
+    }
+    written += g.rows * g.run;
+    if (tiles + nt > 0xffffffffull) return fail(EMU_ERR_UNSUPPORTED, "too many tiles");
+    tilemap.insert(tilemap.end(), nt, uint32_t(i));
+    tiles += nt;
+    P.dsegs.push_back(d);
+  }
+  P.ntiles = tiles;
+  if (written != P.side[1].total_bytes)
+    return fail(EMU_ERR_ARG, "internal: copy map covers %llu of %llu destination bytes",
+                (unsigned long long)written, (unsigned long long)P.side[1].total_bytes);
+
+  // workspace image
+  auto align = [](uint64_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; };
+  WsLayout& w = P.ws;
+  uint64_t off = 0;
+  w.off_segs = off; off = align(off + P.dsegs.size() * sizeof(DevSeg));
+  w.off_tilemap = off; off = align(off + tilemap.size() * 4);
+  for (int sd = 0; sd < 2; ++sd) {
+    const SideInfo& s = P.side[sd];
+    w.side[sd].off_sizes = off; off = align(off + s.tensors.size() * 8);
+    w.side[sd].off_rank_first = off; off = align(off + (s.nranks + 1) * 4);
+    w.side[sd].off_rank_bytes = off; off = align(off + s.nranks * 8);
+    w.side[sd].off_chunk_first = off; off = align(off + (s.nranks + 1) * 8);
+  }
+  w.total = off;
+  P.host_ws.assign(w.total, 0);
+  uint8_t* h = P.host_ws.data();
+  if (!P.dsegs.empty()) std::memcpy(h + w.off_segs, P.dsegs.data(), P.dsegs.size() * sizeof(DevSeg));
+  if (!tilemap.empty()) std::memcpy(h + w.off_tilemap, tilemap.data(), tilemap.size() * 4);
+  for (int sd = 0; sd < 2; ++sd) {
+    const SideInfo& s = P.side[sd];
+    uint64_t* sz = reinterpret_cast<uint64_t*>(h + w.side[sd].off_sizes);
+    for (size_t i = 0; i < s.tensors.size(); ++i) sz[i] = s.tensors[i].bytes;
+    std::memcpy(h + w.side[sd].off_rank_first, s.rank_first.data(), s.rank_first.size() * 4);
+    std::memcpy(h + w.side[sd].off_rank_bytes, s.rank_bytes.data(), s.rank_bytes.size() * 8);
+    std::memcpy(h + w.side[sd].off_chunk_first, s.chunk_first.data(), s.chunk_first.size() * 8);
+  }
+
+  emu_plan_info_t& I = P.info;
+  I = emu_plan_info_t{};
+  I.n_src_ranks = P.side[0].nranks;
+  I.n_dst_ranks = P.side[1].nranks;
+  I.n_src_tensors = int32_t(P.side[0].tensors.size());
+  I.n_dst_tensors = int32_t(P.side[1].tensors.size());
+  I.n_segments = int64_t(P.segs.size());
+  I.n_zero_segments = nzero;
+  I.n_tiles = int64_t(tiles);
+  I.tile_bytes = TB;
+  I.bytes_written = written;
+  I.zero_fill_bytes = zero_bytes;
+  I.bytes_read = written - zero_bytes;
+  I.src_bytes = P.side[0].total_bytes;
+  I.dst_bytes = P.side[1].total_bytes;
+  I.workspace_bytes = w.total;
+  I.src_vocab_padded = int32_t(P.side[0].vp);
+  I.dst_vocab_padded = int32_t(P.side[1].vp);
+  I.n_general_segments = ngeneral;
+  return EMU_OK;
+}
+
+}  // namespace emu
+
+using namespace emu;
+
+// ------------------------------------------------------------------------------------------------
+// C ABI (host part)
+// ------------------------------------------------------------------------------------------------
+
+extern "C" {
+
+int emu_version(void) { return EMU_ABI_VERSION; }
+
+const char* emu_status_str(int s) {
+  switch (s) {
+    case EMU_OK: return "EMU_OK";
+    case EMU_ERR_NULL: return "EMU_ERR_NULL";
+    case EMU_ERR_LAYOUT: return "EMU_ERR_LAYOUT";
+    case EMU_ERR_MISMATCH: return "EMU_ERR_MISMATCH";
+    case EMU_ERR_UNSUPPORTED: return "EMU_ERR_UNSUPPORTED";
+    case EMU_ERR_WORKSPACE: return "EMU_ERR_WORKSPACE";
+    case EMU_ERR_BUCKET: return "EMU_ERR_BUCKET";
+    case EMU_ERR_ALIGN: return "EMU_ERR_ALIGN";
+    case EMU_ERR_HIP: return "EMU_ERR_HIP";
+    case EMU_ERR_HANDLE: return "EMU_ERR_HANDLE";
+    case EMU_ERR_RANGE: return "EMU_ERR_RANGE";
+    case EMU_ERR_ARG: return "EMU_ERR_ARG";
+    default: return "EMU_ERR_UNKNOWN";
+  }
+}
+
+const char* emu_last_error(void) { return g_err; }
+
+int emu_set_option(int32_t key, int64_t value) {
+  clear_error();
+  switch (key) {
+    case EMU_OPT_TILE_VECS:
+      if (value != 4 && value != 8 && value != 16) return fail(EMU_ERR_ARG, "tile vectors must be 4, 8 or 16");
+      break;
+    case EMU_OPT_WG_PER_CU:
+    case EMU_OPT_BUCKET_WG_PER_CU:
+      if (value < 0 || value > 64) return fail(EMU_ERR_ARG, "workgroups per CU must be in [0, 64]");
+      if (key == EMU_OPT_BUCKET_WG_PER_CU && value == 0) return fail(EMU_ERR_ARG, "need at least one workgroup per CU");
+      break;
+    case EMU_OPT_NONTEMPORAL:
+    case EMU_OPT_LDS_STAGING:
+      if (value != 0 && value != 1) return fail(EMU_ERR_ARG, "flag must be 0 or 1");
+      break;
+    default:
+      return fail(EMU_ERR_RANGE, "unknown option %d", key);
+  }
+  g_opt[key].store(value, std::memory_order_relaxed);
+  return EMU_OK;
+}
+
+int emu_get_option(int32_t key, int64_t* value) {
+  clear_error();
+  if (!value) return fail(EMU_ERR_NULL, "value is NULL");
+  if (key < 0 || key > EMU_OPT_BUCKET_WG_PER_CU) return fail(EMU_ERR_RANGE, "unknown option %d", key);
+  *value = option(key);
+  return EMU_OK;
+}
+
+int emu_layout_check(const emu_layout_t* layout) {
+  clear_error();
+  return check_layout(layout);
+}
+
+int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out) {
+  clear_error();
+  if (!src || !dst || !out) return fail(EMU_ERR_NULL, "NULL argument");
+  *out = nullptr;
+  int rc = check_layout(src);
+  if (rc) return rc;
+  rc = check_layout(dst);
+  if (rc) return rc;
+  if (std::memcmp(&src->model, &dst->model, sizeof(emu_model_t)) != 0)
+    return fail(EMU_ERR_MISMATCH, "source and destination layouts describe different models");
+  if (src->dtype != dst->dtype) return fail(EMU_ERR_MISMATCH, "source and destination element types differ");
+  Plan* P = new (std::nothrow) Plan();
+  if (!P) return fail(EMU_ERR_ARG, "out of host memory");
+  try {
+    P->tile_vecs = int(option(EMU_OPT_TILE_VECS));
+    std::vector<std::vector<Block>> sb, db;
+    rc = build_side(*src, P->side[0], sb);
+    if (!rc) rc = build_side(*dst, P->side[1], db);
+    if (!rc) rc = compile(*P, sb, db);
+    if (!rc) rc = finalize(*P);
+  } catch (const std::bad_alloc&) {
+    rc = fail(EMU_ERR_ARG, "out of host memory");
+  }
+  if (rc) {
+    delete P;
+    return rc;
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_plans_mu);
+    g_plans.insert(P);
+  }
+  *out = reinterpret_cast<emu_plan_t>(P);
+  return EMU_OK;
+}
+
+int emu_plan_free(emu_plan_t plan) {
+  clear_error();
+  Plan* P = reinterpret_cast<Plan*>(plan);
+  {
+    std::lock_guard<std::mutex> lk(g_plans_mu);
+    if (!P || !g_plans.count(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
+    g_plans.erase(P);
+  }
+  P->magic = 0;
+  delete P;
+  return EMU_OK;
+}
+
+int emu_plan_info(emu_plan_t plan, emu_plan_info_t* out) {
+  clear_error();
+  const Plan* P = reinterpret_cast<const Plan*>(plan);
+  if (!plan_live(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
+  if (!out) return fail(EMU_ERR_NULL, "out is NULL");
+  *out = P->info;
+  return EMU_OK;
+}
+
+int emu_tensor_info(emu_plan_t plan, int32_t side, int32_t index, emu_tensor_desc_t* out) {
+  clear_error();
+  const Plan* P = reinterpret_cast<const Plan*>(plan);
+  if (!plan_live(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
+  if (!out) return fail(EMU_ERR_NULL, "out is NULL");
+  if (side != 0 && side != 1) return fail(EMU_ERR_RANGE, "side must be 0 (source) or 1 (destination)");
+  const auto& t = P->side[side].tensors;
+  if (index < 0 || size_t(index) >= t.size()) return fail(EMU_ERR_RANGE, "tensor index %d out of range", index);
+  *out = t[index];
+  return EMU_OK;
+}
+
+int emu_plan_segments(emu_plan_t plan, int64_t first, int64_t count, emu_segment_t* out) {
+  clear_error();
+  const Plan* P = reinterpret_cast<const Plan*>(plan);
+  if (!plan_live(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
+  if (count > 0 && !out) return fail(EMU_ERR_NULL, "out is NULL");
+  if (first < 0 || count < 0 || uint64_t(first) + uint64_t(count) > P->segs.size())
+    return fail(EMU_ERR_RANGE, "segment range out of bounds");
+  if (count) std::memcpy(out, P->segs.data() + first, size_t(count) * sizeof(emu_segment_t));
+  return EMU_OK;
+}
+
+int emu_bucket_layout(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, int32_t rank, uint64_t* n_buckets,
+                      uint64_t* stream_bytes) {
+  clear_error();
+  const Plan* P = reinterpret_cast<const Plan*>(plan);
+  if (!plan_live(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
+  if (side != 0 && side != 1) return fail(EMU_ERR_RANGE, "side must be 0 or 1");
+  const SideInfo& s = P->side[side];
+  const uint64_t es = uint64_t(elem_size(s.lay.dtype));
+  if (bucket_bytes == 0 || bucket_bytes % es)
+    return fail(EMU_ERR_BUCKET, "bucket size %llu is not a positive multiple of %llu",
+                (unsigned long long)bucket_bytes, (unsigned long long)es);
+  if (rank < -1 || rank >= s.nranks) return fail(EMU_ERR_RANGE, "rank %d out of range", rank);
+  uint64_t nb = 0, sb = 0;
+  for (int r = (rank < 0 ? 0 : rank); r < (rank < 0 ? s.nranks : rank + 1); ++r) {
+    nb += (s.rank_bytes[r] + bucket_bytes - 1) / bucket_bytes;
+    sb += s.rank_bytes[r];
+  }
+  if (n_buckets) *n_buckets = nb;
+  if (stream_bytes) *stream_bytes = sb;
+  return EMU_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,324 @@
+"""Python binding of libemu.so (the EMU Split/Merge reshard, C ABI in include/emu.h).
+
+Argument marshalling only: every step of the reshard and of bucket pack/unpack runs in the library's
+HIP kernels. PyTorch provides device memory, pointer tables and streams. There is no fallback: if the
+library is not built, :func:`load` raises.
+
+Typical use::
+
+    src = Layout(model, tp=2, pp=2)
+    dst = Layout(model, tp=4, pp=1)
+    plan = Plan(src, dst)
+    ws = plan.workspace()                      # uploads the plan tables to a fresh device buffer
+    S = plan.alloc(0); D = plan.alloc(1)       # one buffer per rank, tensors as views
+    plan.reshard(ws, S.ptrs, D.ptrs)           # enqueued on torch's current stream
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libemu.so")
+
+BF16, FP32 = 0, 1
+QKV_HEAD_INTERLEAVED, QKV_SEPARATE = 0, 1
+GATE_UP_BLOCK, GATE_UP_SEPARATE = 0, 1
+DTYPES = {"bf16": BF16, "fp32": FP32}
+ESIZE = {BF16: 2, FP32: 4}
+
+OPT_TILE_VECS, OPT_WG_PER_CU, OPT_NONTEMPORAL, OPT_LDS_STAGING, OPT_BUCKET_WG_PER_CU = range(5)
+
+KINDS = ["embed", "attn_norm", "qkv", "q", "k", "v", "o", "mlp_norm", "gate_up", "gate", "up", "down",
+         "final_norm", "lm_head"]
+
+STATUS = {0: "EMU_OK", -1: "EMU_ERR_NULL", -2: "EMU_ERR_LAYOUT", -3: "EMU_ERR_MISMATCH",
+          -4: "EMU_ERR_UNSUPPORTED", -5: "EMU_ERR_WORKSPACE", -6: "EMU_ERR_BUCKET", -7: "EMU_ERR_ALIGN",
+          -8: "EMU_ERR_HIP", -9: "EMU_ERR_HANDLE", -10: "EMU_ERR_RANGE", -11: "EMU_ERR_ARG"}
+
+
+class c_model(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("num_layers", "hidden", "num_heads", "num_kv_heads", "head_dim", "ffn_hidden", "vocab")]
+
+
+class c_layout(ctypes.Structure):
+    _fields_ = [("model", c_model)] + [(n, ctypes.c_int32) for n in
+                                       ("tp", "pp", "vocab_pad_multiple", "dtype", "qkv_format", "mlp_format")]
+
+
+class c_plan_info(ctypes.Structure):
+    _fields_ = [("n_src_ranks", ctypes.c_int32), ("n_dst_ranks", ctypes.c_int32),
+                ("n_src_tensors", ctypes.c_int32), ("n_dst_tensors", ctypes.c_int32),
+                ("n_segments", ctypes.c_int64), ("n_zero_segments", ctypes.c_int64),
+                ("n_tiles", ctypes.c_int64), ("tile_bytes", ctypes.c_uint64),
+                ("bytes_read", ctypes.c_uint64), ("bytes_written", ctypes.c_uint64),
+                ("zero_fill_bytes", ctypes.c_uint64), ("src_bytes", ctypes.c_uint64),
+                ("dst_bytes", ctypes.c_uint64), ("workspace_bytes", ctypes.c_uint64),
+                ("src_vocab_padded", ctypes.c_int32), ("dst_vocab_padded", ctypes.c_int32),
+                ("n_general_segments", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class c_tensor_desc(ctypes.Structure):
+    _fields_ = [("rank", ctypes.c_int32), ("kind", ctypes.c_int32), ("layer", ctypes.c_int32),
+                ("ndim", ctypes.c_int32), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
+                ("bytes", ctypes.c_uint64), ("stream_offset", ctypes.c_uint64)]
+
+
+class c_segment(ctypes.Structure):
+    _fields_ = [("src_tensor", ctypes.c_int32), ("dst_tensor", ctypes.c_int32),
+                ("src_offset", ctypes.c_uint64), ("dst_offset", ctypes.c_uint64),
+                ("src_stride", ctypes.c_uint64), ("dst_stride", ctypes.c_uint64),
+                ("rows", ctypes.c_uint64), ("run", ctypes.c_uint64)]
+
+
+class EmuError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{STATUS.get(code, code)}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load libemu.so (once). Raises if it has not been built: there is no other implementation."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2609_34645_amd.build`")
+    lib = ctypes.CDLL(path)
+    P, V, I32, I64, U64 = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
+    sig = {
+        "emu_version": ([], ctypes.c_int),
+        "emu_status_str": ([ctypes.c_int], ctypes.c_char_p),
+        "emu_last_error": ([], ctypes.c_char_p),
+        "emu_set_option": ([I32, I64], ctypes.c_int),
+        "emu_get_option": ([I32, ctypes.POINTER(I64)], ctypes.c_int),
+        "emu_layout_check": ([ctypes.POINTER(c_layout)], ctypes.c_int),
+        "emu_plan": ([ctypes.POINTER(c_layout), ctypes.POINTER(c_layout), ctypes.POINTER(P)], ctypes.c_int),
+        "emu_plan_free": ([P], ctypes.c_int),
+        "emu_plan_info": ([P, ctypes.POINTER(c_plan_info)], ctypes.c_int),
+        "emu_tensor_info": ([P, I32, I32, ctypes.POINTER(c_tensor_desc)], ctypes.c_int),
+        "emu_plan_segments": ([P, I64, I64, ctypes.POINTER(c_segment)], ctypes.c_int),
+        "emu_plan_upload": ([P, V, U64, V], ctypes.c_int),
+        "emu_reshard": ([P, V, V, V, V], ctypes.c_int),
+        "emu_bucket_layout": ([P, I32, U64, I32, ctypes.POINTER(U64), ctypes.POINTER(U64)], ctypes.c_int),
+        "emu_pack_buckets": ([P, V, I32, U64, V, V, V], ctypes.c_int),
+        "emu_unpack_buckets": ([P, V, I32, U64, V, V, V], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    _lib = lib
+    return lib
+
+
+def check(rc: int) -> None:
+    if rc != 0:
+        raise EmuError(rc, load().emu_last_error().decode())
+
+
+def set_option(key: int, value: int) -> None:
+    check(load().emu_set_option(key, value))
+
+
+def get_option(key: int) -> int:
+    v = ctypes.c_int64()
+    check(load().emu_get_option(key, ctypes.byref(v)))
+    return v.value
+
+
+@dataclass(frozen=True)
+class Model:
+    num_layers: int
+    hidden: int
+    num_heads: int
+    head_dim: int
+    num_kv_heads: int
+    ffn_hidden: int
+    vocab: int
+
+    @classmethod
+    def from_tuple(cls, t):
+        """(L, H, nH, hd, G, I, V)."""
+        return cls(*t)
+
+
+@dataclass(frozen=True)
+class Layout:
+    model: Model
+    tp: int
+    pp: int
+    pad: int = 0
+    dtype: str = "bf16"
+    qkv: str = "interleaved"
+    mlp: str = "block"
+
+    def c(self) -> c_layout:
+        m = self.model
+        return c_layout(c_model(m.num_layers, m.hidden, m.num_heads, m.num_kv_heads, m.head_dim, m.ffn_hidden,
+                                m.vocab), self.tp, self.pp, self.pad, DTYPES[self.dtype],
+                        QKV_HEAD_INTERLEAVED if self.qkv == "interleaved" else QKV_SEPARATE,
+                        GATE_UP_BLOCK if self.mlp == "block" else GATE_UP_SEPARATE)
+
+
+def layout_check(lay: Layout) -> int:
+    c = lay.c()
+    return load().emu_layout_check(ctypes.byref(c))
+
+
+def _stream_handle(stream):
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+class ShardSet:
+    """One side's tensors on the device: one uint8 buffer per rank, tensors as 256-byte aligned views.
+
+    ``ptrs`` is the device pointer table (int64) in global tensor order; ``tensors[i]`` is a uint8 view
+    of tensor i's bytes.
+    """
+
+    def __init__(self, bufs, tensors, ptrs):
+        self.bufs = bufs
+        self.tensors = tensors
+        self.ptrs = ptrs
+
+
+class Plan:
+    """A compiled copy map between two layouts (``emu_plan``)."""
+
+    def __init__(self, src: Layout, dst: Layout):
+        lib = load()
+        self.src, self.dst = src, dst
+        cs, cd = src.c(), dst.c()
+        h = ctypes.c_void_p()
+        check(lib.emu_plan(ctypes.byref(cs), ctypes.byref(cd), ctypes.byref(h)))
+        self._h = h
+        info = c_plan_info()
+        check(lib.emu_plan_info(h, ctypes.byref(info)))
+        self.info = {f: getattr(info, f) for f, _ in c_plan_info._fields_}
+        self._descs = [None, None]
+
+    # -- host queries ------------------------------------------------------------------------
+    def tensors(self, side: int) -> list:
+        """Per tensor of one side (0 = source, 1 = destination): dict(rank, kind, layer, shape, bytes,
+        stream_offset)."""
+        if self._descs[side] is None:
+            lib = load()
+            n = self.info["n_src_tensors" if side == 0 else "n_dst_tensors"]
+            out = []
+            d = c_tensor_desc()
+            for i in range(n):
+                check(lib.emu_tensor_info(self._h, side, i, ctypes.byref(d)))
+                shape = (d.cols,) if d.ndim == 1 else (d.rows, d.cols)
+                out.append(dict(rank=d.rank, kind=KINDS[d.kind], layer=d.layer, shape=shape, bytes=d.bytes,
+                                stream_offset=d.stream_offset))
+            self._descs[side] = out
+        return self._descs[side]
+
+    def segments(self) -> list:
+        n = self.info["n_segments"]
+        arr = (c_segment * max(1, n))()
+        check(load().emu_plan_segments(self._h, 0, n, arr))
+        return [{f: getattr(arr[i], f) for f, _ in c_segment._fields_} for i in range(n)]
+
+    def bucket_layout(self, side: int, bucket_bytes: int, rank: int = -1):
+        nb, sb = ctypes.c_uint64(), ctypes.c_uint64()
+        check(load().emu_bucket_layout(self._h, side, bucket_bytes, rank, ctypes.byref(nb), ctypes.byref(sb)))
+        return nb.value, sb.value
+
+    # -- device helpers (plumbing) -------------------------------------------------------------
+    def workspace(self, device=None, stream=None):
+        """Allocate a workspace tensor and enqueue the plan upload into it."""
+        import torch
+
+        n = self.info["workspace_bytes"]
+        ws = torch.empty(max(n, 256), dtype=torch.uint8, device=device or "cuda")
+        self.upload(ws, stream)
+        return ws
+
+    def upload(self, ws, stream=None):
+        check(load().emu_plan_upload(self._h, ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream_handle(stream)))
+
+    def alloc(self, side: int, device=None, fill=None) -> ShardSet:
+        """Allocate one side's shard set (one buffer per rank, 256-byte aligned tensor views)."""
+        import torch
+
+        descs = self.tensors(side)
+        nranks = self.info["n_src_ranks" if side == 0 else "n_dst_ranks"]
+        offs, sizes = [], [0] * nranks
+        for d in descs:
+            o = (sizes[d["rank"]] + 255) // 256 * 256
+            offs.append(o)
+            sizes[d["rank"]] = o + d["bytes"]
+        bufs = [torch.empty(max(s, 16), dtype=torch.uint8, device=device or "cuda") for s in sizes]
+        if fill is not None:
+            for b in bufs:
+                b.fill_(fill)
+        tensors = [bufs[d["rank"]][o:o + d["bytes"]] for d, o in zip(descs, offs)]
+        return ShardSet(bufs, tensors, ptr_table(tensors, device))
+
+    def alloc_buckets(self, side: int, bucket_bytes: int, device=None, fill=None):
+        """Bucket buffers for one side (rank 0's first) and their pointer table. The buckets are
+        256-byte aligned views of one backing allocation."""
+        import torch
+
+        nranks = self.info["n_src_ranks" if side == 0 else "n_dst_ranks"]
+        sizes = []
+        for r in range(nranks):
+            nb, sb = self.bucket_layout(side, bucket_bytes, r)
+            sizes += [min(bucket_bytes, sb - k * bucket_bytes) for k in range(nb)]
+        offs, total = [], 0
+        for n in sizes:
+            offs.append(total)
+            total = (total + n + 255) // 256 * 256
+        backing = torch.empty(max(total, 256), dtype=torch.uint8, device=device or "cuda")
+        if fill is not None:
+            backing.fill_(fill)
+        bufs = [backing[o:o + n] for o, n in zip(offs, sizes)]
+        return bufs, ptr_table(bufs, device)
+
+    # -- execution -----------------------------------------------------------------------------
+    def reshard(self, ws, src_ptrs, dst_ptrs, stream=None):
+        check(load().emu_reshard(self._h, ctypes.c_void_p(ws.data_ptr()), ctypes.c_void_p(src_ptrs.data_ptr()),
+                                 ctypes.c_void_p(dst_ptrs.data_ptr()), _stream_handle(stream)))
+
+    def pack(self, ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs, stream=None):
+        check(load().emu_pack_buckets(self._h, ctypes.c_void_p(ws.data_ptr()), side, bucket_bytes,
+                                      ctypes.c_void_p(tensor_ptrs.data_ptr()), ctypes.c_void_p(bucket_ptrs.data_ptr()),
+                                      _stream_handle(stream)))
+
+    def unpack(self, ws, side, bucket_bytes, bucket_ptrs, tensor_ptrs, stream=None):
+        check(load().emu_unpack_buckets(self._h, ctypes.c_void_p(ws.data_ptr()), side, bucket_bytes,
+                                        ctypes.c_void_p(bucket_ptrs.data_ptr()), ctypes.c_void_p(tensor_ptrs.data_ptr()),
+                                        _stream_handle(stream)))
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and _lib is not None:
+            check(_lib.emu_plan_free(self._h))
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def ptr_table(tensors, device=None):
+    """Device int64 table of the tensors' addresses; every address must be 16-byte aligned."""
+    import torch
+
+    addrs = [t.data_ptr() for t in tensors]
+    bad = [i for i, a in enumerate(addrs) if a % 16]
+    if bad:
+        raise EmuError(-7, f"tensors {bad[:4]} are not 16-byte aligned")
+    return torch.tensor(addrs, dtype=torch.int64, device=device or "cuda")

@@ -1,0 +1,213 @@
+"""GPU parity at full benchmark sizes, in the launch configuration the benchmark times.
+
+* 1B-class decoder, TP4 PP1 -> TP2 PP1 (bf16): every byte against the oracle.
+* 8B decoder, TP2 PP2 -> TP4 PP1 (bf16, 16 GB each side): every byte against the oracle, streamed per
+  tensor group; then the reverse transition checked as a round trip on the device.
+* 8B, padded vocabulary, TP8 PP4 -> TP2 PP2, packed into 2^28-byte buckets (mid-row bucket boundaries)
+  and unpacked on the receiver side: reshard, bucket bytes and unpacked tensors against the oracle;
+  again with 2^28 - 2 byte buckets, which put tensor and bucket bytes at different 16-byte phases.
+* 8B training state, fp32 master + Adam m + v (96 GB in): TP4 PP1 -> TP1 PP1, one launch per tensor
+  group, then split back into the source buffers; master checked in full against the oracle, m and v on
+  sampled tensor groups, the back transition against a seeded regeneration of the original state.
+
+Inputs are seeded device draws (synthetic.device_fill); the oracle reads them back as its input.
+"""
+import gc
+import time
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_34645_amd import emu
+from tests.gpu_util import check_reshard, fill_device, host_view, o_layout, say
+from tests.shapes import EIGHT_B, ONE_B
+
+pytestmark = pytest.mark.gpu
+
+
+def free_gb():
+    import torch
+
+    return torch.cuda.mem_get_info()[0] / 1e9
+
+
+def cleanup():
+    import torch
+
+    gc.collect()
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def make_consistent_replicas(plan, side, sset):
+    """Copy each norm's TP-rank-0 replica over the other TP ranks' replicas (a consistent EMU state)."""
+    descs = plan.tensors(side)
+    lay = plan.src if side == 0 else plan.dst
+    first = {}
+    for i, d in enumerate(descs):
+        if d["kind"].endswith("norm") and d["rank"] % lay.tp == 0:
+            first[(d["rank"] // lay.tp, d["kind"], d["layer"])] = i
+    for i, d in enumerate(descs):
+        if d["kind"].endswith("norm") and d["rank"] % lay.tp:
+            sset.tensors[i].copy_(sset.tensors[first[(d["rank"] // lay.tp, d["kind"], d["layer"])]])
+
+
+def test_1b_tp4_to_tp2(gpu_lib):
+    import torch
+
+    m = emu.Model(*ONE_B)
+    p = emu.Plan(emu.Layout(m, 4, 1), emu.Layout(m, 2, 1))
+    assert p.info["bytes_read"] == 2_997_100_544
+    ws = p.workspace()
+    S = p.alloc(0)
+    fill_device(p, 0, S, seed=21)
+    D = p.alloc(1, fill=0xA5)
+    p.reshard(ws, S.ptrs, D.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(p, S, D, label="1B TP4PP1->TP2PP1")
+    del S, D, ws
+    cleanup()
+
+
+def test_8b_tp2pp2_to_tp4pp1(gpu_lib):
+    import torch
+
+    m = emu.Model(*EIGHT_B)
+    src, dst = emu.Layout(m, 2, 2), emu.Layout(m, 4, 1)
+    p, back = emu.Plan(src, dst), emu.Plan(dst, src)
+    assert p.info["bytes_read"] == 16_062_119_936
+    ws, wb = p.workspace(), back.workspace()
+    S = p.alloc(0)
+    fill_device(p, 0, S, seed=1234)
+    D = p.alloc(1, fill=0xA5)
+    t = time.time()
+    p.reshard(ws, S.ptrs, D.ptrs)
+    torch.cuda.synchronize()
+    say(f"  8B reshard done in {time.time() - t:.3f} s (incl. launch)")
+    check_reshard(p, S, D, label="8B TP2PP2->TP4PP1")
+    # Merge back: the round trip reproduces the source; norm replicas of TP rank 1 come back as rank 0's
+    A2 = back.alloc(1, fill=0x5A)
+    back.reshard(wb, D.ptrs, A2.ptrs)
+    torch.cuda.synchronize()
+    make_consistent_replicas(p, 0, S)
+    for i, (x, y) in enumerate(zip(S.tensors, A2.tensors)):
+        assert torch.equal(x, y), f"round trip differs in source tensor {i}"
+    del S, D, A2, ws, wb
+    cleanup()
+
+
+def _pack_check(p, ws, D, B, label):
+    """Pack D at bucket size B, compare every bucket with oracle.pack of the (oracle-verified) destination
+    tensors rank by rank, unpack into a receiver set and compare it with D."""
+    import torch
+
+    bufs, bptrs = p.alloc_buckets(1, B, fill=0x77)
+    p.pack(ws, 1, B, D.ptrs, bptrs)
+    torch.cuda.synchronize()
+    dd = p.tensors(1)
+    k = 0
+    t = time.time()
+    for r in range(p.info["n_dst_ranks"]):
+        tensors = [host_view(D.tensors[i], d, p.dst.dtype) for i, d in enumerate(dd) if d["rank"] == r]
+        for w in oracle.pack(tensors, B):
+            got = bufs[k].cpu().numpy()
+            assert got.size == w.size and np.array_equal(got, w), f"{label}: bucket {k} of rank {r} differs"
+            k += 1
+        del tensors
+    assert k == len(bufs)
+    say(f"  {label}: {k} buckets checked against the oracle in {time.time() - t:.1f} s")
+    R = p.alloc(1, fill=0x11)
+    p.unpack(ws, 1, B, bptrs, R.ptrs)
+    torch.cuda.synchronize()
+    for i, (x, y) in enumerate(zip(D.tensors, R.tensors)):
+        assert torch.equal(x, y), f"{label}: unpacked tensor {i} differs"
+    del R, bufs, bptrs
+    cleanup()
+
+
+def test_8b_padded_tp8pp4_to_tp2pp2_buckets(gpu_lib):
+    import torch
+
+    m = emu.Model(*EIGHT_B)
+    p = emu.Plan(emu.Layout(m, 8, 4, 128), emu.Layout(m, 2, 2, 128))
+    assert p.info["src_vocab_padded"] == 129024 and p.info["dst_vocab_padded"] == 128256
+    assert p.bucket_layout(1, 1 << 28, -1) == (60, 16_061_054_976)
+    ws = p.workspace()
+    S = p.alloc(0)
+    fill_device(p, 0, S, seed=55)    # source pad rows hold random values: they must never be read
+    D = p.alloc(1, fill=0xA5)
+    p.reshard(ws, S.ptrs, D.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(p, S, D, label="8B TP8PP4(pad)->TP2PP2")
+    del S
+    cleanup()
+    _pack_check(p, ws, D, 1 << 28, "buckets 2^28")
+    _pack_check(p, ws, D, (1 << 28) - 2, "buckets 2^28-2 (phase-shifted)")
+    del D, ws
+    cleanup()
+
+
+@pytest.fixture(scope="module")
+def train_state(gpu_lib):
+    """fp32 master, Adam m and v in the TP4 PP1 layout, resharded to TP1 PP1 with one launch per group."""
+    import torch
+
+    need = 2 * 96.4 + 33
+    if free_gb() < need:
+        pytest.skip(f"needs {need:.0f} GB of free device memory, {free_gb():.0f} GB free")
+    m = emu.Model(*EIGHT_B)
+    a, b = emu.Layout(m, 4, 1, 0, "fp32"), emu.Layout(m, 1, 1, 0, "fp32")
+    fwd, back = emu.Plan(a, b), emu.Plan(b, a)
+    wf, wb = fwd.workspace(), back.workspace()
+    groups = {"master": ("weight", 301), "adam_m": ("adam_m", 302), "adam_v": ("adam_v", 303)}
+    S, D = {}, {}
+    t = time.time()
+    for name, (dist, seed) in groups.items():
+        S[name] = fwd.alloc(0)
+        fill_device(fwd, 0, S[name], seed=seed, dtype="fp32",
+                    dist_override=None if name == "master" else dist)
+        make_consistent_replicas(fwd, 0, S[name])
+        D[name] = fwd.alloc(1, fill=0xA5)
+    torch.cuda.synchronize()
+    say(f"  fp32 state filled ({3 * fwd.info['src_bytes'] / 1e9:.1f} GB) in {time.time() - t:.1f} s")
+    for name in groups:
+        fwd.reshard(wf, S[name].ptrs, D[name].ptrs)     # one launch per tensor group
+    torch.cuda.synchronize()
+    yield dict(fwd=fwd, back=back, wf=wf, wb=wb, S=S, D=D, groups=groups)
+    S.clear()
+    D.clear()
+    cleanup()
+
+
+def test_8b_fp32_master_full(train_state):
+    st = train_state
+    assert st["fwd"].info["bytes_read"] * 3 == 96_363_134_976
+    check_reshard(st["fwd"], st["S"]["master"], st["D"]["master"], label="fp32 master TP4->TP1")
+
+
+def test_8b_fp32_adam_sampled_groups(train_state):
+    st = train_state
+    for name in ("adam_m", "adam_v"):
+        check_reshard(st["fwd"], st["S"][name], st["D"][name], groups=["embed", 0, 17, 31, "final"],
+                      label=f"fp32 {name} TP4->TP1 (sampled groups)")
+
+
+def test_8b_fp32_split_back_in_place(train_state):
+    import torch
+
+    st = train_state
+    fwd, back = st["fwd"], st["back"]
+    assert back.info["bytes_read"] * 3 == 96_372_719_616
+    for name in st["groups"]:
+        back.reshard(st["wb"], st["D"][name].ptrs, st["S"][name].ptrs)   # into the original source buffers
+    torch.cuda.synchronize()
+    for name, (dist, seed) in st["groups"].items():
+        ref = fwd.alloc(0)
+        fill_device(fwd, 0, ref, seed=seed, dtype="fp32", dist_override=None if name == "master" else dist)
+        make_consistent_replicas(fwd, 0, ref)
+        for i, (x, y) in enumerate(zip(ref.tensors, st["S"][name].tensors)):
+            assert torch.equal(x, y), f"{name}: tensor {i} differs after the round trip"
+        del ref
+        cleanup()
+    say("  fp32 training state round trip TP4->TP1->TP4 bit-exact")

@@ -1,0 +1,216 @@
+"""GPU parity on small models: every output byte compared with the oracle on the same seeded inputs.
+
+Covers the micro models (which also exercise the byte-granular path: 8-byte o/down runs at TP4),
+the tiny 2-layer decoder's Split TP1 PP1 -> TP2 PP1 and Merge back, format changes, padded vocabularies
+with zero-filled destination pad rows, every launch option, and bucket pack/unpack at awkward bucket
+sizes (including sizes that put source and bucket bytes at different 16-byte phases).
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_34645_amd import emu
+from tests.gpu_util import (check_buckets, check_reshard, full_model, host_view, o_layout, say, upload_shards)
+from tests.shapes import MICRO, MICRO8, TINY
+
+pytestmark = pytest.mark.gpu
+
+FORMATS = [("interleaved", "block"), ("separate", "separate"), ("interleaved", "separate")]
+
+
+def run_pair(src, dst, seed=5, options=None, bucket_sizes=()):
+    import torch
+
+    for k, v in (options or {}).items():
+        emu.set_option(k, v)
+    plan = emu.Plan(src, dst)
+    os_ = o_layout(src)
+    ws = plan.workspace()
+    S = plan.alloc(0, fill=0x5A)
+    D = plan.alloc(1, fill=0xA5)
+    upload_shards(oracle.shard(full_model(os_.model, seed, src.dtype), os_), S, tp=src.tp)
+    plan.reshard(ws, S.ptrs, D.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(plan, S, D, label=f"{src.tp}x{src.pp}->{dst.tp}x{dst.pp}")
+    for B in bucket_sizes:
+        bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77)
+        plan.pack(ws, 1, B, D.ptrs, bptrs)
+        R = plan.alloc(1, fill=0x11)
+        plan.unpack(ws, 1, B, bptrs, R.ptrs)
+        torch.cuda.synchronize()
+        dd = plan.tensors(1)
+        ranks = {}
+        for i, d in enumerate(dd):
+            ranks.setdefault(d["rank"], []).append(host_view(D.tensors[i], d, dst.dtype))
+        check_buckets(plan, 1, B, [ranks[r] for r in sorted(ranks)], bufs, label=f"B={B}")
+        for a, b in zip(D.tensors, R.tensors):
+            assert torch.equal(a, b)
+    return plan
+
+
+def micro_pairs(shape, dtype):
+    m = emu.Model(*shape)
+    lays = [emu.Layout(m, tp, pp, pad, dtype, q, g) for tp, pp, pad, (q, g) in
+            itertools.product((1, 2, 4), (1, 2, 4), (0, 2), FORMATS)]
+    return lays
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_micro_pairs(gpu_lib, dtype):
+    lays = micro_pairs(MICRO, dtype)
+    n = 0
+    for i, src in enumerate(lays):
+        for dst in lays[i % 5::5]:
+            run_pair(src, dst, seed=i)
+            n += 1
+    say(f"  {n} micro layout pairs bit-exact ({dtype})")
+
+
+def test_micro_general_path_is_exercised(gpu_lib):
+    m = emu.Model(*MICRO)
+    plan = emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 4, 1))
+    assert plan.info["n_general_segments"] > 0
+
+
+def test_t_sub_paper_example_micro8(gpu_lib):
+    """Section 6.1: (TP4, PP8) split to (TP4, PP2) units, merged into (TP8, PP2): two launches through the
+    intermediate layout give the direct result, on the GPU."""
+    import torch
+
+    m = emu.Model(*MICRO8)
+    a, b, c = emu.Layout(m, 4, 8), emu.Layout(m, 4, 2), emu.Layout(m, 8, 2)
+    pab, pbc, pac = emu.Plan(a, b), emu.Plan(b, c), emu.Plan(a, c)
+    wab, wbc, wac = pab.workspace(), pbc.workspace(), pac.workspace()
+    A = pab.alloc(0)
+    upload_shards(oracle.shard(full_model(o_layout(a).model, 3), o_layout(a)), A, tp=4)
+    B, C1, C2 = pab.alloc(1), pbc.alloc(1), pac.alloc(1)
+    pab.reshard(wab, A.ptrs, B.ptrs)
+    pbc.reshard(wbc, B.ptrs, C1.ptrs)
+    pac.reshard(wac, A.ptrs, C2.ptrs)
+    torch.cuda.synchronize()
+    for x, y in zip(C1.tensors, C2.tensors):
+        assert torch.equal(x, y)
+    check_reshard(pac, A, C2, label="TP4PP8->TP8PP2")
+
+
+def test_tiny_split_and_merge_back(gpu_lib):
+    """The tiny decoder: Split TP1 PP1 -> TP2 PP1, then Merge back; the round trip is the identity."""
+    import torch
+
+    m = emu.Model(*TINY)
+    a, b = emu.Layout(m, 1, 1), emu.Layout(m, 2, 1)
+    fwd, back = emu.Plan(a, b), emu.Plan(b, a)
+    assert fwd.info["bytes_read"] == 3_953_664 and back.info["bytes_read"] == 3_951_104
+    wf, wb = fwd.workspace(), back.workspace()
+    A = fwd.alloc(0)
+    upload_shards(oracle.shard(full_model(o_layout(a).model, 1), o_layout(a)), A)
+    B, A2 = fwd.alloc(1, fill=0xA5), back.alloc(1, fill=0xA5)
+    fwd.reshard(wf, A.ptrs, B.ptrs)
+    back.reshard(wb, B.ptrs, A2.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(fwd, A, B, label="tiny TP1->TP2")
+    check_reshard(back, B, A2, label="tiny TP2->TP1")
+    for x, y in zip(A.tensors, A2.tensors):
+        assert torch.equal(x, y)
+
+
+@pytest.mark.parametrize("opts", [
+    {emu.OPT_TILE_VECS: 4}, {emu.OPT_TILE_VECS: 16}, {emu.OPT_WG_PER_CU: 2},
+    {emu.OPT_NONTEMPORAL: 0}, {emu.OPT_LDS_STAGING: 1}, {emu.OPT_LDS_STAGING: 1, emu.OPT_TILE_VECS: 16},
+])
+def test_launch_options(gpu_lib, opts):
+    defaults = {k: emu.get_option(k) for k in range(5)}
+    try:
+        m = emu.Model(*TINY)
+        run_pair(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate"), options=opts)
+        mm = emu.Model(*MICRO)
+        run_pair(emu.Layout(mm, 1, 2), emu.Layout(mm, 4, 1, 2), options=opts)
+    finally:
+        for k, v in defaults.items():
+            emu.set_option(k, v)
+
+
+def test_padded_vocab_zero_fill_and_source_pad_not_read(gpu_lib):
+    """Reverse of the padded case: destination pad rows are zeros although the destination buffer was
+    prefilled with a sentinel; source pad rows (filled with garbage) never reach the destination."""
+    import torch
+
+    m = emu.Model(2, 256, 4, 64, 2, 688, 1000)
+    a, b = emu.Layout(m, 2, 1, 0), emu.Layout(m, 2, 2, 128)
+    p = emu.Plan(a, b)
+    assert p.info["zero_fill_bytes"] == 2 * 24 * 256 * 2
+    ws = p.workspace()
+    S = p.alloc(0)
+    upload_shards(oracle.shard(full_model(o_layout(a).model, 9), o_layout(a)), S, tp=2)
+    D = p.alloc(1, fill=0xA5)
+    p.reshard(ws, S.ptrs, D.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(p, S, D, label="pad 0 -> pad 128")
+    back = emu.Plan(b, a)
+    wb = back.workspace()
+    for t, d in zip(D.tensors, back.tensors(0)):
+        if d["kind"] in ("embed", "lm_head") and d["rank"] % 2 == 1:
+            t.view(-1)[-24 * 256 * 2:] = 0xEE      # garbage in the source pad rows
+    A2 = back.alloc(1, fill=0xA5)
+    back.reshard(wb, D.ptrs, A2.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(back, D, A2, label="pad 128 -> pad 0")
+    for x, y, d in zip(S.tensors, A2.tensors, p.tensors(0)):
+        if not (d["kind"].endswith("norm") and d["rank"] % 2):   # TP-rank-1 replicas were altered on upload
+            assert torch.equal(x, y)
+
+
+@pytest.mark.parametrize("B", [30, 1000, 4094, 65536, 65538, 1 << 20])
+def test_buckets_awkward_sizes(gpu_lib, B):
+    m = emu.Model(*TINY)
+    run_pair(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1), bucket_sizes=(B,))
+
+
+def test_buckets_source_side_and_fp32(gpu_lib):
+    import torch
+
+    m = emu.Model(*TINY)
+    a, b = emu.Layout(m, 2, 2, 0, "fp32"), emu.Layout(m, 1, 1, 0, "fp32")
+    p = emu.Plan(a, b)
+    ws = p.workspace()
+    S = p.alloc(0)
+    upload_shards(oracle.shard(full_model(o_layout(a).model, 4, "fp32"), o_layout(a)), S, tp=2)
+    for B in (4, 1 << 16, 12345 * 4):
+        bufs, bptrs = p.alloc_buckets(0, B)
+        p.pack(ws, 0, B, S.ptrs, bptrs)
+        R = p.alloc(0, fill=0)
+        p.unpack(ws, 0, B, bptrs, R.ptrs)
+        torch.cuda.synchronize()
+        sd = p.tensors(0)
+        ranks = {}
+        for i, d in enumerate(sd):
+            ranks.setdefault(d["rank"], []).append(host_view(S.tensors[i], d, "fp32"))
+        check_buckets(p, 0, B, [ranks[r] for r in sorted(ranks)], bufs, label=f"src side B={B}")
+        for x, y in zip(S.tensors, R.tensors):
+            assert torch.equal(x, y)
+
+
+def test_execute_errors(gpu_lib):
+    import torch
+
+    m = emu.Model(*TINY)
+    p = emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1))
+    ws = p.workspace()
+    S, D = p.alloc(0), p.alloc(1)
+    small = torch.empty(256, dtype=torch.uint8, device="cuda")
+    with pytest.raises(emu.EmuError) as e:
+        p.upload(small)
+    assert e.value.code == -5
+    off = torch.empty(p.info["workspace_bytes"] + 512, dtype=torch.uint8, device="cuda")[16:]
+    with pytest.raises(emu.EmuError) as e:
+        p.reshard(off, S.ptrs, D.ptrs)
+    assert e.value.code == -5
+    with pytest.raises(emu.EmuError) as e:
+        p.pack(ws, 1, 3, D.ptrs, D.ptrs)
+    assert e.value.code == -6
+    with pytest.raises(emu.EmuError) as e:
+        emu.ptr_table([S.bufs[0][1:]])
+    assert e.value.code == -7
+    torch.cuda.synchronize()

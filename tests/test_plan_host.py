@@ -1,0 +1,215 @@
+"""Host-side checks of libemu.so (no GPU needed): symbols, plan compiler, bucket geometry, errors.
+
+The plan compiler is checked against the oracle through a test-only interpreter of its segment
+table (tests/plan_interp.py) and for exact cover: every destination byte written exactly once.
+"""
+import ctypes
+import itertools
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_34645_amd import emu
+from synthetic import host_tensor
+from tests.plan_interp import coverage, run_plan
+from tests.shapes import EIGHT_B, MICRO, MICRO8, ONE_B, TINY
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FMT = {("interleaved", "block"), ("separate", "separate"), ("interleaved", "separate"), ("separate", "block")}
+
+
+def o_layout(lay):
+    m = lay.model
+    om = oracle.Model(m.num_layers, m.hidden, m.num_heads, m.head_dim, m.num_kv_heads, m.ffn_hidden, m.vocab)
+    return oracle.Layout(om, lay.tp, lay.pp, lay.pad, lay.dtype, lay.qkv, lay.mlp)
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "emu.h")).read()
+    return sorted(set(re.findall(r"^(?:int|void|const char\*)\s+(emu_\w+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_function():
+    lib = emu.load()
+    names = header_functions()
+    assert len(names) >= 14
+    for n in names:
+        assert hasattr(lib, n), n
+    assert lib.emu_version() == 1
+
+
+def full_model(model, seed=11, dtype="bf16"):
+    full = {}
+    for i, (_, key, shape, kind) in enumerate(oracle.logical_tensors(model)):
+        full[key] = host_tensor(seed, (1, i), shape, "norm" if kind.endswith("norm") else "weight", dtype)
+    return full
+
+
+def check_pair(src, dst, full=None, seed=11):
+    plan = emu.Plan(src, dst)
+    os_, od = o_layout(src), o_layout(dst)
+    # tensor inventory matches the oracle's
+    for side, ol in ((0, os_), (1, od)):
+        descs = plan.tensors(side)
+        inv = [s for specs in oracle.rank_inventory(ol) for s in specs]
+        assert [(d["kind"], d["layer"], tuple(d["shape"])) for d in descs] == \
+            [(s.kind, s.layer, tuple(s.shape)) for s in inv]
+    if full is None:
+        full = full_model(os_.model, seed, src.dtype)
+    src_shards = oracle.shard(full, os_)
+    # replicas on TP ranks > 0 get different values: the plan must read TP rank 0
+    for r, specs in enumerate(oracle.rank_inventory(os_)):
+        for j, s in enumerate(specs):
+            if s.kind.endswith("norm") and r % os_.tp:
+                src_shards[r][j] = src_shards[r][j] ^ np.array(0x5A5A, dtype=src_shards[r][j].dtype) \
+                    if src_shards[r][j].dtype == np.uint16 else src_shards[r][j] * 3
+    flat_src = [np.ascontiguousarray(a).reshape(-1).view(np.uint8) for rank in src_shards for a in rank]
+    want = [np.ascontiguousarray(a).reshape(-1).view(np.uint8) for rank in oracle.reshard(src_shards, os_, od)
+            for a in rank]
+    got = run_plan(plan.segments(), flat_src, [w.size for w in want])
+    for j, (g, w) in enumerate(zip(got, want)):
+        assert np.array_equal(g, w), (src, dst, j)
+    info = plan.info
+    assert info["bytes_written"] == sum(w.size for w in want)
+    return plan
+
+
+def micro_layouts(shape=MICRO):
+    m = emu.Model(*shape)
+    return [emu.Layout(m, tp, pp, pad, "bf16", q, g)
+            for tp, pp, pad, (q, g) in itertools.product((1, 2, 4), (1, 2, 4), (0, 2), sorted(FMT))]
+
+
+MICRO_LAYS = micro_layouts()
+
+
+@pytest.mark.parametrize("i", range(0, len(MICRO_LAYS), 3))
+def test_plan_interpreter_matches_oracle_micro(i):
+    src = MICRO_LAYS[i]
+    full = full_model(o_layout(src).model)
+    for dst in MICRO_LAYS[::2] + MICRO_LAYS[1::7]:
+        check_pair(src, dst, full)
+
+
+def test_plan_interpreter_matches_oracle_tiny_config():
+    m = emu.Model(*TINY)
+    a, b = emu.Layout(m, 1, 1), emu.Layout(m, 2, 1)
+    check_pair(a, b)
+    check_pair(b, a)
+    check_pair(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate"))
+
+
+def test_plan_interpreter_fp32_micro8_t_sub():
+    m = emu.Model(*MICRO8)
+    for pad in (0, 2):
+        check_pair(emu.Layout(m, 4, 8, pad, "fp32"), emu.Layout(m, 8, 2, pad, "fp32"))
+        check_pair(emu.Layout(m, 4, 8, pad, "fp32"), emu.Layout(m, 4, 2, pad, "fp32"))
+
+
+def test_interrupted_plan_never_writes_the_source():
+    """A transition stopped partway loses no state (section 6.2, safe concurrent execution): running
+    any prefix of the copy map reads the source only."""
+    m = emu.Model(*TINY)
+    src, dst = emu.Layout(m, 2, 1), emu.Layout(m, 1, 1)
+    plan = emu.Plan(src, dst)
+    segs = plan.segments()
+    os_ = o_layout(src)
+    flat = [np.ascontiguousarray(a).reshape(-1).view(np.uint8) for rank in oracle.shard(full_model(os_.model), os_)
+            for a in rank]
+    before = [x.copy() for x in flat]
+    sizes = [d["bytes"] for d in plan.tensors(1)]
+    for k in (0, 1, len(segs) // 2, len(segs)):
+        run_plan(segs, flat, sizes, prefix=k)
+        assert all(np.array_equal(a, b) for a, b in zip(before, flat))
+
+
+def exact_cover(plan):
+    sizes = [d["bytes"] for d in plan.tensors(1)]
+    for n, iv in zip(sizes, coverage(plan.segments(), sizes)):
+        pos = 0
+        for a, b in iv:
+            assert a == pos, "gap or overlap in destination coverage"
+            pos = b
+        assert pos == n
+
+
+@pytest.mark.parametrize("src,dst,read", [
+    ((ONE_B, 4, 1, 0), (ONE_B, 2, 1, 0), 2_997_100_544),
+    ((EIGHT_B, 2, 2, 0), (EIGHT_B, 4, 1, 0), 16_062_119_936),
+    ((EIGHT_B, 8, 4, 128), (EIGHT_B, 2, 2, 128), 16_061_054_976),
+    ((EIGHT_B, 2, 2, 128), (EIGHT_B, 8, 4, 128), None),
+])
+def test_exact_cover_and_bytes_at_benchmark_shapes(src, dst, read):
+    ms, md = emu.Model(*src[0]), emu.Model(*dst[0])
+    plan = emu.Plan(emu.Layout(ms, *src[1:]), emu.Layout(md, *dst[1:]))
+    exact_cover(plan)
+    if read is not None:
+        assert plan.info["bytes_read"] == read == plan.info["bytes_written"]
+    else:
+        # reverse of the padded case: the 768 destination pad rows of the embedding (rank t=7, p=0) and
+        # of the LM head (rank t=7, p=3) are zero-filled
+        assert plan.info["zero_fill_bytes"] == 2 * (129024 - 128256) * 4096 * 2
+        assert plan.info["n_general_segments"] == 0
+
+
+def test_fp32_training_state_bytes():
+    m = emu.Model(*EIGHT_B)
+    a = emu.Plan(emu.Layout(m, 4, 1, 0, "fp32"), emu.Layout(m, 1, 1, 0, "fp32"))
+    b = emu.Plan(emu.Layout(m, 1, 1, 0, "fp32"), emu.Layout(m, 4, 1, 0, "fp32"))
+    assert a.info["bytes_read"] == 96_363_134_976 // 3
+    assert b.info["bytes_read"] == 96_372_719_616 // 3
+    exact_cover(a)
+
+
+def test_bucket_layout_padded_case():
+    m = emu.Model(*EIGHT_B)
+    plan = emu.Plan(emu.Layout(m, 8, 4, 128), emu.Layout(m, 2, 2, 128))
+    assert plan.bucket_layout(1, 2**28, 0) == (15, 4_015_259_648)
+    assert plan.bucket_layout(1, 2**28, 3) == (15, 4_015_267_840)
+    assert plan.bucket_layout(1, 2**28, -1) == (60, 16_061_054_976)
+    descs = plan.tensors(1)
+    assert [d["stream_offset"] for d in descs[:3]] == [0, 525_336_576, 525_344_768]
+
+
+def test_error_codes():
+    lib = emu.load()
+    m = emu.Model(*TINY)
+    assert emu.layout_check(emu.Layout(m, 2, 2)) == 0
+    assert emu.layout_check(emu.Layout(m, 4, 1)) == -4          # tp > KV heads
+    assert emu.layout_check(emu.Layout(m, 1, 3)) == -2          # pp does not divide L
+    assert emu.layout_check(emu.Layout(emu.Model(2, 256, 4, 64, 2, 688, 1023), 2, 1)) == -2
+    assert emu.layout_check(emu.Layout(emu.Model(2, 256, 4, 64, 2, 688, 1023), 2, 1, pad=64)) == 0
+    with pytest.raises(emu.EmuError) as e:
+        emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 1, 1, dtype="fp32"))
+    assert e.value.code == -3
+    with pytest.raises(emu.EmuError) as e:
+        emu.Plan(emu.Layout(m, 1, 1), emu.Layout(emu.Model(*MICRO), 1, 1))
+    assert e.value.code == -3
+    plan = emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1))
+    with pytest.raises(emu.EmuError) as e:
+        plan.bucket_layout(1, 0)
+    assert e.value.code == -6
+    with pytest.raises(emu.EmuError) as e:
+        plan.bucket_layout(1, 3)                                 # not a multiple of 2 bytes
+    assert e.value.code == -6
+    with pytest.raises(emu.EmuError) as e:
+        plan.bucket_layout(1, 1024, 2)
+    assert e.value.code == -10
+    d = emu.c_tensor_desc()
+    assert lib.emu_tensor_info(plan._h, 2, 0, ctypes.byref(d)) == -10
+    assert lib.emu_tensor_info(plan._h, 0, 10**6, ctypes.byref(d)) == -10
+    assert lib.emu_plan(None, None, None) == -1
+    h = plan._h
+    plan.close()
+    info = emu.c_plan_info()
+    assert lib.emu_plan_info(h, ctypes.byref(info)) == -9        # freed handle
+    assert lib.emu_plan_free(h) == -9
+    assert lib.emu_reshard(h, None, None, None, None) == -9
+    assert b"live plan" in lib.emu_last_error()
+    assert lib.emu_set_option(0, 5) == -11
+    assert lib.emu_set_option(99, 1) == -10
+    for s in range(-11, 1):
+        assert lib.emu_status_str(s).startswith(b"EMU_")
