@@ -100,7 +100,7 @@ def main():
     ap.add_argument("--cpu-layers", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--tile-vecs", type=int, default=None)
-    ap.add_argument("--wg-per-cu", type=int, default=None)
+    ap.add_argument("--xcd-remap", type=int, default=None)
     ap.add_argument("--nontemporal", type=int, default=None)
     ap.add_argument("--lds", type=int, default=None)
     ap.add_argument("--bucket-wg-per-cu", type=int, default=None)
@@ -117,7 +117,7 @@ def main():
     from synthetic import device_fill
 
     emu.load()
-    for opt, v in ((emu.OPT_TILE_VECS, args.tile_vecs), (emu.OPT_WG_PER_CU, args.wg_per_cu),
+    for opt, v in ((emu.OPT_TILE_VECS, args.tile_vecs), (emu.OPT_XCD_REMAP, args.xcd_remap),
                    (emu.OPT_NONTEMPORAL, args.nontemporal), (emu.OPT_LDS_STAGING, args.lds),
                    (emu.OPT_BUCKET_WG_PER_CU, args.bucket_wg_per_cu)):
         if v is not None:
@@ -241,7 +241,7 @@ def main():
             "algorithmic_bytes_per_launch": reshard_bytes,
         },
         "options": {k: emu.get_option(v) for k, v in (("tile_vecs", emu.OPT_TILE_VECS),
-                                                      ("wg_per_cu", emu.OPT_WG_PER_CU),
+                                                      ("xcd_remap", emu.OPT_XCD_REMAP),
                                                       ("nontemporal", emu.OPT_NONTEMPORAL),
                                                       ("lds_staging", emu.OPT_LDS_STAGING),
                                                       ("bucket_wg_per_cu", emu.OPT_BUCKET_WG_PER_CU))},

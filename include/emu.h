@@ -138,13 +138,13 @@ typedef struct {
 
 /* Tuning knobs (process-wide; change them only while no emu call is running). */
 typedef enum {
-  EMU_OPT_TILE_VECS = 0,     /* 16-byte vectors per thread per tile: 4, 8 or 16 (default 8); read by
+  EMU_OPT_TILE_VECS = 0,     /* 16-byte vectors per thread per tile: 4, 8 or 16 (default 4); read by
                                 emu_plan, so a plan keeps the value it was compiled with */
-  EMU_OPT_WG_PER_CU = 1,     /* reshard grid: workgroups per compute unit; 0 = one workgroup per tile
-                                (default 0) */
+  EMU_OPT_XCD_REMAP = 1,     /* 1 = give each XCD one contiguous eighth of the reshard tiles instead of
+                                every eighth tile (default 1) */
   EMU_OPT_NONTEMPORAL = 2,   /* 1 = streaming (non-temporal) loads and stores (default 1) */
   EMU_OPT_LDS_STAGING = 3,   /* 1 = stage each tile through LDS between load and store (default 0) */
-  EMU_OPT_BUCKET_WG_PER_CU = 4 /* pack/unpack grid: workgroups per compute unit (default 8) */
+  EMU_OPT_BUCKET_WG_PER_CU = 4 /* pack/unpack grid: workgroups per compute unit (default 16) */
 } emu_option;
 
 /* Library version (EMU_ABI_VERSION). */

@@ -19,17 +19,26 @@ typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 // device helpers
 // ------------------------------------------------------------------------------------------------
 
+// Global-address-space views: table-loaded pointers are generic to the compiler, which would emit
+// flat loads; casting to address space 1 gives global_load/store_dwordx4 with a scalar base.
+typedef __attribute__((address_space(1))) v4u gv4u;
+typedef __attribute__((address_space(1))) uint8_t gu8;
+
 template <bool NT>
-__device__ __forceinline__ v4u ld16(const v4u* p) {
+__device__ __forceinline__ v4u ld16(const uint8_t* base, uint32_t off) {
+  const gv4u* p = (const gv4u*)((const gu8*)base + off);
   if constexpr (NT) return __builtin_nontemporal_load(p);
   else return *p;
 }
 
 template <bool NT>
-__device__ __forceinline__ void st16(v4u* p, v4u v) {
+__device__ __forceinline__ void st16(uint8_t* base, uint32_t off, v4u v) {
+  gv4u* p = (gv4u*)((gu8*)base + off);
   if constexpr (NT) __builtin_nontemporal_store(v, p);
   else *p = v;
 }
+
+__device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b ? a : b; }
 
 __device__ __forceinline__ uint64_t uniform64(uint64_t x) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(x));
@@ -51,29 +60,26 @@ __device__ __forceinline__ v4u funnel(v4u lo, v4u hi, uint32_t b) {
 }
 
 // Workgroup-cooperative copy of nv 16-byte vectors, both sides 16-byte aligned (ZERO: store zeros).
+// nv * 16 must fit in 32 bits: offsets are 32-bit from uniform base pointers. Lanes past the end load
+// the last valid vector again (so every load is unconditional and all U are in flight together) and
+// skip their store.
 template <int U, bool NT, bool ZERO>
-__device__ __forceinline__ void wg_vec_copy(const v4u* __restrict__ s, v4u* __restrict__ d, uint64_t nv) {
+__device__ __forceinline__ void wg_vec_copy(const uint8_t* __restrict__ s, uint8_t* __restrict__ d, uint32_t nv) {
   const uint32_t tid = threadIdx.x;
   constexpr uint32_t TV = uint32_t(kThreads) * U;
-  for (uint64_t base = 0; base < nv; base += TV) {
-    const uint64_t cnt = nv - base < TV ? nv - base : TV;
+#pragma nounroll
+  for (uint32_t base = 0; base < nv; base += TV) {
+    const uint32_t last = umin(nv - base, TV) - 1;
     v4u r[U];
-    if (cnt == TV) {
 #pragma unroll
-      for (int u = 0; u < U; ++u) r[u] = ZERO ? v4u{0, 0, 0, 0} : ld16<NT>(s + base + u * kThreads + tid);
+    for (int u = 0; u < U; ++u) {
+      if constexpr (ZERO) r[u] = v4u{0, 0, 0, 0};
+      else r[u] = ld16<NT>(s, (base + umin(u * kThreads + tid, last)) * 16u);
+    }
 #pragma unroll
-      for (int u = 0; u < U; ++u) st16<NT>(d + base + u * kThreads + tid, r[u]);
-    } else {
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const uint32_t i = u * kThreads + tid;
-        r[u] = (!ZERO && i < cnt) ? ld16<NT>(s + base + i) : v4u{0, 0, 0, 0};
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const uint32_t i = u * kThreads + tid;
-        if (i < cnt) st16<NT>(d + base + i, r[u]);
-      }
+    for (int u = 0; u < U; ++u) {
+      const uint32_t i = u * kThreads + tid;
+      if (i <= last) st16<NT>(d, (base + i) * 16u, r[u]);
     }
   }
 }
@@ -83,57 +89,55 @@ __device__ __forceinline__ void wg_vec_copy(const v4u* __restrict__ s, v4u* __re
 // vectors. The second vector of the last output lies in the granule of the last source byte, so no
 // read leaves the granules the copy's own bytes occupy.
 template <int U, bool NT, int Q>
-__device__ __forceinline__ void wg_shift_copy(const v4u* __restrict__ sa, v4u* __restrict__ d, uint64_t nv,
+__device__ __forceinline__ void wg_shift_copy(const uint8_t* __restrict__ sa, uint8_t* __restrict__ d, uint32_t nv,
                                               uint32_t b) {
   const uint32_t tid = threadIdx.x;
   constexpr uint32_t TV = uint32_t(kThreads) * U;
-  for (uint64_t base = 0; base < nv; base += TV) {
-    const uint64_t cnt = nv - base < TV ? nv - base : TV;
+#pragma nounroll
+  for (uint32_t base = 0; base < nv; base += TV) {
+    const uint32_t last = umin(nv - base, TV) - 1;
     v4u lo[U], hi[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const uint32_t i = u * kThreads + tid;
-      if (i < cnt) {
-        lo[u] = ld16<NT>(sa + base + i);
-        hi[u] = ld16<NT>(sa + base + i + 1);
-      }
+      const uint32_t o = (base + umin(u * kThreads + tid, last)) * 16u;
+      lo[u] = ld16<NT>(sa, o);
+      hi[u] = ld16<NT>(sa, o + 16u);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const uint32_t i = u * kThreads + tid;
-      if (i < cnt) st16<NT>(d + base + i, funnel<Q>(lo[u], hi[u], b));
+      if (i <= last) st16<NT>(d, (base + i) * 16u, funnel<Q>(lo[u], hi[u], b));
     }
   }
 }
 
-// Workgroup-cooperative copy of n bytes at any alignment (ZERO: write n zero bytes).
+// Workgroup-cooperative copy of n bytes (n < 2^32) at any alignment (ZERO: write n zero bytes).
 // The destination drives the split: a head up to the first 16-byte boundary, a vector body and a
-// tail, the head and tail moved byte by byte.
-template <int U, bool NT, bool ZERO>
-__device__ void wg_copy_bytes(const uint8_t* s, uint8_t* d, uint64_t n) {
+// tail, the head and tail moved byte by byte. UA is the unroll of the co-aligned body, US that of the
+// realigned body (which holds two source vectors per output vector).
+template <int UA, int US, bool NT, bool ZERO>
+__device__ __forceinline__ void wg_copy_bytes(const uint8_t* s, uint8_t* d, uint32_t n) {
   const uint32_t tid = threadIdx.x;
-  const uint64_t head0 = (16 - (reinterpret_cast<uintptr_t>(d) & 15)) & 15;
-  const uint64_t head = head0 < n ? head0 : n;
-  const uint64_t nv = (n - head) / 16;
-  const uint64_t tail = n - head - nv * 16;
+  const uint32_t head0 = (16u - uint32_t(reinterpret_cast<uintptr_t>(d) & 15)) & 15u;
+  const uint32_t head = head0 < n ? head0 : n;
+  const uint32_t nv = (n - head) / 16u;
+  const uint32_t tail = n - head - nv * 16u;
   if (tid < head) d[tid] = ZERO ? 0 : s[tid];
-  if (tid < tail) d[head + nv * 16 + tid] = ZERO ? 0 : s[head + nv * 16 + tid];
+  if (tid < tail) d[head + nv * 16u + tid] = ZERO ? 0 : s[head + nv * 16u + tid];
   if (nv == 0) return;
-  v4u* dv = reinterpret_cast<v4u*>(d + head);
   if constexpr (ZERO) {
-    wg_vec_copy<U, NT, true>(nullptr, dv, nv);
+    wg_vec_copy<UA, NT, true>(nullptr, d + head, nv);
   } else {
-    const uintptr_t sp = reinterpret_cast<uintptr_t>(s + head);
-    const uint32_t sh = uint32_t(sp & 15);
+    const uint32_t sh = uint32_t(reinterpret_cast<uintptr_t>(s + head) & 15);
     if (sh == 0) {
-      wg_vec_copy<U, NT, false>(reinterpret_cast<const v4u*>(sp), dv, nv);
+      wg_vec_copy<UA, NT, false>(s + head, d + head, nv);
     } else {
-      const v4u* sa = reinterpret_cast<const v4u*>(sp - sh);
+      const uint8_t* sa = s + head - sh;
       switch (sh >> 2) {
-        case 0: wg_shift_copy<U, NT, 0>(sa, dv, nv, sh & 3); break;
-        case 1: wg_shift_copy<U, NT, 1>(sa, dv, nv, sh & 3); break;
-        case 2: wg_shift_copy<U, NT, 2>(sa, dv, nv, sh & 3); break;
-        default: wg_shift_copy<U, NT, 3>(sa, dv, nv, sh & 3); break;
+        case 0: wg_shift_copy<US, NT, 0>(sa, d + head, nv, sh & 3); break;
+        case 1: wg_shift_copy<US, NT, 1>(sa, d + head, nv, sh & 3); break;
+        case 2: wg_shift_copy<US, NT, 2>(sa, d + head, nv, sh & 3); break;
+        default: wg_shift_copy<US, NT, 3>(sa, d + head, nv, sh & 3); break;
       }
     }
   }
@@ -143,76 +147,85 @@ __device__ void wg_copy_bytes(const uint8_t* s, uint8_t* d, uint64_t n) {
 // reshard kernel: one tile = kThreads * U destination vectors of one segment
 // ------------------------------------------------------------------------------------------------
 
-template <int U, bool NT, bool ZERO, bool LDS>
-__device__ __forceinline__ void tile_rows(const DevSeg& g, uint64_t lt, const uint8_t* sb, uint8_t* db,
-                                          v4u* stage) {
-  // SEG_VEC_ROWS: `param` whole rows of rv vectors per tile; n -> (row, col) by a multiply-high
-  const uint32_t tid = threadIdx.x;
-  const uint64_t row0 = lt * g.param;
-  const uint64_t nrows = g.rows - row0 < g.param ? g.rows - row0 : g.param;
-  const uint32_t cnt = uint32_t(nrows) * g.rv;
-  const uint8_t* s = sb + g.src_off + row0 * g.src_stride;
-  uint8_t* d = db + g.dst_off + row0 * g.dst_stride;
-  v4u r[U];
-  uint32_t q[U], c[U];
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const uint32_t n = u * kThreads + tid;
-    q[u] = g.rv > 1 ? __umulhi(n, g.magic) : n;
-    c[u] = n - q[u] * g.rv;
-    if (!ZERO && n < cnt)
-      r[u] = ld16<NT>(reinterpret_cast<const v4u*>(s + q[u] * g.src_stride) + c[u]);
-    else
-      r[u] = v4u{0, 0, 0, 0};
-  }
+#ifndef EMU_RESHARD_WAVES_PER_EU
+#define EMU_RESHARD_WAVES_PER_EU 4
+#endif
+#ifndef EMU_BUCKET_WAVES_PER_EU
+#define EMU_BUCKET_WAVES_PER_EU 4
+#endif
+#ifndef EMU_BUCKET_UNROLL
+#define EMU_BUCKET_UNROLL 16
+#endif
+#ifndef EMU_SHIFT_UNROLL
+#define EMU_SHIFT_UNROLL 4
+#endif
+constexpr int kXcds = 8;           // XCDs of an MI355X; workgroups are dealt to them round-robin
+constexpr int kGeneralUnroll = 2;  // byte-granular reshard segments (misaligned runs; rare)
+constexpr int kBucketUnroll = EMU_BUCKET_UNROLL;
+constexpr int kShiftUnroll = EMU_SHIFT_UNROLL;
+
+template <int U, bool LDS>
+__device__ __forceinline__ void stage_through_lds(v4u (&r)[U], v4u* stage) {
   if constexpr (LDS) {
+    const uint32_t tid = threadIdx.x;
 #pragma unroll
     for (int u = 0; u < U; ++u) stage[u * kThreads + tid] = r[u];
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < U; ++u) r[u] = stage[u * kThreads + tid];
     __syncthreads();
-  }
-#pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const uint32_t n = u * kThreads + tid;
-    if (n < cnt) st16<NT>(reinterpret_cast<v4u*>(d + q[u] * g.dst_stride) + c[u], r[u]);
   }
 }
 
+// SEG_VEC_ROWS: `param` whole rows of rv vectors per tile. Vector n of the tile is at row n / rv
+// (a multiply-high by the host-computed magic number) and column n % rv; the host keeps
+// param * stride below 2^31 so that offsets stay 32-bit.
 template <int U, bool NT, bool ZERO, bool LDS>
-__device__ __forceinline__ void tile_run(const v4u* s, v4u* d, uint64_t cnt, v4u* stage) {
-  // a contiguous run of cnt <= kThreads*U vectors on both sides
+__device__ __forceinline__ void tile_rows(const DevSeg& g, uint64_t lt, const uint8_t* sb, uint8_t* db,
+                                          v4u* stage) {
   const uint32_t tid = threadIdx.x;
-  constexpr uint32_t TV = uint32_t(kThreads) * U;
+  const uint64_t row0 = lt * g.param;
+  const uint32_t nrows = uint32_t(g.rows - row0 < g.param ? g.rows - row0 : g.param);
+  const uint32_t last = nrows * g.rv - 1;
+  const uint32_t ss = uint32_t(g.src_stride), ds = uint32_t(g.dst_stride), rv = g.rv, mg = g.magic;
+  const uint8_t* s = ZERO ? nullptr : sb + g.src_off + row0 * g.src_stride;
+  uint8_t* d = db + g.dst_off + row0 * g.dst_stride;
   v4u r[U];
-  if (cnt == TV) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) r[u] = ZERO ? v4u{0, 0, 0, 0} : ld16<NT>(s + u * kThreads + tid);
-  } else {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t i = u * kThreads + tid;
-      r[u] = (!ZERO && i < cnt) ? ld16<NT>(s + i) : v4u{0, 0, 0, 0};
+  for (int u = 0; u < U; ++u) {
+    if constexpr (ZERO) {
+      r[u] = v4u{0, 0, 0, 0};
+    } else {
+      const uint32_t n = umin(u * kThreads + tid, last);
+      const uint32_t q = rv > 1 ? __umulhi(n, mg) : n;
+      r[u] = ld16<NT>(s, q * ss + (n - q * rv) * 16u);
     }
   }
-  if constexpr (LDS) {
+  stage_through_lds<U, LDS>(r, stage);
 #pragma unroll
-    for (int u = 0; u < U; ++u) stage[u * kThreads + tid] = r[u];
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < U; ++u) r[u] = stage[u * kThreads + tid];
-    __syncthreads();
+  for (int u = 0; u < U; ++u) {
+    const uint32_t n = u * kThreads + tid;
+    const uint32_t q = rv > 1 ? __umulhi(n, mg) : n;
+    if (n <= last) st16<NT>(d, q * ds + (n - q * rv) * 16u, r[u]);
   }
-  if (cnt == TV) {
+}
+
+// A contiguous run of cnt (1 <= cnt <= kThreads * U) vectors on both sides.
+template <int U, bool NT, bool ZERO, bool LDS>
+__device__ __forceinline__ void tile_run(const uint8_t* s, uint8_t* d, uint32_t cnt, v4u* stage) {
+  const uint32_t tid = threadIdx.x;
+  const uint32_t last = cnt - 1;
+  v4u r[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) st16<NT>(d + u * kThreads + tid, r[u]);
-  } else {
+  for (int u = 0; u < U; ++u) {
+    if constexpr (ZERO) r[u] = v4u{0, 0, 0, 0};
+    else r[u] = ld16<NT>(s, umin(u * kThreads + tid, last) * 16u);
+  }
+  stage_through_lds<U, LDS>(r, stage);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t i = u * kThreads + tid;
-      if (i < cnt) st16<NT>(d + i, r[u]);
-    }
+  for (int u = 0; u < U; ++u) {
+    const uint32_t i = u * kThreads + tid;
+    if (i <= last) st16<NT>(d, i * 16u, r[u]);
   }
 }
 
@@ -222,42 +235,52 @@ __device__ __forceinline__ void run_tile(const DevSeg& g, uint64_t lt, const uin
   const uint32_t mode = g.mode & SEG_MODE_MASK;
   if (mode == SEG_VEC_1D) {
     const uint64_t nv = g.run / 16, v0 = lt * TV;
-    const uint64_t cnt = nv - v0 < TV ? nv - v0 : TV;
-    tile_run<U, NT, ZERO, LDS>(reinterpret_cast<const v4u*>(sb + g.src_off) + v0,
-                               reinterpret_cast<v4u*>(db + g.dst_off) + v0, cnt, stage);
+    const uint32_t cnt = uint32_t(nv - v0 < TV ? nv - v0 : TV);
+    tile_run<U, NT, ZERO, LDS>(ZERO ? nullptr : sb + g.src_off + v0 * 16, db + g.dst_off + v0 * 16, cnt, stage);
   } else if (mode == SEG_VEC_ROWS) {
     tile_rows<U, NT, ZERO, LDS>(g, lt, sb, db, stage);
   } else if (mode == SEG_VEC_ROWCHUNK) {
     const uint64_t row = lt / g.param, ch = lt - row * g.param;
     const uint64_t nv = g.run / 16, v0 = ch * TV;
-    const uint64_t cnt = nv - v0 < TV ? nv - v0 : TV;
-    tile_run<U, NT, ZERO, LDS>(reinterpret_cast<const v4u*>(sb + g.src_off + row * g.src_stride) + v0,
-                               reinterpret_cast<v4u*>(db + g.dst_off + row * g.dst_stride) + v0, cnt, stage);
-  } else {  // SEG_GENERAL
+    const uint32_t cnt = uint32_t(nv - v0 < TV ? nv - v0 : TV);
+    tile_run<U, NT, ZERO, LDS>(ZERO ? nullptr : sb + g.src_off + row * g.src_stride + v0 * 16,
+                               db + g.dst_off + row * g.dst_stride + v0 * 16, cnt, stage);
+  } else {  // SEG_GENERAL: misaligned runs, moved at a small unroll so that this rare path does not set
+            // the kernel's register budget
     const uint64_t row = lt / g.param, ch = lt - row * g.param;
     const uint64_t b0 = ch * TV * 16;
-    const uint64_t n = g.run - b0 < TV * 16 ? g.run - b0 : TV * 16;
-    wg_copy_bytes<U, NT, ZERO>(sb + g.src_off + row * g.src_stride + b0, db + g.dst_off + row * g.dst_stride + b0, n);
+    const uint32_t n = uint32_t(g.run - b0 < TV * 16 ? g.run - b0 : TV * 16);
+    wg_copy_bytes<kGeneralUnroll, kGeneralUnroll, NT, ZERO>(ZERO ? nullptr : sb + g.src_off + row * g.src_stride + b0,
+                                                            db + g.dst_off + row * g.dst_stride + b0, n);
   }
 }
 
-template <int U, bool NT, bool LDS>
-__global__ __launch_bounds__(kThreads) void k_reshard(const DevSeg* __restrict__ segs,
-                                                      const uint32_t* __restrict__ tilemap, uint64_t ntiles,
-                                                      const uint64_t* __restrict__ src_ptrs,
-                                                      const uint64_t* __restrict__ dst_ptrs) {
+// One workgroup per tile. With XCD remapping, the round-robin dispatch of workgroups over the 8 XCDs is
+// undone: XCD x (workgroups x, x+8, ...) works through one contiguous eighth of the tile range, so each
+// XCD's L2 sees one stream instead of every eighth tile of all of them.
+template <int U, bool NT, bool LDS, bool XCD>
+__global__ __launch_bounds__(kThreads, EMU_RESHARD_WAVES_PER_EU) void k_reshard(const DevSeg* __restrict__ segs,
+                                                                             const uint32_t* __restrict__ tilemap,
+                                                                             uint64_t tile_base, uint32_t ntiles,
+                                                                             const uint64_t* __restrict__ src_ptrs,
+                                                                             const uint64_t* __restrict__ dst_ptrs) {
   extern __shared__ v4u stage[];
-  for (uint64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-    const uint32_t si = tilemap[tile];
-    const DevSeg g = segs[si];
-    const uint64_t lt = tile - g.tile0;
-    uint8_t* db = reinterpret_cast<uint8_t*>(dst_ptrs[g.dst_idx]);
-    if (g.mode & SEG_ZERO) {
-      run_tile<U, NT, true, LDS>(g, lt, nullptr, db, stage);
-    } else {
-      const uint8_t* sb = reinterpret_cast<const uint8_t*>(src_ptrs[g.src_idx]);
-      run_tile<U, NT, false, LDS>(g, lt, sb, db, stage);
-    }
+  uint32_t local = blockIdx.x;
+  if constexpr (XCD) {
+    const uint32_t per = gridDim.x / kXcds;  // the host launches a multiple of kXcds workgroups
+    local = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+  }
+  if (local >= ntiles) return;
+  const uint64_t tile = tile_base + local;
+  const uint32_t si = tilemap[tile];
+  const DevSeg g = segs[si];
+  const uint64_t lt = tile - g.tile0;
+  uint8_t* db = reinterpret_cast<uint8_t*>(dst_ptrs[g.dst_idx]);
+  if (g.mode & SEG_ZERO) {
+    run_tile<U, NT, true, LDS>(g, lt, nullptr, db, stage);
+  } else {
+    const uint8_t* sb = reinterpret_cast<const uint8_t*>(src_ptrs[g.src_idx]);
+    run_tile<U, NT, false, LDS>(g, lt, sb, db, stage);
   }
 }
 
@@ -286,7 +309,7 @@ __device__ __forceinline__ uint64_t wave_sum(uint64_t v) {
 }
 
 template <bool UNPACK, bool NT, int U>
-__global__ __launch_bounds__(kThreads) void k_buckets(const uint64_t* __restrict__ sizes,
+__global__ __launch_bounds__(kThreads, EMU_BUCKET_WAVES_PER_EU) void k_buckets(const uint64_t* __restrict__ sizes,
                                                       const uint32_t* __restrict__ rank_first,
                                                       const uint64_t* __restrict__ rank_bytes,
                                                       const uint64_t* __restrict__ chunk_first, int32_t nranks,
@@ -296,9 +319,19 @@ __global__ __launch_bounds__(kThreads) void k_buckets(const uint64_t* __restrict
   __shared__ uint64_t s_bucket0;
   const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint64_t nchunks = chunk_first[nranks];
+  // XCD-aware chunk order: with a grid that is a multiple of the XCD count, the workgroups of XCD x
+  // (x, x+8, ...) stride through the contiguous eighth [x*N/8, (x+1)*N/8) of the chunks.
+  uint64_t c_begin = blockIdx.x, c_end = nchunks, c_step = gridDim.x;
+  if (gridDim.x % kXcds == 0) {
+    const uint32_t x = blockIdx.x % kXcds;
+    c_begin = nchunks * x / kXcds + blockIdx.x / kXcds;
+    c_end = nchunks * (x + 1) / kXcds;
+    c_step = gridDim.x / kXcds;
+  }
   int32_t r = 0, cur = -1;
-  uint32_t t0 = 0, nt = 0;
-  for (uint64_t c = blockIdx.x; c < nchunks; c += gridDim.x) {
+  uint32_t t0 = 0, nt = 0, ti = 0;
+  uint64_t bucket0 = 0;
+  for (uint64_t c = c_begin; c < c_end; c += c_step) {
     while (chunk_first[r + 1] <= c) ++r;
     if (r != cur) {
       __syncthreads();  // previous rank's offsets no longer read
@@ -321,31 +354,41 @@ __global__ __launch_bounds__(kThreads) void k_buckets(const uint64_t* __restrict
       }
       __syncthreads();
       cur = r;
+      ti = 0;
+      bucket0 = uniform64(s_bucket0);
     }
-    const uint64_t S = offs[nt];
+    const uint64_t S = uniform64(offs[nt]);
     const uint64_t start = (c - chunk_first[r]) * kChunkBytes;
     const uint64_t end = start + kChunkBytes < S ? start + kChunkBytes : S;
-    const uint64_t bucket0 = s_bucket0;
-    // last tensor whose offset is <= start
-    uint32_t lo = 0, hi = nt;
-    while (hi - lo > 1) {
-      const uint32_t mid = (lo + hi) >> 1;
-      if (offs[mid] <= start) lo = mid; else hi = mid;
+    // tensor holding `start`: chunks of one workgroup move forward through the rank, so walk on from
+    // the previous chunk's tensor when it is close, else binary-search the offsets
+    if (offs[ti] > start || (ti + 8 < nt && offs[ti + 8] <= start)) {
+      uint32_t lo = 0, hi = nt;
+      while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (offs[mid] <= start) lo = mid; else hi = mid;
+      }
+      ti = lo;
     }
-    uint32_t ti = lo;
+    ti = __builtin_amdgcn_readfirstlane(ti);
+    uint64_t k = start / B;            // bucket of `start`; advanced incrementally below
+    uint64_t kend = (k + 1) * B;
     uint64_t pos = start;
     while (pos < end) {
-      while (offs[ti + 1] <= pos) ++ti;  // skips zero-size tensors too
-      const uint64_t toff = offs[ti], tend = offs[ti + 1];
-      const uint64_t k = pos / B;
+      while (uniform64(offs[ti + 1]) <= pos) ti = __builtin_amdgcn_readfirstlane(ti + 1);  // skips empty tensors
+      const uint64_t toff = uniform64(offs[ti]), tend = uniform64(offs[ti + 1]);
       uint64_t pend = end < tend ? end : tend;
-      if ((k + 1) * B < pend) pend = (k + 1) * B;
+      if (kend < pend) pend = kend;
       uint8_t* tp = reinterpret_cast<uint8_t*>(tensor_ptrs[t0 + ti]) + (pos - toff);
       uint8_t* bp = reinterpret_cast<uint8_t*>(bucket_ptrs[bucket0 + k]) + (pos - k * B);
-      const uint64_t n = uniform64(pend - pos);
-      if constexpr (UNPACK) wg_copy_bytes<U, NT, false>(bp, tp, n);
-      else wg_copy_bytes<U, NT, false>(tp, bp, n);
-      pos = uniform64(pend);
+      const uint32_t n = uint32_t(pend - pos);
+      if constexpr (UNPACK) wg_copy_bytes<U, kShiftUnroll, NT, false>(bp, tp, n);
+      else wg_copy_bytes<U, kShiftUnroll, NT, false>(tp, bp, n);
+      pos = pend;
+      if (pos == kend) {
+        ++k;
+        kend += B;
+      }
     }
   }
 }
@@ -374,22 +417,31 @@ static int hip_check(const char* what) {
   return EMU_OK;
 }
 
-template <int U, bool NT, bool LDS>
-static void launch_reshard(uint32_t grid, hipStream_t st, const DevSeg* segs, const uint32_t* tm, uint64_t nt,
-                           const uint64_t* sp, const uint64_t* dp) {
+template <int U, bool NT, bool LDS, bool XCD>
+static void launch_reshard(hipStream_t st, const DevSeg* segs, const uint32_t* tm, uint64_t ntiles, const uint64_t* sp,
+                           const uint64_t* dp) {
   const size_t lds = LDS ? size_t(kThreads) * U * 16 : 0;
-  hipLaunchKernelGGL((k_reshard<U, NT, LDS>), dim3(grid), dim3(kThreads), lds, st, segs, tm, nt, sp, dp);
+  constexpr uint64_t kMaxGrid = 0x7ffffff8ull;  // a multiple of kXcds below the grid-size limit
+  for (uint64_t base = 0; base < ntiles; base += kMaxGrid) {
+    const uint32_t n = uint32_t(ntiles - base < kMaxGrid ? ntiles - base : kMaxGrid);
+    const uint32_t grid = XCD ? (n + kXcds - 1) / kXcds * kXcds : n;
+    hipLaunchKernelGGL((k_reshard<U, NT, LDS, XCD>), dim3(grid), dim3(kThreads), lds, st, segs, tm, base, n, sp, dp);
+  }
 }
 
 template <int U>
-static void dispatch_reshard(bool nt_hint, bool lds, uint32_t grid, hipStream_t st, const DevSeg* segs,
-                             const uint32_t* tm, uint64_t nt, const uint64_t* sp, const uint64_t* dp) {
-  if (nt_hint) {
-    if (lds) launch_reshard<U, true, true>(grid, st, segs, tm, nt, sp, dp);
-    else launch_reshard<U, true, false>(grid, st, segs, tm, nt, sp, dp);
-  } else {
-    if (lds) launch_reshard<U, false, true>(grid, st, segs, tm, nt, sp, dp);
-    else launch_reshard<U, false, false>(grid, st, segs, tm, nt, sp, dp);
+static void dispatch_reshard(bool nt_hint, bool lds, bool xcd, hipStream_t st, const DevSeg* segs, const uint32_t* tm,
+                             uint64_t nt, const uint64_t* sp, const uint64_t* dp) {
+  const int key = (nt_hint ? 4 : 0) | (lds ? 2 : 0) | (xcd ? 1 : 0);
+  switch (key) {
+    case 0: launch_reshard<U, false, false, false>(st, segs, tm, nt, sp, dp); break;
+    case 1: launch_reshard<U, false, false, true>(st, segs, tm, nt, sp, dp); break;
+    case 2: launch_reshard<U, false, true, false>(st, segs, tm, nt, sp, dp); break;
+    case 3: launch_reshard<U, false, true, true>(st, segs, tm, nt, sp, dp); break;
+    case 4: launch_reshard<U, true, false, false>(st, segs, tm, nt, sp, dp); break;
+    case 5: launch_reshard<U, true, false, true>(st, segs, tm, nt, sp, dp); break;
+    case 6: launch_reshard<U, true, true, false>(st, segs, tm, nt, sp, dp); break;
+    default: launch_reshard<U, true, true, true>(st, segs, tm, nt, sp, dp); break;
   }
 }
 
@@ -413,7 +465,8 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
   const int cus = device_cus();
   if (cus <= 0) return fail(EMU_ERR_HIP, "cannot query the current device");
   const uint64_t want = uint64_t(cus) * uint64_t(option(EMU_OPT_BUCKET_WG_PER_CU));
-  const uint32_t grid = uint32_t(nchunks < want ? nchunks : want);
+  uint64_t grid = nchunks < want ? nchunks : want;
+  if (grid > kXcds) grid -= grid % kXcds;  // keep the XCD-aware chunk order available
   const uint8_t* w = static_cast<const uint8_t*>(ws);
   const SideTables& t = P->ws.side[side];
   const uint64_t* sizes = reinterpret_cast<const uint64_t*>(w + t.off_sizes);
@@ -423,11 +476,11 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool ntm = option(EMU_OPT_NONTEMPORAL) != 0;
   if (unpack) {
-    if (ntm) hipLaunchKernelGGL((k_buckets<true, true, 16>), dim3(grid), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);
-    else hipLaunchKernelGGL((k_buckets<true, false, 16>), dim3(grid), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);
+    if (ntm) hipLaunchKernelGGL((k_buckets<true, true, kBucketUnroll>), dim3(uint32_t(grid)), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);
+    else hipLaunchKernelGGL((k_buckets<true, false, kBucketUnroll>), dim3(uint32_t(grid)), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);
   } else {
-    if (ntm) hipLaunchKernelGGL((k_buckets<false, true, 16>), dim3(grid), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);
-    else hipLaunchKernelGGL((k_buckets<false, false, 16>), dim3(grid), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);
+    if (ntm) hipLaunchKernelGGL((k_buckets<false, true, kBucketUnroll>), dim3(uint32_t(grid)), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);
+    else hipLaunchKernelGGL((k_buckets<false, false, kBucketUnroll>), dim3(uint32_t(grid)), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);
   }
   return hip_check(unpack ? "emu_unpack_buckets launch" : "emu_pack_buckets launch");
 }
@@ -462,21 +515,16 @@ int emu_reshard(emu_plan_t plan, const void* d_workspace, const uint64_t* d_src_
   if (misaligned(d_workspace, kWsAlign)) return fail(EMU_ERR_WORKSPACE, "workspace not %llu-byte aligned", (unsigned long long)kWsAlign);
   if (misaligned(d_src_ptrs, 8) || misaligned(d_dst_ptrs, 8)) return fail(EMU_ERR_ALIGN, "pointer tables must be 8-byte aligned");
   if (P->ntiles == 0) return EMU_OK;
-  const int cus = device_cus();
-  if (cus <= 0) return fail(EMU_ERR_HIP, "cannot query the current device");
-  const int64_t per_cu = option(EMU_OPT_WG_PER_CU);
-  uint64_t grid = per_cu == 0 ? P->ntiles : uint64_t(cus) * uint64_t(per_cu);
-  if (grid > P->ntiles) grid = P->ntiles;
-  if (grid > 0x7fffffffull) grid = 0x7fffffffull;
   const uint8_t* w = static_cast<const uint8_t*>(d_workspace);
   const DevSeg* segs = reinterpret_cast<const DevSeg*>(w + P->ws.off_segs);
   const uint32_t* tm = reinterpret_cast<const uint32_t*>(w + P->ws.off_tilemap);
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
   const bool ntm = option(EMU_OPT_NONTEMPORAL) != 0, lds = option(EMU_OPT_LDS_STAGING) != 0;
+  const bool xcd = option(EMU_OPT_XCD_REMAP) != 0;
   switch (P->tile_vecs) {
-    case 4: dispatch_reshard<4>(ntm, lds, uint32_t(grid), st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
-    case 16: dispatch_reshard<16>(ntm, lds, uint32_t(grid), st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
-    default: dispatch_reshard<8>(ntm, lds, uint32_t(grid), st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
+    case 4: dispatch_reshard<4>(ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
+    case 16: dispatch_reshard<16>(ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
+    default: dispatch_reshard<8>(ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
   }
   return hip_check("emu_reshard launch");
 }

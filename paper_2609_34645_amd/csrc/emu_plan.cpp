@@ -47,7 +47,7 @@ bool plan_live(const Plan* p) {
   return g_plans.count(p) && p->magic == kPlanMagic;
 }
 
-static std::atomic<int64_t> g_opt[5] = {{8}, {0}, {1}, {0}, {8}};
+static std::atomic<int64_t> g_opt[5] = {{4}, {1}, {1}, {0}, {16}};
 
 int64_t option(int32_t key) { return g_opt[key].load(std::memory_order_relaxed); }
 
@@ -315,7 +315,10 @@ static int finalize(Plan& P) {
     } else if (g.run <= TB) {
       d.mode = SEG_VEC_ROWS;
       d.rv = uint32_t(g.run / 16);
-      d.param = uint32_t(TB / g.run);
+      // whole rows per tile, few enough that every in-tile byte offset stays below 2^31
+      const uint64_t stride = std::max(g.src_stride, g.dst_stride);
+      const uint64_t by_offset = stride < (1ull << 31) ? ((1ull << 31) - g.run) / stride + 1 : 1;
+      d.param = uint32_t(std::max<uint64_t>(1, std::min<uint64_t>(TB / g.run, by_offset)));
       d.magic = d.rv > 1 ? uint32_t(((1ull << 32) + d.rv - 1) / d.rv) : 0u;
       nt = (g.rows + d.param - 1) / d.param;
     } else {
@@ -427,11 +430,10 @@ int emu_set_option(int32_t key, int64_t value) {
     case EMU_OPT_TILE_VECS:
       if (value != 4 && value != 8 && value != 16) return fail(EMU_ERR_ARG, "tile vectors must be 4, 8 or 16");
       break;
-    case EMU_OPT_WG_PER_CU:
     case EMU_OPT_BUCKET_WG_PER_CU:
-      if (value < 0 || value > 64) return fail(EMU_ERR_ARG, "workgroups per CU must be in [0, 64]");
-      if (key == EMU_OPT_BUCKET_WG_PER_CU && value == 0) return fail(EMU_ERR_ARG, "need at least one workgroup per CU");
+      if (value < 1 || value > 64) return fail(EMU_ERR_ARG, "workgroups per CU must be in [1, 64]");
       break;
+    case EMU_OPT_XCD_REMAP:
     case EMU_OPT_NONTEMPORAL:
     case EMU_OPT_LDS_STAGING:
       if (value != 0 && value != 1) return fail(EMU_ERR_ARG, "flag must be 0 or 1");

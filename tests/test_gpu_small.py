@@ -117,7 +117,8 @@ def test_tiny_split_and_merge_back(gpu_lib):
 
 
 @pytest.mark.parametrize("opts", [
-    {emu.OPT_TILE_VECS: 4}, {emu.OPT_TILE_VECS: 16}, {emu.OPT_WG_PER_CU: 2},
+    {emu.OPT_TILE_VECS: 8}, {emu.OPT_TILE_VECS: 16}, {emu.OPT_XCD_REMAP: 1},
+    {emu.OPT_BUCKET_WG_PER_CU: 1}, {emu.OPT_TILE_VECS: 16, emu.OPT_XCD_REMAP: 1},
     {emu.OPT_NONTEMPORAL: 0}, {emu.OPT_LDS_STAGING: 1}, {emu.OPT_LDS_STAGING: 1, emu.OPT_TILE_VECS: 16},
 ])
 def test_launch_options(gpu_lib, opts):
