@@ -62,8 +62,8 @@ typedef enum {
   EMU_ERR_NULL = -1,        /* a required pointer argument is NULL */
   EMU_ERR_LAYOUT = -2,      /* a layout does not divide its model (invalid EMU layout) */
   EMU_ERR_MISMATCH = -3,    /* source and destination describe different models or element types */
-  EMU_ERR_UNSUPPORTED = -4, /* valid by definition but not implemented (tp > KV heads, > 2048 tensors
-                               on one rank) */
+  EMU_ERR_UNSUPPORTED = -4, /* valid by definition but not implemented (tp > KV heads; pack/unpack of
+                               a side with more than 2048 tensors on one rank) */
   EMU_ERR_WORKSPACE = -5,   /* workspace too small or not 256-byte aligned */
   EMU_ERR_BUCKET = -6,      /* bucket size zero or not a multiple of the element size */
   EMU_ERR_ALIGN = -7,       /* a device pointer argument is not 16-byte aligned */
@@ -80,7 +80,8 @@ typedef enum { EMU_GATE_UP_BLOCK = 0, EMU_GATE_UP_SEPARATE = 1 } emu_mlp_format;
 typedef enum {
   EMU_T_EMBED = 0, EMU_T_ATTN_NORM = 1, EMU_T_QKV = 2, EMU_T_Q = 3, EMU_T_K = 4, EMU_T_V = 5,
   EMU_T_O = 6, EMU_T_MLP_NORM = 7, EMU_T_GATE_UP = 8, EMU_T_GATE = 9, EMU_T_UP = 10,
-  EMU_T_DOWN = 11, EMU_T_FINAL_NORM = 12, EMU_T_LM_HEAD = 13
+  EMU_T_DOWN = 11, EMU_T_FINAL_NORM = 12, EMU_T_LM_HEAD = 13,
+  EMU_T_BUCKET = 14  /* destination side of a plan made by emu_plan_to_buckets */
 } emu_tensor_kind;
 
 /* Llama-style decoder shape: L layers, hidden H, nH query heads of head_dim, KV heads, MLP width, V. */
@@ -165,6 +166,16 @@ int emu_layout_check(const emu_layout_t* layout);
  * Destination-driven: every destination byte is covered by exactly one segment (zero-fill for
  * destination vocabulary pad rows). Host only: no GPU call. *out receives a new plan. */
 int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out);
+/* Compile the fused sender-side map: source shards of layout *src straight into the contiguous
+ * transfer buckets of layout *dst's ranks (bucket k of rank r = bytes [k*B, (k+1)*B) of r's stream),
+ * skipping the destination tensors. The paper sends each shard once as a contiguous buffer after a
+ * local layout change (section 6.2, transport and resharding-transport interplay); this plan does both
+ * in one pass over HBM. The plan's destination side (side 1) is the bucket list, rank 0's first, so it
+ * is executed with emu_reshard(plan, ws, d_src_ptrs, d_bucket_ptrs, stream), and the receiver restores
+ * the tensors with emu_unpack_buckets on an ordinary emu_plan(src, dst). Bucket bytes are identical to
+ * emu_pack_buckets applied to the emu_reshard result. bucket_bytes must be a positive multiple of the
+ * element size (EMU_ERR_BUCKET). Host only. */
+int emu_plan_to_buckets(const emu_layout_t* src, const emu_layout_t* dst, uint64_t bucket_bytes, emu_plan_t* out);
 /* Free a plan. Work enqueued with it must have completed. */
 int emu_plan_free(emu_plan_t plan);
 int emu_plan_info(emu_plan_t plan, emu_plan_info_t* out);

@@ -460,6 +460,9 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
   const uint64_t es = s.lay.dtype == EMU_BF16 ? 2 : 4;
   if (B == 0 || B % es) return fail(EMU_ERR_BUCKET, "bucket size %llu is not a positive multiple of %llu",
                                     (unsigned long long)B, (unsigned long long)es);
+  for (int r = 0; r < s.nranks; ++r)
+    if (s.rank_first[r + 1] - s.rank_first[r] > uint32_t(kMaxRankTensors))
+      return fail(EMU_ERR_UNSUPPORTED, "rank %d has more than %d tensors on this side", r, kMaxRankTensors);
   const uint64_t nchunks = s.chunk_first[s.nranks];
   if (nchunks == 0) return EMU_OK;
   const int cus = device_cus();

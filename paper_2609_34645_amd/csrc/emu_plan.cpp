@@ -279,6 +279,91 @@ static int compile(Plan& P, const std::vector<std::vector<Block>>& sb, const std
   return EMU_OK;
 }
 
+// Rewrite a destination-driven copy map so that it writes the destination ranks' bucket streams
+// instead of the destination tensors: tensor j's byte o lands at stream position
+// stream_offset(j) + o of its rank, i.e. in bucket (pos / B) at offset (pos % B). Rows that stay inside
+// one bucket keep their 2D shape; a row that crosses a bucket boundary is cut into 1D pieces there.
+// The destination side becomes the list of buckets (rank 0's first), so the result runs on the
+// ordinary reshard kernel with the bucket pointer table as its destination table.
+static int to_buckets(Plan& P, uint64_t B) {
+  SideInfo& D = P.side[1];
+  const uint64_t es = uint64_t(elem_size(D.lay.dtype));
+  if (B == 0 || B % es)
+    return fail(EMU_ERR_BUCKET, "bucket size %llu is not a positive multiple of %llu", (unsigned long long)B,
+                (unsigned long long)es);
+  std::vector<uint64_t> base(D.nranks + 1, 0);
+  for (int r = 0; r < D.nranks; ++r) base[r + 1] = base[r] + (D.rank_bytes[r] + B - 1) / B;
+  if (base[D.nranks] > 0x7fffffffull) return fail(EMU_ERR_UNSUPPORTED, "too many buckets");
+  std::vector<emu_segment_t> out;
+  out.reserve(P.segs.size() + 64);
+  auto emit = [&](const emu_segment_t& g, uint64_t src_off, int64_t bucket, uint64_t dst_off, uint64_t rows,
+                  uint64_t run, bool one_d) {
+    emu_segment_t s = g;
+    s.src_offset = src_off;
+    s.dst_tensor = int32_t(bucket);
+    s.dst_offset = dst_off;
+    s.rows = rows;
+    s.run = run;
+    if (one_d) s.src_stride = s.dst_stride = run;
+    push_segment(out, s);
+  };
+  for (const emu_segment_t& g : P.segs) {
+    const emu_tensor_desc_t& t = D.tensors[g.dst_tensor];
+    const uint64_t s0 = t.stream_offset + g.dst_offset;
+    uint64_t i = 0;
+    while (i < g.rows) {
+      const uint64_t si = s0 + i * g.dst_stride;
+      const uint64_t k = si / B, bend = (k + 1) * B;
+      const uint64_t so = g.src_offset + i * g.src_stride;
+      if (si + g.run <= bend) {
+        // rows i .. i+n-1 end inside bucket k
+        uint64_t n = 1;
+        if (g.rows > 1) n = std::min<uint64_t>(g.rows - i, (bend - si - g.run) / g.dst_stride + 1);
+        emit(g, so, int64_t(base[t.rank] + k), si - k * B, n, g.run, g.rows == 1);
+        i += n;
+      } else {
+        // row i crosses at least one bucket boundary: cut it there
+        for (uint64_t pos = 0; pos < g.run;) {
+          const uint64_t sp = si + pos, kk = sp / B;
+          const uint64_t e = std::min<uint64_t>(g.run, (kk + 1) * B - si);
+          emit(g, so + (g.src_tensor >= 0 ? pos : 0), int64_t(base[t.rank] + kk), sp - kk * B, 1, e - pos, true);
+          pos = e;
+        }
+        i += 1;
+      }
+    }
+  }
+  P.segs.swap(out);
+  // the destination side is now the bucket list
+  SideInfo bk;
+  bk.lay = D.lay;
+  bk.vp = D.vp;
+  bk.nranks = D.nranks;
+  bk.total_bytes = D.total_bytes;
+  bk.rank_first.assign(D.nranks + 1, 0);
+  bk.rank_bytes = D.rank_bytes;
+  bk.chunk_first.assign(D.nranks + 1, 0);
+  for (int r = 0; r < D.nranks; ++r) {
+    bk.rank_first[r] = uint32_t(bk.tensors.size());
+    for (uint64_t k = 0; k * B < D.rank_bytes[r]; ++k) {
+      emu_tensor_desc_t d{};
+      d.rank = r;
+      d.kind = EMU_T_BUCKET;
+      d.layer = -1;
+      d.ndim = 1;
+      d.bytes = std::min<uint64_t>(B, D.rank_bytes[r] - k * B);
+      d.rows = 1;
+      d.cols = int64_t(d.bytes / es);
+      d.stream_offset = k * B;
+      bk.tensors.push_back(d);
+    }
+    bk.chunk_first[r + 1] = bk.chunk_first[r] + (D.rank_bytes[r] + kChunkBytes - 1) / kChunkBytes;
+  }
+  bk.rank_first[D.nranks] = uint32_t(bk.tensors.size());
+  P.side[1] = std::move(bk);
+  return EMU_OK;
+}
+
 // Device segments, tiles and the workspace image.
 static int finalize(Plan& P) {
   const int U = P.tile_vecs;
@@ -490,6 +575,36 @@ int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out) 
     g_plans.insert(P);
   }
   *out = reinterpret_cast<emu_plan_t>(P);
+  return EMU_OK;
+}
+
+int emu_plan_to_buckets(const emu_layout_t* src, const emu_layout_t* dst, uint64_t bucket_bytes, emu_plan_t* out) {
+  clear_error();
+  if (!src || !dst || !out) return fail(EMU_ERR_NULL, "NULL argument");
+  *out = nullptr;
+  emu_plan_t base = nullptr;
+  int rc = emu_plan(src, dst, &base);
+  if (rc) return rc;
+  Plan* P = reinterpret_cast<Plan*>(base);
+  {
+    std::lock_guard<std::mutex> lk(g_plans_mu);
+    g_plans.erase(P);
+  }
+  try {
+    rc = to_buckets(*P, bucket_bytes);
+    if (!rc) rc = finalize(*P);
+  } catch (const std::bad_alloc&) {
+    rc = fail(EMU_ERR_ARG, "out of host memory");
+  }
+  if (rc) {
+    delete P;
+    return rc;
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_plans_mu);
+    g_plans.insert(P);
+  }
+  *out = base;
   return EMU_OK;
 }
 

@@ -31,7 +31,7 @@ ESIZE = {BF16: 2, FP32: 4}
 OPT_TILE_VECS, OPT_XCD_REMAP, OPT_NONTEMPORAL, OPT_LDS_STAGING, OPT_BUCKET_WG_PER_CU = range(5)
 
 KINDS = ["embed", "attn_norm", "qkv", "q", "k", "v", "o", "mlp_norm", "gate_up", "gate", "up", "down",
-         "final_norm", "lm_head"]
+         "final_norm", "lm_head", "bucket"]
 
 STATUS = {0: "EMU_OK", -1: "EMU_ERR_NULL", -2: "EMU_ERR_LAYOUT", -3: "EMU_ERR_MISMATCH",
           -4: "EMU_ERR_UNSUPPORTED", -5: "EMU_ERR_WORKSPACE", -6: "EMU_ERR_BUCKET", -7: "EMU_ERR_ALIGN",
@@ -99,6 +99,8 @@ def load(path: str = LIB_PATH):
         "emu_get_option": ([I32, ctypes.POINTER(I64)], ctypes.c_int),
         "emu_layout_check": ([ctypes.POINTER(c_layout)], ctypes.c_int),
         "emu_plan": ([ctypes.POINTER(c_layout), ctypes.POINTER(c_layout), ctypes.POINTER(P)], ctypes.c_int),
+        "emu_plan_to_buckets": ([ctypes.POINTER(c_layout), ctypes.POINTER(c_layout), U64, ctypes.POINTER(P)],
+                                ctypes.c_int),
         "emu_plan_free": ([P], ctypes.c_int),
         "emu_plan_info": ([P, ctypes.POINTER(c_plan_info)], ctypes.c_int),
         "emu_tensor_info": ([P, I32, I32, ctypes.POINTER(c_tensor_desc)], ctypes.c_int),
@@ -195,12 +197,17 @@ class ShardSet:
 class Plan:
     """A compiled copy map between two layouts (``emu_plan``)."""
 
-    def __init__(self, src: Layout, dst: Layout):
+    def __init__(self, src: Layout, dst: Layout, bucket_bytes: int = 0):
+        """bucket_bytes > 0 compiles the fused map (``emu_plan_to_buckets``): its destination side is
+        the destination ranks' buckets of that size."""
         lib = load()
-        self.src, self.dst = src, dst
+        self.src, self.dst, self.bucket_bytes = src, dst, bucket_bytes
         cs, cd = src.c(), dst.c()
         h = ctypes.c_void_p()
-        check(lib.emu_plan(ctypes.byref(cs), ctypes.byref(cd), ctypes.byref(h)))
+        if bucket_bytes:
+            check(lib.emu_plan_to_buckets(ctypes.byref(cs), ctypes.byref(cd), bucket_bytes, ctypes.byref(h)))
+        else:
+            check(lib.emu_plan(ctypes.byref(cs), ctypes.byref(cd), ctypes.byref(h)))
         self._h = h
         info = c_plan_info()
         check(lib.emu_plan_info(h, ctypes.byref(info)))
@@ -219,6 +226,8 @@ class Plan:
             for i in range(n):
                 check(lib.emu_tensor_info(self._h, side, i, ctypes.byref(d)))
                 shape = (d.cols,) if d.ndim == 1 else (d.rows, d.cols)
+                if d.kind == 14:
+                    shape = (d.bytes,)
                 out.append(dict(rank=d.rank, kind=KINDS[d.kind], layer=d.layer, shape=shape, bytes=d.bytes,
                                 stream_offset=d.stream_offset))
             self._descs[side] = out

@@ -86,6 +86,7 @@ def test_8b_tp2pp2_to_tp4pp1(gpu_lib):
     torch.cuda.synchronize()
     say(f"  8B reshard done in {time.time() - t:.3f} s (incl. launch)")
     check_reshard(p, S, D, label="8B TP2PP2->TP4PP1")
+    _pack_check(p, ws, D, 1 << 28, "fused reshard->buckets 2^28 (benchmark workload)", S=S)
     # Merge back: the round trip reproduces the source; norm replicas of TP rank 1 come back as rank 0's
     A2 = back.alloc(1, fill=0x5A)
     back.reshard(wb, D.ptrs, A2.ptrs)
@@ -97,13 +98,19 @@ def test_8b_tp2pp2_to_tp4pp1(gpu_lib):
     cleanup()
 
 
-def _pack_check(p, ws, D, B, label):
-    """Pack D at bucket size B, compare every bucket with oracle.pack of the (oracle-verified) destination
-    tensors rank by rank, unpack into a receiver set and compare it with D."""
+def _pack_check(p, ws, D, B, label, S=None):
+    """Fill buckets of size B -- with emu_pack_buckets from D, or, when the source set S is given, with
+    the fused source -> bucket plan -- and compare every bucket with oracle.pack of the (oracle-verified)
+    destination tensors rank by rank; then unpack into a receiver set and compare it with D."""
     import torch
 
     bufs, bptrs = p.alloc_buckets(1, B, fill=0x77)
-    p.pack(ws, 1, B, D.ptrs, bptrs)
+    if S is None:
+        p.pack(ws, 1, B, D.ptrs, bptrs)
+    else:
+        fused = emu.Plan(p.src, p.dst, bucket_bytes=B)
+        wf = fused.workspace()
+        fused.reshard(wf, S.ptrs, bptrs)
     torch.cuda.synchronize()
     dd = p.tensors(1)
     k = 0
@@ -140,11 +147,11 @@ def test_8b_padded_tp8pp4_to_tp2pp2_buckets(gpu_lib):
     p.reshard(ws, S.ptrs, D.ptrs)
     torch.cuda.synchronize()
     check_reshard(p, S, D, label="8B TP8PP4(pad)->TP2PP2")
-    del S
-    cleanup()
     _pack_check(p, ws, D, 1 << 28, "buckets 2^28")
     _pack_check(p, ws, D, (1 << 28) - 2, "buckets 2^28-2 (phase-shifted)")
-    del D, ws
+    _pack_check(p, ws, D, 1 << 28, "fused reshard->buckets 2^28", S=S)
+    _pack_check(p, ws, D, (1 << 28) - 2, "fused reshard->buckets 2^28-2", S=S)
+    del D, S, ws
     cleanup()
 
 

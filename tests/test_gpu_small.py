@@ -215,3 +215,37 @@ def test_execute_errors(gpu_lib):
         emu.ptr_table([S.bufs[0][1:]])
     assert e.value.code == -7
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("B", [64, 1000, 4094, 65536, 65538])
+def test_fused_reshard_to_buckets(gpu_lib, B):
+    """emu_plan_to_buckets: source shards straight into the destination ranks' buckets; the receiver
+    unpacks with the ordinary plan. Buckets and unpacked tensors against the oracle."""
+    import torch
+
+    m = emu.Model(*TINY)
+    pairs = [(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1)),
+             (emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate")),
+             (emu.Layout(m, 2, 1, 0, "fp32"), emu.Layout(m, 1, 2, 0, "fp32"))]
+    for src, dst in pairs:
+        if B % (2 if src.dtype == "bf16" else 4):
+            continue
+        fused, base = emu.Plan(src, dst, bucket_bytes=B), emu.Plan(src, dst)
+        wf, wb = fused.workspace(), base.workspace()
+        os_, od = o_layout(src), o_layout(dst)
+        S = base.alloc(0)
+        upload_shards(oracle.shard(full_model(os_.model, 8, src.dtype), os_), S, tp=src.tp)
+        K = fused.alloc(1, fill=0x77)          # side 1 of the fused plan = the buckets
+        fused.reshard(wf, S.ptrs, K.ptrs)
+        R = base.alloc(1, fill=0x11)
+        base.unpack(wb, 1, B, K.ptrs, R.ptrs)
+        torch.cuda.synchronize()
+        sd = base.tensors(0)
+        ranks_src = {}
+        for i, d in enumerate(sd):
+            ranks_src.setdefault(d["rank"], []).append(host_view(S.tensors[i], d, src.dtype))
+        want = oracle.reshard([ranks_src[r] for r in sorted(ranks_src)], os_, od)
+        check_buckets(fused, 1, B, want, K.tensors, label=f"fused B={B}")
+        flat = [np.ascontiguousarray(a).reshape(-1).view(np.uint8) for rank in want for a in rank]
+        for i, (t, w) in enumerate(zip(R.tensors, flat)):
+            assert np.array_equal(t.cpu().numpy(), w), f"unpacked tensor {i}"

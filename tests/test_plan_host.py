@@ -213,3 +213,74 @@ def test_error_codes():
     assert lib.emu_set_option(99, 1) == -10
     for s in range(-11, 1):
         assert lib.emu_status_str(s).startswith(b"EMU_")
+
+
+# ------------------------------------------------------------------------------------------------
+# fused reshard -> buckets (emu_plan_to_buckets)
+# ------------------------------------------------------------------------------------------------
+
+def check_fused(src, dst, B, full=None, seed=13):
+    plan = emu.Plan(src, dst, bucket_bytes=B)
+    os_, od = o_layout(src), o_layout(dst)
+    if full is None:
+        full = full_model(os_.model, seed, src.dtype)
+    src_shards = oracle.shard(full, os_)
+    for r, specs in enumerate(oracle.rank_inventory(os_)):
+        for j, s in enumerate(specs):
+            if s.kind.endswith("norm") and r % os_.tp:
+                src_shards[r][j] = src_shards[r][j] + np.array(1, dtype=src_shards[r][j].dtype)
+    flat_src = [np.ascontiguousarray(a).reshape(-1).view(np.uint8) for rank in src_shards for a in rank]
+    want = [b for rank in oracle.reshard(src_shards, os_, od) for b in oracle.pack(rank, B)]
+    descs = plan.tensors(1)
+    assert [d["kind"] for d in descs] == ["bucket"] * len(want)
+    assert [d["bytes"] for d in descs] == [w.size for w in want]
+    got = run_plan(plan.segments(), flat_src, [w.size for w in want])
+    for k, (g, w) in enumerate(zip(got, want)):
+        assert np.array_equal(g, w), (src, dst, B, k)
+    return plan
+
+
+@pytest.mark.parametrize("B", [8, 30, 64, 1000, 4094, 1 << 20])
+def test_fused_plan_matches_oracle_micro(B):
+    lays = MICRO_LAYS[::5]
+    full = full_model(o_layout(lays[0]).model)
+    for i, src in enumerate(lays):
+        for dst in lays[i % 3::3]:
+            check_fused(src, dst, B, full)
+
+
+def test_fused_plan_matches_oracle_tiny_and_fp32():
+    m = emu.Model(*TINY)
+    for B in (1 << 16, (1 << 16) - 2, 12345 * 2):
+        check_fused(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1), B)
+        check_fused(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate"), B)
+    check_fused(emu.Layout(m, 2, 1, 0, "fp32"), emu.Layout(m, 1, 2, 0, "fp32"), 4 * 1001)
+
+
+@pytest.mark.parametrize("B", [1 << 28, (1 << 28) - 2, 256 * 10**6])
+def test_fused_plan_exact_cover_8b(B):
+    m = emu.Model(*EIGHT_B)
+    plan = emu.Plan(emu.Layout(m, 2, 2), emu.Layout(m, 4, 1), bucket_bytes=B)
+    base = emu.Plan(emu.Layout(m, 2, 2), emu.Layout(m, 4, 1))
+    nb, sb = base.bucket_layout(1, B, -1)
+    assert plan.info["n_dst_tensors"] == nb and plan.info["bytes_written"] == sb == base.info["bytes_written"]
+    exact_cover(plan)
+    if B % 16 == 0:
+        assert plan.info["n_general_segments"] == 0
+
+
+def test_fused_plan_errors():
+    m = emu.Model(*TINY)
+    lib = emu.load()
+    a, b, h = emu.Layout(m, 1, 1).c(), emu.Layout(m, 2, 1).c(), ctypes.c_void_p()
+    assert lib.emu_plan_to_buckets(ctypes.byref(a), ctypes.byref(b), 0, ctypes.byref(h)) == -6
+    assert lib.emu_plan_to_buckets(ctypes.byref(a), ctypes.byref(b), 3, ctypes.byref(h)) == -6
+    assert lib.emu_plan_to_buckets(None, ctypes.byref(b), 64, ctypes.byref(h)) == -1
+    # a fused plan may hold any number of buckets, but packing its bucket side (more than 2048 buckets
+    # on one rank) is rejected before anything is launched
+    p = emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1), bucket_bytes=64)
+    assert p.info["n_dst_tensors"] == 2 * -(-1_976_832 // 64)
+    ws = ctypes.create_string_buffer(512)
+    addr = (ctypes.addressof(ws) + 255) // 256 * 256
+    fake = ctypes.c_void_p(addr)
+    assert lib.emu_pack_buckets(p._h, fake, 1, 64, fake, fake, None) == -4
