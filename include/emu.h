@@ -61,7 +61,7 @@ typedef enum {
   EMU_OK = 0,
   EMU_ERR_NULL = -1,        /* a required pointer argument is NULL */
   EMU_ERR_LAYOUT = -2,      /* a layout does not divide its model (invalid EMU layout) */
-  EMU_ERR_MISMATCH = -3,    /* source and destination describe different models or element types */
+  EMU_ERR_MISMATCH = -3,    /* source and destination describe different models */
   EMU_ERR_UNSUPPORTED = -4, /* valid by definition but not implemented (tp > KV heads; pack/unpack of
                                a side with more than 2048 tensors on one rank) */
   EMU_ERR_WORKSPACE = -5,   /* workspace too small or not 256-byte aligned */
@@ -108,14 +108,14 @@ typedef struct {
   int64_t n_zero_segments;
   int64_t n_tiles;           /* work tiles of one emu_reshard launch */
   uint64_t tile_bytes;       /* destination bytes per full tile */
-  uint64_t bytes_read;       /* bytes emu_reshard reads: destination bytes minus zero-filled bytes */
+  uint64_t bytes_read;       /* bytes emu_reshard reads (source bytes of all non-zero-fill segments) */
   uint64_t bytes_written;    /* bytes emu_reshard writes: all destination bytes */
   uint64_t zero_fill_bytes;
   uint64_t src_bytes, dst_bytes;
   uint64_t workspace_bytes;  /* device workspace emu_plan_upload needs */
   int32_t src_vocab_padded, dst_vocab_padded;
   int32_t n_general_segments; /* segments not on the 16-byte vector path (misaligned runs) */
-  int32_t reserved;
+  int32_t converts;          /* 0: same element type; 1: fp32 -> bf16; 2: bf16 -> fp32 */
 } emu_plan_info_t;
 
 typedef struct {
@@ -128,13 +128,16 @@ typedef struct {
   uint64_t stream_offset; /* byte offset inside its rank's bucket stream */
 } emu_tensor_desc_t;
 
-/* One entry of the copy map: rows x run bytes copied from the source tensor (src_tensor < 0: zeros)
- * at src_offset + i*src_stride to the destination tensor at dst_offset + i*dst_stride, i < rows. */
+/* One entry of the copy map: for i < rows, src_run bytes of the source tensor (src_tensor < 0: none,
+ * the destination gets zeros) at src_offset + i*src_stride become run bytes of the destination tensor at
+ * dst_offset + i*dst_stride. src_run == run unless the plan converts the element type (then the run
+ * holds the same elements in each side's type). */
 typedef struct {
   int32_t src_tensor, dst_tensor;   /* global tensor indices (pointer-table positions) */
   uint64_t src_offset, dst_offset;  /* bytes */
   uint64_t src_stride, dst_stride;  /* bytes between consecutive rows */
-  uint64_t rows, run;
+  uint64_t rows, run;               /* rows x destination bytes */
+  uint64_t src_run;                 /* source bytes read per row */
 } emu_segment_t;
 
 /* Tuning knobs (process-wide; change them only while no emu call is running). */
@@ -161,10 +164,13 @@ int emu_get_option(int32_t option, int64_t* value);
  * integer factor). Returns EMU_OK, EMU_ERR_LAYOUT or EMU_ERR_UNSUPPORTED. Host only. */
 int emu_layout_check(const emu_layout_t* layout);
 
-/* Compile the copy map from layout *src to layout *dst of the same model and element type
- * (section 5.2, Split and Merge; the call is direction-free and covers both and their compositions).
- * Destination-driven: every destination byte is covered by exactly one segment (zero-fill for
- * destination vocabulary pad rows). Host only: no GPU call. *out receives a new plan. */
+/* Compile the copy map from layout *src to layout *dst of the same model (section 5.2, Split and
+ * Merge; the call is direction-free and covers both and their compositions). Destination-driven: every
+ * destination byte is covered by exactly one segment (zero-fill for destination vocabulary pad rows).
+ * When the two layouts store different element types the map also converts every element: fp32 -> bf16
+ * rounds to nearest, ties to even (NaNs stay NaN with the quiet bit set), bf16 -> fp32 is exact. This is
+ * the weight synchronisation from a training model-stage to a generation model-stage of the same model
+ * (section 5, EMU definition). Host only: no GPU call. *out receives a new plan. */
 int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out);
 /* Compile the fused sender-side map: source shards of layout *src straight into the contiguous
  * transfer buckets of layout *dst's ranks (bucket k of rank r = bytes [k*B, (k+1)*B) of r's stream),

@@ -26,6 +26,7 @@ Modules:
   sharding -- logical tensors, shard, unshard, reshard (whole model or one tensor group at a time)
   buckets  -- per-rank byte streams, bucket pack and unpack
   coords   -- per-element coordinate formulas (pure Python) used by the brute-force pins
+  convert  -- fp32 <-> bf16 conversion for the weight-synchronising reshard (round to nearest even)
 """
 
 from .model import (  # noqa: F401
@@ -36,3 +37,4 @@ from .sharding import (  # noqa: F401
     logical_tensors, shard, unshard, reshard, shard_group, unshard_group, reshard_group,
 )
 from .buckets import stream_bytes, bucket_count, pack, unpack  # noqa: F401
+from .convert import convert, f32_to_bf16, bf16_to_f32  # noqa: F401

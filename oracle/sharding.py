@@ -12,13 +12,16 @@ norm + LM head), so that multi-GB models can be streamed through host memory. Re
 conventions are listed in ``oracle.model``; the direction-free form covers the paper's Split, its Merge,
 and compositions of the two.
 
-Arrays are NumPy arrays of any element type (bf16 is carried as uint16 bit patterns). Nothing here
-rounds or converts: the reshard is a selection and permutation of elements.
+Arrays are NumPy arrays of any element type (bf16 is carried as uint16 bit patterns). Between layouts
+of the same element type nothing rounds or converts: the reshard is a selection and permutation of
+elements. Between an fp32 and a bf16 layout (training state to generation weights) the logical tensors
+are converted by ``oracle.convert`` between unshard and shard.
 """
 from __future__ import annotations
 
 import numpy as np
 
+from .convert import convert
 from .model import Layout, LayoutError, check_layout, group_of, groups, padded_vocab, rank_inventory, \
     rank_of, stage_layers
 
@@ -190,14 +193,16 @@ def _same_state(src: Layout, dst: Layout) -> None:
     check_layout(dst)
     if src.model != dst.model:
         raise LayoutError("source and destination layouts describe different models")
-    if src.dtype != dst.dtype:
-        raise LayoutError("source and destination element types differ")
 
 
 def reshard_group(get, src: Layout, dst: Layout, group) -> dict:
-    """Destination shard tensors of one group: shard(unshard(src), dst)."""
+    """Destination shard tensors of one group: shard(convert(unshard(src)), dst). The conversion is the
+    identity when both layouts store the same element type (see oracle.convert)."""
     _same_state(src, dst)
-    return shard_group(dst, group, unshard_group(src, group, get))
+    full = unshard_group(src, group, get)
+    if src.dtype != dst.dtype:
+        full = {k: convert(v, src.dtype, dst.dtype) for k, v in full.items()}
+    return shard_group(dst, group, full)
 
 
 def shard(full: dict, lay: Layout) -> list:
@@ -219,7 +224,8 @@ def unshard(shards: list, lay: Layout) -> dict:
 
 
 def reshard(shards: list, src: Layout, dst: Layout) -> list:
-    """Destination shard set from a source shard set (the Split/Merge reshard)."""
+    """Destination shard set from a source shard set (the Split/Merge reshard, with an element-type
+    conversion when the two layouts store different types)."""
     _same_state(src, dst)
     inv = rank_inventory(dst)
     out = [[None] * len(specs) for specs in inv]

@@ -40,6 +40,76 @@ __device__ __forceinline__ void st16(uint8_t* base, uint32_t off, v4u v) {
 
 __device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b ? a : b; }
 
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(1))) v2u gv2u;
+
+template <bool NT>
+__device__ __forceinline__ v2u ld8(const uint8_t* base, uint32_t off) {
+  const gv2u* p = (const gv2u*)((const gu8*)base + off);
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+
+// fp32 bits -> bf16 bits: round to nearest, ties to even; a NaN keeps its sign and top payload bits and
+// gets the quiet bit (so that a NaN whose payload sits in the low half never turns into infinity).
+__device__ __forceinline__ uint32_t bf16_rne(uint32_t u) {
+  const uint32_t r = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  return (u & 0x7fffffffu) > 0x7f800000u ? ((u >> 16) | 0x40u) : r;
+}
+
+// Source data behind one 16-byte destination vector, per element conversion of the plan:
+// CVT_NONE one 16-byte vector; CVT_F32_BF16 two (8 fp32 -> 8 bf16); CVT_BF16_F32 half of one (4 bf16).
+template <int CVT> struct Raw { v4u a; };
+template <> struct Raw<CVT_F32_BF16> { v4u a, b; };
+template <> struct Raw<CVT_BF16_F32> { v2u a; };
+
+template <int CVT>
+constexpr uint32_t kSrcVecBytes = CVT == CVT_F32_BF16 ? 32u : CVT == CVT_BF16_F32 ? 8u : 16u;
+
+template <int CVT, bool NT>
+__device__ __forceinline__ Raw<CVT> ld_raw(const uint8_t* s, uint32_t off) {
+  Raw<CVT> r;
+  if constexpr (CVT == CVT_F32_BF16) {
+    r.a = ld16<NT>(s, off);
+    r.b = ld16<NT>(s, off + 16u);
+  } else if constexpr (CVT == CVT_BF16_F32) {
+    r.a = ld8<NT>(s, off);
+  } else {
+    r.a = ld16<NT>(s, off);
+  }
+  return r;
+}
+
+template <int CVT>
+__device__ __forceinline__ v4u cook(const Raw<CVT>& r) {
+  if constexpr (CVT == CVT_F32_BF16) {
+    v4u o;
+    o.x = bf16_rne(r.a.x) | (bf16_rne(r.a.y) << 16);
+    o.y = bf16_rne(r.a.z) | (bf16_rne(r.a.w) << 16);
+    o.z = bf16_rne(r.b.x) | (bf16_rne(r.b.y) << 16);
+    o.w = bf16_rne(r.b.z) | (bf16_rne(r.b.w) << 16);
+    return o;
+  } else if constexpr (CVT == CVT_BF16_F32) {
+    return v4u{r.a.x << 16, r.a.x & 0xffff0000u, r.a.y << 16, r.a.y & 0xffff0000u};
+  } else {
+    return r.a;
+  }
+}
+
+// Element-wise conversion of n destination elements (misaligned converting segments; rare).
+template <int CVT>
+__device__ void wg_convert_elems(const uint8_t* s, uint8_t* d, uint32_t n) {
+  for (uint32_t i = threadIdx.x; i < n; i += kThreads) {
+    if constexpr (CVT == CVT_F32_BF16) {
+      const uint32_t u = *(const __attribute__((address_space(1))) uint32_t*)((const gu8*)s + 4u * i);
+      *(__attribute__((address_space(1))) uint16_t*)((gu8*)d + 2u * i) = uint16_t(bf16_rne(u));
+    } else {
+      const uint32_t b = *(const __attribute__((address_space(1))) uint16_t*)((const gu8*)s + 2u * i);
+      *(__attribute__((address_space(1))) uint32_t*)((gu8*)d + 4u * i) = b << 16;
+    }
+  }
+}
+
 __device__ __forceinline__ uint64_t uniform64(uint64_t x) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(x));
   const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(x >> 32));
@@ -180,7 +250,7 @@ __device__ __forceinline__ void stage_through_lds(v4u (&r)[U], v4u* stage) {
 // SEG_VEC_ROWS: `param` whole rows of rv vectors per tile. Vector n of the tile is at row n / rv
 // (a multiply-high by the host-computed magic number) and column n % rv; the host keeps
 // param * stride below 2^31 so that offsets stay 32-bit.
-template <int U, bool NT, bool ZERO, bool LDS>
+template <int U, bool NT, bool ZERO, bool LDS, int CVT>
 __device__ __forceinline__ void tile_rows(const DevSeg& g, uint64_t lt, const uint8_t* sb, uint8_t* db,
                                           v4u* stage) {
   const uint32_t tid = threadIdx.x;
@@ -191,15 +261,19 @@ __device__ __forceinline__ void tile_rows(const DevSeg& g, uint64_t lt, const ui
   const uint8_t* s = ZERO ? nullptr : sb + g.src_off + row0 * g.src_stride;
   uint8_t* d = db + g.dst_off + row0 * g.dst_stride;
   v4u r[U];
+  if constexpr (ZERO) {
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    if constexpr (ZERO) {
-      r[u] = v4u{0, 0, 0, 0};
-    } else {
+    for (int u = 0; u < U; ++u) r[u] = v4u{0, 0, 0, 0};
+  } else {
+    Raw<CVT> raw[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
       const uint32_t n = umin(u * kThreads + tid, last);
       const uint32_t q = rv > 1 ? __umulhi(n, mg) : n;
-      r[u] = ld16<NT>(s, q * ss + (n - q * rv) * 16u);
+      raw[u] = ld_raw<CVT, NT>(s, q * ss + (n - q * rv) * kSrcVecBytes<CVT>);
     }
+#pragma unroll
+    for (int u = 0; u < U; ++u) r[u] = cook<CVT>(raw[u]);
   }
   stage_through_lds<U, LDS>(r, stage);
 #pragma unroll
@@ -210,16 +284,21 @@ __device__ __forceinline__ void tile_rows(const DevSeg& g, uint64_t lt, const ui
   }
 }
 
-// A contiguous run of cnt (1 <= cnt <= kThreads * U) vectors on both sides.
-template <int U, bool NT, bool ZERO, bool LDS>
+// A contiguous run of cnt (1 <= cnt <= kThreads * U) destination vectors.
+template <int U, bool NT, bool ZERO, bool LDS, int CVT>
 __device__ __forceinline__ void tile_run(const uint8_t* s, uint8_t* d, uint32_t cnt, v4u* stage) {
   const uint32_t tid = threadIdx.x;
   const uint32_t last = cnt - 1;
   v4u r[U];
+  if constexpr (ZERO) {
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    if constexpr (ZERO) r[u] = v4u{0, 0, 0, 0};
-    else r[u] = ld16<NT>(s, umin(u * kThreads + tid, last) * 16u);
+    for (int u = 0; u < U; ++u) r[u] = v4u{0, 0, 0, 0};
+  } else {
+    Raw<CVT> raw[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) raw[u] = ld_raw<CVT, NT>(s, umin(u * kThreads + tid, last) * kSrcVecBytes<CVT>);
+#pragma unroll
+    for (int u = 0; u < U; ++u) r[u] = cook<CVT>(raw[u]);
   }
   stage_through_lds<U, LDS>(r, stage);
 #pragma unroll
@@ -229,36 +308,44 @@ __device__ __forceinline__ void tile_run(const uint8_t* s, uint8_t* d, uint32_t 
   }
 }
 
-template <int U, bool NT, bool ZERO, bool LDS>
+template <int U, bool NT, bool ZERO, bool LDS, int CVT>
 __device__ __forceinline__ void run_tile(const DevSeg& g, uint64_t lt, const uint8_t* sb, uint8_t* db, v4u* stage) {
   constexpr uint64_t TV = uint64_t(kThreads) * U;
+  constexpr uint64_t SV = kSrcVecBytes<CVT>;
   const uint32_t mode = g.mode & SEG_MODE_MASK;
   if (mode == SEG_VEC_1D) {
     const uint64_t nv = g.run / 16, v0 = lt * TV;
     const uint32_t cnt = uint32_t(nv - v0 < TV ? nv - v0 : TV);
-    tile_run<U, NT, ZERO, LDS>(ZERO ? nullptr : sb + g.src_off + v0 * 16, db + g.dst_off + v0 * 16, cnt, stage);
+    tile_run<U, NT, ZERO, LDS, CVT>(ZERO ? nullptr : sb + g.src_off + v0 * SV, db + g.dst_off + v0 * 16, cnt, stage);
   } else if (mode == SEG_VEC_ROWS) {
-    tile_rows<U, NT, ZERO, LDS>(g, lt, sb, db, stage);
+    tile_rows<U, NT, ZERO, LDS, CVT>(g, lt, sb, db, stage);
   } else if (mode == SEG_VEC_ROWCHUNK) {
     const uint64_t row = lt / g.param, ch = lt - row * g.param;
     const uint64_t nv = g.run / 16, v0 = ch * TV;
     const uint32_t cnt = uint32_t(nv - v0 < TV ? nv - v0 : TV);
-    tile_run<U, NT, ZERO, LDS>(ZERO ? nullptr : sb + g.src_off + row * g.src_stride + v0 * 16,
-                               db + g.dst_off + row * g.dst_stride + v0 * 16, cnt, stage);
+    tile_run<U, NT, ZERO, LDS, CVT>(ZERO ? nullptr : sb + g.src_off + row * g.src_stride + v0 * SV,
+                                    db + g.dst_off + row * g.dst_stride + v0 * 16, cnt, stage);
   } else {  // SEG_GENERAL: misaligned runs, moved at a small unroll so that this rare path does not set
             // the kernel's register budget
     const uint64_t row = lt / g.param, ch = lt - row * g.param;
     const uint64_t b0 = ch * TV * 16;
     const uint32_t n = uint32_t(g.run - b0 < TV * 16 ? g.run - b0 : TV * 16);
-    wg_copy_bytes<kGeneralUnroll, kGeneralUnroll, NT, ZERO>(ZERO ? nullptr : sb + g.src_off + row * g.src_stride + b0,
-                                                            db + g.dst_off + row * g.dst_stride + b0, n);
+    uint8_t* d = db + g.dst_off + row * g.dst_stride + b0;
+    if constexpr (CVT == CVT_NONE || ZERO) {
+      wg_copy_bytes<kGeneralUnroll, kGeneralUnroll, NT, ZERO>(ZERO ? nullptr : sb + g.src_off + row * g.src_stride + b0,
+                                                              d, n);
+    } else {
+      constexpr uint32_t esd = CVT == CVT_F32_BF16 ? 2u : 4u;  // destination element bytes
+      constexpr uint32_t ess = CVT == CVT_F32_BF16 ? 4u : 2u;  // source element bytes
+      wg_convert_elems<CVT>(sb + g.src_off + row * g.src_stride + b0 / esd * ess, d, n / esd);
+    }
   }
 }
 
 // One workgroup per tile. With XCD remapping, the round-robin dispatch of workgroups over the 8 XCDs is
 // undone: XCD x (workgroups x, x+8, ...) works through one contiguous eighth of the tile range, so each
 // XCD's L2 sees one stream instead of every eighth tile of all of them.
-template <int U, bool NT, bool LDS, bool XCD>
+template <int U, bool NT, bool LDS, bool XCD, int CVT>
 __global__ __launch_bounds__(kThreads, EMU_RESHARD_WAVES_PER_EU) void k_reshard(const DevSeg* __restrict__ segs,
                                                                              const uint32_t* __restrict__ tilemap,
                                                                              uint64_t tile_base, uint32_t ntiles,
@@ -277,10 +364,10 @@ __global__ __launch_bounds__(kThreads, EMU_RESHARD_WAVES_PER_EU) void k_reshard(
   const uint64_t lt = tile - g.tile0;
   uint8_t* db = reinterpret_cast<uint8_t*>(dst_ptrs[g.dst_idx]);
   if (g.mode & SEG_ZERO) {
-    run_tile<U, NT, true, LDS>(g, lt, nullptr, db, stage);
+    run_tile<U, NT, true, LDS, CVT_NONE>(g, lt, nullptr, db, stage);
   } else {
     const uint8_t* sb = reinterpret_cast<const uint8_t*>(src_ptrs[g.src_idx]);
-    run_tile<U, NT, false, LDS>(g, lt, sb, db, stage);
+    run_tile<U, NT, false, LDS, CVT>(g, lt, sb, db, stage);
   }
 }
 
@@ -417,7 +504,7 @@ static int hip_check(const char* what) {
   return EMU_OK;
 }
 
-template <int U, bool NT, bool LDS, bool XCD>
+template <int U, bool NT, bool LDS, bool XCD, int CVT>
 static void launch_reshard(hipStream_t st, const DevSeg* segs, const uint32_t* tm, uint64_t ntiles, const uint64_t* sp,
                            const uint64_t* dp) {
   const size_t lds = LDS ? size_t(kThreads) * U * 16 : 0;
@@ -425,23 +512,39 @@ static void launch_reshard(hipStream_t st, const DevSeg* segs, const uint32_t* t
   for (uint64_t base = 0; base < ntiles; base += kMaxGrid) {
     const uint32_t n = uint32_t(ntiles - base < kMaxGrid ? ntiles - base : kMaxGrid);
     const uint32_t grid = XCD ? (n + kXcds - 1) / kXcds * kXcds : n;
-    hipLaunchKernelGGL((k_reshard<U, NT, LDS, XCD>), dim3(grid), dim3(kThreads), lds, st, segs, tm, base, n, sp, dp);
+    hipLaunchKernelGGL((k_reshard<U, NT, LDS, XCD, CVT>), dim3(grid), dim3(kThreads), lds, st, segs, tm, base, n, sp,
+                       dp);
   }
 }
 
+// Copy plans: every combination of the launch options. Converting plans: no LDS staging.
 template <int U>
-static void dispatch_reshard(bool nt_hint, bool lds, bool xcd, hipStream_t st, const DevSeg* segs, const uint32_t* tm,
-                             uint64_t nt, const uint64_t* sp, const uint64_t* dp) {
+static void dispatch_reshard(int cvt, bool nt_hint, bool lds, bool xcd, hipStream_t st, const DevSeg* segs,
+                             const uint32_t* tm, uint64_t nt, const uint64_t* sp, const uint64_t* dp) {
+  if (cvt != CVT_NONE) {
+    const int key = (cvt == CVT_F32_BF16 ? 0 : 4) | (nt_hint ? 2 : 0) | (xcd ? 1 : 0);
+    switch (key) {
+      case 0: launch_reshard<U, false, false, false, CVT_F32_BF16>(st, segs, tm, nt, sp, dp); break;
+      case 1: launch_reshard<U, false, false, true, CVT_F32_BF16>(st, segs, tm, nt, sp, dp); break;
+      case 2: launch_reshard<U, true, false, false, CVT_F32_BF16>(st, segs, tm, nt, sp, dp); break;
+      case 3: launch_reshard<U, true, false, true, CVT_F32_BF16>(st, segs, tm, nt, sp, dp); break;
+      case 4: launch_reshard<U, false, false, false, CVT_BF16_F32>(st, segs, tm, nt, sp, dp); break;
+      case 5: launch_reshard<U, false, false, true, CVT_BF16_F32>(st, segs, tm, nt, sp, dp); break;
+      case 6: launch_reshard<U, true, false, false, CVT_BF16_F32>(st, segs, tm, nt, sp, dp); break;
+      default: launch_reshard<U, true, false, true, CVT_BF16_F32>(st, segs, tm, nt, sp, dp); break;
+    }
+    return;
+  }
   const int key = (nt_hint ? 4 : 0) | (lds ? 2 : 0) | (xcd ? 1 : 0);
   switch (key) {
-    case 0: launch_reshard<U, false, false, false>(st, segs, tm, nt, sp, dp); break;
-    case 1: launch_reshard<U, false, false, true>(st, segs, tm, nt, sp, dp); break;
-    case 2: launch_reshard<U, false, true, false>(st, segs, tm, nt, sp, dp); break;
-    case 3: launch_reshard<U, false, true, true>(st, segs, tm, nt, sp, dp); break;
-    case 4: launch_reshard<U, true, false, false>(st, segs, tm, nt, sp, dp); break;
-    case 5: launch_reshard<U, true, false, true>(st, segs, tm, nt, sp, dp); break;
-    case 6: launch_reshard<U, true, true, false>(st, segs, tm, nt, sp, dp); break;
-    default: launch_reshard<U, true, true, true>(st, segs, tm, nt, sp, dp); break;
+    case 0: launch_reshard<U, false, false, false, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
+    case 1: launch_reshard<U, false, false, true, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
+    case 2: launch_reshard<U, false, true, false, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
+    case 3: launch_reshard<U, false, true, true, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
+    case 4: launch_reshard<U, true, false, false, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
+    case 5: launch_reshard<U, true, false, true, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
+    case 6: launch_reshard<U, true, true, false, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
+    default: launch_reshard<U, true, true, true, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
   }
 }
 
@@ -525,9 +628,9 @@ int emu_reshard(emu_plan_t plan, const void* d_workspace, const uint64_t* d_src_
   const bool ntm = option(EMU_OPT_NONTEMPORAL) != 0, lds = option(EMU_OPT_LDS_STAGING) != 0;
   const bool xcd = option(EMU_OPT_XCD_REMAP) != 0;
   switch (P->tile_vecs) {
-    case 4: dispatch_reshard<4>(ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
-    case 16: dispatch_reshard<16>(ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
-    default: dispatch_reshard<8>(ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
+    case 4: dispatch_reshard<4>(P->cvt, ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
+    case 16: dispatch_reshard<16>(P->cvt, ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
+    default: dispatch_reshard<8>(P->cvt, ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
   }
   return hip_check("emu_reshard launch");
 }

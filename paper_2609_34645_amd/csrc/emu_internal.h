@@ -27,6 +27,9 @@ enum SegMode : uint32_t {
 constexpr uint32_t SEG_MODE_MASK = 0xff;
 constexpr uint32_t SEG_ZERO = 0x100;  // no source: write zeros
 
+// Element conversion of a plan (all copy segments of one plan share it).
+enum Convert : int { CVT_NONE = 0, CVT_F32_BF16 = 1, CVT_BF16_F32 = 2 };
+
 // Device copy of one segment. 80 bytes, read with scalar loads by the reshard kernel.
 struct alignas(16) DevSeg {
   uint64_t src_off, dst_off;
@@ -73,6 +76,7 @@ struct Plan {
   std::vector<emu_segment_t> segs;  // execution order
   std::vector<DevSeg> dsegs;
   int tile_vecs = 8;                // 16-byte vectors per thread per tile
+  int cvt = CVT_NONE;               // element conversion of the whole plan
   uint64_t tile_bytes = 0;
   uint64_t ntiles = 0;
   emu_plan_info_t info{};

@@ -208,9 +208,11 @@ static void push_segment(std::vector<emu_segment_t>& out, const emu_segment_t& s
     emu_segment_t& p = out.back();
     // append to the previous run when both are single runs, same tensors, contiguous on both sides
     if (p.rows == 1 && s.rows == 1 && p.src_tensor == s.src_tensor && p.dst_tensor == s.dst_tensor &&
-        p.src_tensor >= 0 && p.src_offset + p.run == s.src_offset && p.dst_offset + p.run == s.dst_offset) {
+        p.src_tensor >= 0 && p.src_offset + p.src_run == s.src_offset && p.dst_offset + p.run == s.dst_offset) {
       p.run += s.run;
-      p.src_stride = p.dst_stride = p.run;
+      p.src_run += s.src_run;
+      p.src_stride = p.src_run;
+      p.dst_stride = p.run;
       return;
     }
   }
@@ -220,7 +222,7 @@ static void push_segment(std::vector<emu_segment_t>& out, const emu_segment_t& s
 static int compile(Plan& P, const std::vector<std::vector<Block>>& sb, const std::vector<std::vector<Block>>& db) {
   const SideInfo& S = P.side[0];
   const SideInfo& D = P.side[1];
-  const int es = elem_size(S.lay.dtype);
+  const uint64_t ess = uint64_t(elem_size(S.lay.dtype)), esd = uint64_t(elem_size(D.lay.dtype));
   const int nlt = 3 + 9 * S.lay.model.num_layers;
 
   // source blocks per logical tensor; replicated norms are read from TP rank 0 of their stage
@@ -249,16 +251,19 @@ static int compile(Plan& P, const std::vector<std::vector<Block>>& sb, const std
         emu_segment_t g{};
         g.src_tensor = sr.tensor;
         g.dst_tensor = int32_t(j);
-        g.src_offset = uint64_t((s.row0 + r0 - s.lrow0) * st.cols + (s.col0 + c0 - s.lcol0)) * es;
-        g.dst_offset = uint64_t((b.row0 + r0 - b.lrow0) * dt.cols + (b.col0 + c0 - b.lcol0)) * es;
-        g.src_stride = uint64_t(st.cols) * es;
-        g.dst_stride = uint64_t(dt.cols) * es;
+        g.src_offset = uint64_t((s.row0 + r0 - s.lrow0) * st.cols + (s.col0 + c0 - s.lcol0)) * ess;
+        g.dst_offset = uint64_t((b.row0 + r0 - b.lrow0) * dt.cols + (b.col0 + c0 - b.lcol0)) * esd;
+        g.src_stride = uint64_t(st.cols) * ess;
+        g.dst_stride = uint64_t(dt.cols) * esd;
         g.rows = uint64_t(r1 - r0);
-        g.run = uint64_t(c1 - c0) * es;
-        if (g.rows == 1 || (g.run == g.src_stride && g.run == g.dst_stride)) {
+        g.run = uint64_t(c1 - c0) * esd;
+        g.src_run = uint64_t(c1 - c0) * ess;
+        if (g.rows == 1 || (g.src_run == g.src_stride && g.run == g.dst_stride)) {
           g.run *= g.rows;
+          g.src_run *= g.rows;
           g.rows = 1;
-          g.src_stride = g.dst_stride = g.run;
+          g.src_stride = g.src_run;
+          g.dst_stride = g.run;
         }
         push_segment(P.segs, g);
       }
@@ -269,8 +274,9 @@ static int compile(Plan& P, const std::vector<std::vector<Block>>& sb, const std
       emu_segment_t z{};
       z.src_tensor = -1;
       z.dst_tensor = int32_t(j);
-      z.dst_offset = uint64_t(covered_rows) * dt.cols * es;
-      z.run = uint64_t(dt.rows - covered_rows) * dt.cols * es;
+      z.dst_offset = uint64_t(covered_rows) * dt.cols * esd;
+      z.run = uint64_t(dt.rows - covered_rows) * dt.cols * esd;
+      z.src_run = 0;
       z.rows = 1;
       z.src_stride = z.dst_stride = z.run;
       P.segs.push_back(z);
@@ -288,6 +294,7 @@ static int compile(Plan& P, const std::vector<std::vector<Block>>& sb, const std
 static int to_buckets(Plan& P, uint64_t B) {
   SideInfo& D = P.side[1];
   const uint64_t es = uint64_t(elem_size(D.lay.dtype));
+  const uint64_t ess = uint64_t(elem_size(P.side[0].lay.dtype));  // source bytes per destination element
   if (B == 0 || B % es)
     return fail(EMU_ERR_BUCKET, "bucket size %llu is not a positive multiple of %llu", (unsigned long long)B,
                 (unsigned long long)es);
@@ -304,7 +311,11 @@ static int to_buckets(Plan& P, uint64_t B) {
     s.dst_offset = dst_off;
     s.rows = rows;
     s.run = run;
-    if (one_d) s.src_stride = s.dst_stride = run;
+    s.src_run = g.src_tensor >= 0 ? run / es * ess : 0;
+    if (one_d) {
+      s.src_stride = s.src_run;
+      s.dst_stride = run;
+    }
     push_segment(out, s);
   };
   for (const emu_segment_t& g : P.segs) {
@@ -326,7 +337,8 @@ static int to_buckets(Plan& P, uint64_t B) {
         for (uint64_t pos = 0; pos < g.run;) {
           const uint64_t sp = si + pos, kk = sp / B;
           const uint64_t e = std::min<uint64_t>(g.run, (kk + 1) * B - si);
-          emit(g, so + (g.src_tensor >= 0 ? pos : 0), int64_t(base[t.rank] + kk), sp - kk * B, 1, e - pos, true);
+          emit(g, so + (g.src_tensor >= 0 ? pos / es * ess : 0), int64_t(base[t.rank] + kk), sp - kk * B, 1, e - pos,
+               true);
           pos = e;
         }
         i += 1;
@@ -372,8 +384,11 @@ static int finalize(Plan& P) {
   P.tile_bytes = TB;
   P.dsegs.clear();
   std::vector<uint32_t> tilemap;
-  uint64_t tiles = 0, zero_bytes = 0, written = 0;
+  uint64_t tiles = 0, zero_bytes = 0, written = 0, read = 0;
   int64_t nzero = 0;
+  // source alignment the vector paths need: 16 bytes when each destination vector reads one or two
+  // whole source vectors, 8 bytes when it reads half of one (bf16 -> fp32)
+  const uint64_t salign = P.cvt == CVT_BF16_F32 ? 8 : 16;
   int32_t ngeneral = 0;
   for (size_t i = 0; i < P.segs.size(); ++i) {
     const emu_segment_t& g = P.segs[i];
@@ -385,7 +400,7 @@ static int finalize(Plan& P) {
     d.tile0 = tiles;
     const bool zero = g.src_tensor < 0;
     const bool vec = ((g.dst_offset | g.run) % 16 == 0) && (g.rows == 1 || g.dst_stride % 16 == 0) &&
-                     (zero || (g.src_offset % 16 == 0 && (g.rows == 1 || g.src_stride % 16 == 0)));
+                     (zero || (g.src_offset % salign == 0 && (g.rows == 1 || g.src_stride % salign == 0)));
     uint64_t nt;
     if (!vec) {
       d.mode = SEG_GENERAL;
@@ -418,6 +433,7 @@ static int finalize(Plan& P) {
       ++nzero;
     }
     written += g.rows * g.run;
+    read += g.rows * g.src_run;
     if (tiles + nt > 0xffffffffull) return fail(EMU_ERR_UNSUPPORTED, "too many tiles");
     tilemap.insert(tilemap.end(), nt, uint32_t(i));
     tiles += nt;
@@ -467,7 +483,8 @@ static int finalize(Plan& P) {
   I.tile_bytes = TB;
   I.bytes_written = written;
   I.zero_fill_bytes = zero_bytes;
-  I.bytes_read = written - zero_bytes;
+  I.bytes_read = read;
+  I.converts = P.cvt;
   I.src_bytes = P.side[0].total_bytes;
   I.dst_bytes = P.side[1].total_bytes;
   I.workspace_bytes = w.total;
@@ -553,11 +570,11 @@ int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out) 
   if (rc) return rc;
   if (std::memcmp(&src->model, &dst->model, sizeof(emu_model_t)) != 0)
     return fail(EMU_ERR_MISMATCH, "source and destination layouts describe different models");
-  if (src->dtype != dst->dtype) return fail(EMU_ERR_MISMATCH, "source and destination element types differ");
   Plan* P = new (std::nothrow) Plan();
   if (!P) return fail(EMU_ERR_ARG, "out of host memory");
   try {
     P->tile_vecs = int(option(EMU_OPT_TILE_VECS));
+    P->cvt = src->dtype == dst->dtype ? CVT_NONE : (src->dtype == EMU_FP32 ? CVT_F32_BF16 : CVT_BF16_F32);
     std::vector<std::vector<Block>> sb, db;
     rc = build_side(*src, P->side[0], sb);
     if (!rc) rc = build_side(*dst, P->side[1], db);

@@ -57,7 +57,7 @@ class c_plan_info(ctypes.Structure):
                 ("zero_fill_bytes", ctypes.c_uint64), ("src_bytes", ctypes.c_uint64),
                 ("dst_bytes", ctypes.c_uint64), ("workspace_bytes", ctypes.c_uint64),
                 ("src_vocab_padded", ctypes.c_int32), ("dst_vocab_padded", ctypes.c_int32),
-                ("n_general_segments", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("n_general_segments", ctypes.c_int32), ("converts", ctypes.c_int32)]
 
 
 class c_tensor_desc(ctypes.Structure):
@@ -70,7 +70,7 @@ class c_segment(ctypes.Structure):
     _fields_ = [("src_tensor", ctypes.c_int32), ("dst_tensor", ctypes.c_int32),
                 ("src_offset", ctypes.c_uint64), ("dst_offset", ctypes.c_uint64),
                 ("src_stride", ctypes.c_uint64), ("dst_stride", ctypes.c_uint64),
-                ("rows", ctypes.c_uint64), ("run", ctypes.c_uint64)]
+                ("rows", ctypes.c_uint64), ("run", ctypes.c_uint64), ("src_run", ctypes.c_uint64)]
 
 
 class EmuError(RuntimeError):

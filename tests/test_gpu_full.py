@@ -133,6 +133,27 @@ def _pack_check(p, ws, D, B, label, S=None):
     cleanup()
 
 
+def test_8b_weight_sync_fp32_tp4_to_bf16_tp2pp2(gpu_lib):
+    """Training state -> generation weights: fp32 TP4 PP1 master to bf16 TP2 PP2 with the layout change
+    and the rounding in one pass, then fused into 2^28-byte buckets; every byte against the oracle."""
+    import torch
+
+    m = emu.Model(*EIGHT_B)
+    src, dst = emu.Layout(m, 4, 1, 0, "fp32"), emu.Layout(m, 2, 2, 0, "bf16")
+    p = emu.Plan(src, dst)
+    assert p.info["converts"] == 1 and p.info["bytes_read"] == 2 * p.info["bytes_written"]
+    ws = p.workspace()
+    S = p.alloc(0)
+    fill_device(p, 0, S, seed=404, dtype="fp32")
+    D = p.alloc(1, fill=0xA5)
+    p.reshard(ws, S.ptrs, D.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(p, S, D, label="8B fp32 TP4PP1 -> bf16 TP2PP2")
+    _pack_check(p, ws, D, 1 << 28, "fused fp32 -> bf16 buckets 2^28", S=S)
+    del S, D, ws
+    cleanup()
+
+
 def test_8b_padded_tp8pp4_to_tp2pp2_buckets(gpu_lib):
     import torch
 

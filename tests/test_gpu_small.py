@@ -249,3 +249,41 @@ def test_fused_reshard_to_buckets(gpu_lib, B):
         flat = [np.ascontiguousarray(a).reshape(-1).view(np.uint8) for rank in want for a in rank]
         for i, (t, w) in enumerate(zip(R.tensors, flat)):
             assert np.array_equal(t.cpu().numpy(), w), f"unpacked tensor {i}"
+
+
+@pytest.mark.parametrize("pair", [("fp32", "bf16"), ("bf16", "fp32")])
+def test_converting_reshard_small(gpu_lib, pair):
+    a, b = pair
+    mm = emu.Model(*MICRO)
+    n = 0
+    for tp_s, pp_s, tp_d, pp_d, pad in ((1, 1, 2, 1, 0), (4, 2, 1, 4, 2), (2, 4, 4, 1, 0), (1, 2, 4, 2, 2)):
+        for q, g in FORMATS:
+            run_pair(emu.Layout(mm, tp_s, pp_s, pad, a, q, g), emu.Layout(mm, tp_d, pp_d, pad, b, "separate", g),
+                     seed=n)
+            n += 1
+    m = emu.Model(*TINY)
+    run_pair(emu.Layout(m, 2, 2, 128, a), emu.Layout(m, 1, 1, 0, b), bucket_sizes=(65536, 4096 + 4))
+
+
+def test_fp32_to_bf16_special_values(gpu_lib):
+    """Every fp32 bit pattern class through the kernel: NaNs with payloads in either half, infinities,
+    denormals, ties, overflow to infinity -- against the oracle's round-to-nearest-even."""
+    import torch
+
+    m = emu.Model(*TINY)
+    src, dst = emu.Layout(m, 1, 1, 0, "fp32"), emu.Layout(m, 2, 1, 0, "bf16")
+    p = emu.Plan(src, dst)
+    ws = p.workspace()
+    S = p.alloc(0)
+    rng = np.random.default_rng(77)
+    specials = np.array([0x3F808000, 0x3F818000, 0x7F7F8000, 0x7F7FFFFF, 0x7F800000, 0xFF800000, 0x7FC00000,
+                         0x7F800001, 0xFFA00000, 0x80000000, 0x00000001, 0x00008000, 0x00018000, 0x007FFFFF],
+                        dtype=np.uint32)
+    for t in S.tensors:
+        u = rng.integers(0, 1 << 32, size=t.numel() // 4, dtype=np.uint64).astype(np.uint32)
+        u[:specials.size] = specials[:u.size]
+        t.copy_(torch.from_numpy(u.view(np.uint8)))
+    D = p.alloc(1, fill=0xA5)
+    p.reshard(ws, S.ptrs, D.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(p, S, D, label="fp32 bit patterns -> bf16")

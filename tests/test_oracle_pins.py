@@ -251,4 +251,4 @@ def test_layout_validation():
     with pytest.raises(oracle.LayoutError):
         oracle.check_layout(oracle.Layout(m3, 4, 1))
     with pytest.raises(oracle.LayoutError):
-        oracle.reshard([], oracle.Layout(m, 1, 1, dtype="bf16"), oracle.Layout(m, 1, 1, dtype="fp32"))
+        oracle.reshard([], oracle.Layout(m, 1, 1), oracle.Layout(oracle.Model(*MICRO), 1, 1))

@@ -182,9 +182,7 @@ def test_error_codes():
     assert emu.layout_check(emu.Layout(m, 1, 3)) == -2          # pp does not divide L
     assert emu.layout_check(emu.Layout(emu.Model(2, 256, 4, 64, 2, 688, 1023), 2, 1)) == -2
     assert emu.layout_check(emu.Layout(emu.Model(2, 256, 4, 64, 2, 688, 1023), 2, 1, pad=64)) == 0
-    with pytest.raises(emu.EmuError) as e:
-        emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 1, 1, dtype="fp32"))
-    assert e.value.code == -3
+    assert emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 1, 1, dtype="fp32")).info["converts"] == 2
     with pytest.raises(emu.EmuError) as e:
         emu.Plan(emu.Layout(m, 1, 1), emu.Layout(emu.Model(*MICRO), 1, 1))
     assert e.value.code == -3
@@ -284,3 +282,34 @@ def test_fused_plan_errors():
     addr = (ctypes.addressof(ws) + 255) // 256 * 256
     fake = ctypes.c_void_p(addr)
     assert lib.emu_pack_buckets(p._h, fake, 1, 64, fake, fake, None) == -4
+
+
+# ------------------------------------------------------------------------------------------------
+# element-converting reshard (fp32 training state <-> bf16 generation weights)
+# ------------------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("pair", [("fp32", "bf16"), ("bf16", "fp32")])
+def test_converting_plan_matches_oracle(pair):
+    a, b = pair
+    mm = emu.Model(*MICRO)
+    lays_a = [emu.Layout(mm, tp, pp, pad, a, q, g) for tp, pp, pad, (q, g) in
+              itertools.product((1, 4), (1, 2), (0, 2), sorted(FMT)[:2])]
+    lays_b = [emu.Layout(mm, tp, pp, pad, b, q, g) for tp, pp, pad, (q, g) in
+              itertools.product((2, 4), (1, 4), (0, 2), sorted(FMT)[1:3])]
+    full = full_model(o_layout(lays_a[0]).model, 17, a)
+    for src in lays_a:
+        for dst in lays_b:
+            p = check_pair(src, dst, full)
+            assert p.info["converts"] == (1 if a == "fp32" else 2)
+    m = emu.Model(*TINY)
+    check_pair(emu.Layout(m, 2, 2, 0, a), emu.Layout(m, 1, 1, 128, b))
+    check_fused(emu.Layout(m, 2, 1, 0, a), emu.Layout(m, 1, 2, 0, b), 65536 + 8)
+
+
+def test_converting_plan_bytes_8b():
+    m = emu.Model(*EIGHT_B)
+    p = emu.Plan(emu.Layout(m, 4, 1, 0, "fp32"), emu.Layout(m, 2, 2, 0, "bf16"))
+    # every bf16 destination element reads one fp32 source element
+    assert p.info["bytes_written"] == 16_061_054_976 and p.info["bytes_read"] == 2 * 16_061_054_976
+    assert p.info["converts"] == 1 and p.info["n_general_segments"] == 0
+    exact_cover(p)
