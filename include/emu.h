@@ -18,10 +18,13 @@
  *   - Megatron-style sharding: q/k/v and gate/up column-parallel, o and down row-parallel,
  *     embedding and LM head vocab-parallel, RMSNorm weights replicated on every TP rank.
  *   - Fused QKV (EMU_QKV_HEAD_INTERLEAVED): per rank, for each local KV group g, the rows of g's query
- *     heads, then k_g, then v_g. tp must divide the KV-head count (tp > KV heads: EMU_ERR_UNSUPPORTED).
+ *     heads, then k_g, then v_g. With tp <= KV heads, tp divides the KV-head count. With tp > KV heads
+ *     (KV replication) tp is a multiple of the KV heads and divides the query heads: rank t holds its
+ *     nH/tp query heads, then one copy of k and v of head t*G/tp; copies are read from their first holder.
  *   - Fused gate/up (EMU_GATE_UP_BLOCK): per rank, [gate rows of the rank; up rows of the rank].
- *   - PP stage p holds layers [p*L/pp, (p+1)*L/pp); the embedding is on stage 0, the final norm and
- *     LM head on stage pp-1; embeddings are untied.
+ *   - PP stages hold contiguous layer ranges; with L = q*pp + e the first e stages hold q+1 layers, the
+ *     others q. The embedding is on stage 0, the final norm and LM head on stage pp-1; embeddings are
+ *     untied.
  *   - Rank inside a unit: r = p*tp + t. Per-rank tensor order ("canonical order"): embed (p == 0);
  *     per local layer attn_norm, qkv (or q, k, v), o, mlp_norm, gate_up (or gate, up), down;
  *     final_norm, lm_head (p == pp-1). Tensor index tables list rank 0's tensors first, then rank 1's...
@@ -62,8 +65,8 @@ typedef enum {
   EMU_ERR_NULL = -1,        /* a required pointer argument is NULL */
   EMU_ERR_LAYOUT = -2,      /* a layout does not divide its model (invalid EMU layout) */
   EMU_ERR_MISMATCH = -3,    /* source and destination describe different models */
-  EMU_ERR_UNSUPPORTED = -4, /* valid by definition but not implemented (tp > KV heads; pack/unpack of
-                               a side with more than 2048 tensors on one rank) */
+  EMU_ERR_UNSUPPORTED = -4, /* valid by definition but not implemented (pack/unpack of a side with more
+                               than 2048 tensors on one rank; more than 2^32 tiles) */
   EMU_ERR_WORKSPACE = -5,   /* workspace too small or not 256-byte aligned */
   EMU_ERR_BUCKET = -6,      /* bucket size zero or not a multiple of the element size */
   EMU_ERR_ALIGN = -7,       /* a device pointer argument is not 16-byte aligned */
@@ -161,7 +164,7 @@ int emu_set_option(int32_t option, int64_t value);
 int emu_get_option(int32_t option, int64_t* value);
 
 /* Validate one layout (section 5.2: Split/Merge are defined between compatible layouts for any
- * integer factor). Returns EMU_OK, EMU_ERR_LAYOUT or EMU_ERR_UNSUPPORTED. Host only. */
+ * integer factor). Returns EMU_OK or EMU_ERR_LAYOUT. Host only. */
 int emu_layout_check(const emu_layout_t* layout);
 
 /* Compile the copy map from layout *src to layout *dst of the same model (section 5.2, Split and

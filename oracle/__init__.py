@@ -30,7 +30,7 @@ Modules:
 """
 
 from .model import (  # noqa: F401
-    Model, Layout, LayoutError, UnsupportedLayout, check_layout, padded_vocab, stage_layers,
+    Model, Layout, LayoutError, check_layout, padded_vocab, stage_layers, stage_of_layer, kv_local,
     rank_of, rank_inventory, TensorSpec, groups, DTYPE_BYTES,
 )
 from .sharding import (  # noqa: F401

@@ -24,6 +24,14 @@ def logical_of(lay: Layout, rank: int, kind: str, layer: int, i: int, c: int):
     if kind in ("embed", "lm_head"):
         row = t * (padded_vocab(lay) // tp) + i
         return None if row >= m.V else (kind, row, c)
+    if tp > m.G and kind in ("qkv", "k", "v"):
+        g, nq = t * m.G // tp, m.nH // tp * hd  # replicated KV head of this rank, its query rows
+        if kind == "qkv" and i < nq:
+            return (pre + "q", t * nq + i, c)
+        w = i - nq if kind == "qkv" else i
+        if kind == "k" or (kind == "qkv" and w < hd):
+            return (pre + "k", g * hd + w, c)
+        return (pre + "v", g * hd + (w - hd if kind == "qkv" else w), c)
     if kind == "qkv":
         qpg = m.nH // m.G                     # query heads per KV group
         per_group = (qpg + 2) * hd            # rows of one group: its q heads, its k head, its v head

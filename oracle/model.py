@@ -11,10 +11,14 @@ Readings (the paper is silent on all of these):
   * Sharding rules follow Megatron-LM, which the system integrates with (section 2): q/k/v and gate/up are
     column-parallel, o and down are row-parallel, embedding and LM head are vocab-parallel, norms are
     replicated on every TP rank.
-  * Fused QKV is head-interleaved per KV group; one KV head is never split or replicated across TP
-    ranks, so tp must divide the KV-head count (tp > kv_heads is rejected as unsupported).
-  * PP stages hold even contiguous layer ranges; the embedding sits on stage 0, the final norm and the
-    LM head on the last stage. Embeddings are untied.
+  * Fused QKV is head-interleaved per KV group: per local group, its query heads, its k head, its v head.
+    A KV head is never split. With tp <= kv_heads, tp divides the KV-head count and each rank holds
+    kv_heads/tp whole groups. With tp > kv_heads (the Megatron/vLLM convention), tp must be a multiple of
+    the KV-head count and divide the query heads: rank t holds nH/tp query heads and one replica of KV head
+    t * kv_heads / tp, which is read back from its first replica (the lowest rank holding it).
+  * PP stages hold contiguous layer ranges; when pp does not divide L, the first L mod pp stages hold
+    one extra layer. The embedding sits on stage 0, the final norm and the LM head on the last stage.
+    Embeddings are untied.
   * Rank order inside a unit is r = p * tp + t (TP fastest).
   * Vocabulary padding: with pad multiple m > 0 the padded vocabulary is ceil(V / (tp*m)) * tp * m;
     with m = 0 there is no padding and tp must divide V.
@@ -28,10 +32,6 @@ DTYPE_BYTES = {"bf16": 2, "fp32": 4}
 
 class LayoutError(ValueError):
     """The layout does not divide the model (an invalid EMU layout)."""
-
-
-class UnsupportedLayout(LayoutError):
-    """A layout the definition allows but this reading does not cover (tp > KV heads)."""
 
 
 @dataclass(frozen=True)
@@ -87,7 +87,7 @@ class TensorSpec:
 
 
 def check_layout(lay: Layout) -> None:
-    """Raise LayoutError / UnsupportedLayout unless ``lay`` is a valid layout of its model."""
+    """Raise LayoutError unless ``lay`` is a valid layout of its model."""
     m = lay.model
     for name in ("L", "H", "nH", "hd", "G", "I", "V"):
         if getattr(m, name) <= 0:
@@ -100,14 +100,14 @@ def check_layout(lay: Layout) -> None:
         raise LayoutError("unknown fused-weight format")
     if m.nH % m.G:
         raise LayoutError("query heads must be a multiple of KV heads")
-    if lay.tp > m.G:
-        raise UnsupportedLayout("tp larger than the KV-head count would replicate KV heads")
-    if m.G % lay.tp:
+    if lay.tp <= m.G and m.G % lay.tp:
         raise LayoutError("tp must divide the KV-head count")
+    if lay.tp > m.G and (lay.tp % m.G or m.nH % lay.tp):
+        raise LayoutError("with KV replication tp must be a multiple of the KV heads and divide the query heads")
     if m.I % lay.tp:
         raise LayoutError("tp must divide the MLP width")
-    if m.L % lay.pp:
-        raise LayoutError("pp must divide the layer count")
+    if lay.pp > m.L:
+        raise LayoutError("pp must not exceed the layer count")
     if lay.pad == 0 and m.V % lay.tp:
         raise LayoutError("tp must divide the vocabulary when it is not padded")
 
@@ -122,9 +122,23 @@ def padded_vocab(lay: Layout) -> int:
 
 
 def stage_layers(lay: Layout, p: int) -> range:
-    """Layers held by pipeline stage p: an even contiguous range."""
-    per = lay.model.L // lay.pp
-    return range(p * per, (p + 1) * per)
+    """Layers held by pipeline stage p: a contiguous range; the first L mod pp stages hold one more."""
+    per, extra = divmod(lay.model.L, lay.pp)
+    start = p * per + min(p, extra)
+    return range(start, start + per + (1 if p < extra else 0))
+
+
+def stage_of_layer(lay: Layout, layer: int) -> int:
+    """The pipeline stage holding ``layer``."""
+    for p in range(lay.pp):
+        if layer in stage_layers(lay, p):
+            return p
+    raise IndexError(layer)
+
+
+def kv_local(lay: Layout) -> int:
+    """KV heads held by one TP rank (1 when KV heads are replicated, tp > kv_heads)."""
+    return max(lay.model.G // lay.tp, 1)
 
 
 def rank_of(lay: Layout, t: int, p: int) -> int:
@@ -136,12 +150,13 @@ def _layer_specs(lay: Layout, layer: int) -> list:
     m, tp = lay.model, lay.tp
     H, hd = m.H, m.hd
     out = [TensorSpec("attn_norm", layer, (H,))]
+    kvl = kv_local(lay)
     if lay.qkv == "interleaved":
-        out.append(TensorSpec("qkv", layer, ((m.nH // tp + 2 * m.G // tp) * hd, H)))
+        out.append(TensorSpec("qkv", layer, ((m.nH // tp + 2 * kvl) * hd, H)))
     else:
         out += [TensorSpec("q", layer, (m.nH // tp * hd, H)),
-                TensorSpec("k", layer, (m.G // tp * hd, H)),
-                TensorSpec("v", layer, (m.G // tp * hd, H))]
+                TensorSpec("k", layer, (kvl * hd, H)),
+                TensorSpec("v", layer, (kvl * hd, H))]
     out.append(TensorSpec("o", layer, (H, m.nH * hd // tp)))
     out.append(TensorSpec("mlp_norm", layer, (H,)))
     if lay.mlp == "block":

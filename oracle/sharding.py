@@ -22,8 +22,8 @@ from __future__ import annotations
 import numpy as np
 
 from .convert import convert
-from .model import Layout, LayoutError, check_layout, group_of, groups, padded_vocab, rank_inventory, \
-    rank_of, stage_layers
+from .model import Layout, LayoutError, check_layout, group_of, groups, kv_local, padded_vocab, rank_inventory, \
+    rank_of, stage_of_layer
 
 LAYER_TENSORS = ("attn_norm", "q", "k", "v", "o", "mlp_norm", "gate", "up", "down")
 
@@ -68,7 +68,7 @@ def _owner_stage(lay: Layout, layer: int, kind: str) -> int:
         return 0
     if kind in ("final_norm", "lm_head"):
         return lay.pp - 1
-    return layer // (lay.model.L // lay.pp)
+    return stage_of_layer(lay, layer)
 
 
 # ----------------------------------------------------------------------------------------------
@@ -78,6 +78,13 @@ def _owner_stage(lay: Layout, layer: int, kind: str) -> int:
 def _shard_one(lay: Layout, kind: str, layer: int, t: int, full: dict) -> np.ndarray:
     m, tp = lay.model, lay.tp
     hd, qpg, gl = m.hd, m.nH // m.G, m.G // tp
+    if tp > m.G and kind in ("qkv", "k", "v"):
+        # KV replication: rank t holds nH/tp query heads and a replica of KV head t*G/tp
+        g, nq = t * m.G // tp, m.nH // tp * hd
+        q, k, v = (full[_key(n, layer)] for n in ("q", "k", "v"))
+        if kind == "qkv":
+            return np.concatenate([q[t * nq:(t + 1) * nq], k[g * hd:(g + 1) * hd], v[g * hd:(g + 1) * hd]], axis=0)
+        return (k if kind == "k" else v)[g * hd:(g + 1) * hd].copy()
     if kind in ("attn_norm", "mlp_norm", "final_norm"):
         # replicated on every TP rank of the owning stage
         return full[_key(kind, layer)].copy()
@@ -158,7 +165,19 @@ def unshard_group(lay: Layout, group, get) -> dict:
     layer = group
     full[_key("attn_norm", layer)] = first("attn_norm", layer)
     full[_key("mlp_norm", layer)] = first("mlp_norm", layer)
-    if lay.qkv == "interleaved":
+    if tp > m.G:
+        # KV replication: queries from every rank, each KV head from its first replica (rank g*tp/G)
+        rep, nq = tp // m.G, m.nH // tp * hd
+        blks = [np.asarray(b) for b in shards("qkv" if lay.qkv == "interleaved" else "q", layer)]
+        full[_key("q", layer)] = np.concatenate([b[:nq] for b in blks], axis=0)
+        if lay.qkv == "interleaved":
+            full[_key("k", layer)] = np.concatenate([blks[g * rep][nq:nq + hd] for g in range(m.G)], axis=0)
+            full[_key("v", layer)] = np.concatenate([blks[g * rep][nq + hd:nq + 2 * hd] for g in range(m.G)], axis=0)
+        else:
+            for n in ("k", "v"):
+                kb = [np.asarray(b) for b in shards(n, layer)]
+                full[_key(n, layer)] = np.concatenate([kb[g * rep] for g in range(m.G)], axis=0)
+    elif lay.qkv == "interleaved":
         qs, ks, vs = [], [], []
         for blk in shards("qkv", layer):
             b = np.asarray(blk).reshape(gl, qpg + 2, hd, m.H)

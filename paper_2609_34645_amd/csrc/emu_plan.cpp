@@ -64,6 +64,7 @@ struct Block {
   int64_t lrow0, nrows;   // logical rows covered
   int64_t lcol0, ncols;   // logical columns covered
   int64_t row0, col0;     // position inside the shard tensor
+  bool replica = false;   // a copy of data an earlier rank holds too (never used as a source)
 };
 
 static int elem_size(int32_t dtype) { return dtype == EMU_BF16 ? 2 : dtype == EMU_FP32 ? 4 : 0; }
@@ -83,11 +84,13 @@ static int check_layout(const emu_layout_t* l) {
     return fail(EMU_ERR_LAYOUT, "unknown mlp format %d", l->mlp_format);
   if (m.num_heads % m.num_kv_heads)
     return fail(EMU_ERR_LAYOUT, "query heads (%d) not a multiple of KV heads (%d)", m.num_heads, m.num_kv_heads);
-  if (l->tp > m.num_kv_heads)
-    return fail(EMU_ERR_UNSUPPORTED, "tp=%d exceeds the KV-head count %d (KV replication)", l->tp, m.num_kv_heads);
-  if (m.num_kv_heads % l->tp) return fail(EMU_ERR_LAYOUT, "tp=%d does not divide %d KV heads", l->tp, m.num_kv_heads);
+  if (l->tp <= m.num_kv_heads && m.num_kv_heads % l->tp)
+    return fail(EMU_ERR_LAYOUT, "tp=%d does not divide %d KV heads", l->tp, m.num_kv_heads);
+  if (l->tp > m.num_kv_heads && (l->tp % m.num_kv_heads || m.num_heads % l->tp))
+    return fail(EMU_ERR_LAYOUT, "tp=%d replicates KV heads: it must be a multiple of %d KV heads and divide %d heads",
+                l->tp, m.num_kv_heads, m.num_heads);
   if (m.ffn_hidden % l->tp) return fail(EMU_ERR_LAYOUT, "tp=%d does not divide the MLP width %d", l->tp, m.ffn_hidden);
-  if (m.num_layers % l->pp) return fail(EMU_ERR_LAYOUT, "pp=%d does not divide %d layers", l->pp, m.num_layers);
+  if (l->pp > m.num_layers) return fail(EMU_ERR_LAYOUT, "pp=%d exceeds %d layers", l->pp, m.num_layers);
   if (l->vocab_pad_multiple == 0 && m.vocab % l->tp)
     return fail(EMU_ERR_LAYOUT, "tp=%d does not divide the unpadded vocabulary %d", l->tp, m.vocab);
   return EMU_OK;
@@ -107,8 +110,10 @@ static int build_side(const emu_layout_t& lay, SideInfo& s, std::vector<std::vec
   const emu_model_t& m = lay.model;
   const int tp = lay.tp, pp = lay.pp, es = elem_size(lay.dtype);
   const int64_t H = m.hidden, hd = m.head_dim, G = m.num_kv_heads, nH = m.num_heads, I = m.ffn_hidden;
-  const int64_t qpg = nH / G, gl = G / tp, V = m.vocab;
-  const int L = m.num_layers, per_stage = L / pp;
+  const int64_t qpg = nH / G, V = m.vocab;
+  const bool kv_rep = tp > G;                 // KV heads replicated over tp / G ranks each
+  const int64_t gl = kv_rep ? 1 : G / tp;     // KV heads (groups) held per rank
+  const int L = m.num_layers, per_stage = L / pp, extra = L % pp;  // the first `extra` stages hold one more
   s.lay = lay;
   s.vp = padded_vocab(lay);
   s.nranks = tp * pp;
@@ -135,10 +140,33 @@ static int build_side(const emu_layout_t& lay, SideInfo& s, std::vector<std::vec
     for (int t = 0; t < tp; ++t) {
       const int r = p * tp + t;
       s.rank_first[r] = uint32_t(s.tensors.size());
+      const bool norm_rep = t != 0;                              // norms: TP rank 0 is the source
+      const int64_t rep = kv_rep ? tp / G : 1;                   // ranks sharing one KV head
+      const bool kv_replica = kv_rep && t % rep != 0;            // not the first holder of its KV head
+      const int l0 = p * per_stage + std::min(p, extra);
+      const int l1 = l0 + per_stage + (p < extra ? 1 : 0);
       if (p == 0) vocab_block(add(r, EMU_T_EMBED, -1, 2, vr, H), 0, t);
-      for (int l = p * per_stage; l < (p + 1) * per_stage; ++l) {
-        add(r, EMU_T_ATTN_NORM, l, 1, 1, H)->push_back({lt_layer(l, LK_ATTN_NORM), 0, 1, 0, H, 0, 0});
-        if (lay.qkv_format == EMU_QKV_HEAD_INTERLEAVED) {
+      for (int l = l0; l < l1; ++l) {
+        add(r, EMU_T_ATTN_NORM, l, 1, 1, H)->push_back({lt_layer(l, LK_ATTN_NORM), 0, 1, 0, H, 0, 0, norm_rep});
+        const int64_t nq = nH / tp * hd;                         // query rows of this rank
+        if (kv_rep) {
+          const int64_t g = t / rep;                             // the KV head this rank holds a copy of
+          Block q{lt_layer(l, LK_Q), t * nq, nq, 0, H, 0, 0};
+          Block k{lt_layer(l, LK_K), g * hd, hd, 0, H, 0, 0, kv_replica};
+          Block v{lt_layer(l, LK_V), g * hd, hd, 0, H, 0, 0, kv_replica};
+          if (lay.qkv_format == EMU_QKV_HEAD_INTERLEAVED) {
+            auto* b = add(r, EMU_T_QKV, l, 2, nq + 2 * hd, H);
+            k.row0 = nq;
+            v.row0 = nq + hd;
+            b->push_back(q);
+            b->push_back(k);
+            b->push_back(v);
+          } else {
+            add(r, EMU_T_Q, l, 2, nq, H)->push_back(q);
+            add(r, EMU_T_K, l, 2, hd, H)->push_back(k);
+            add(r, EMU_T_V, l, 2, hd, H)->push_back(v);
+          }
+        } else if (lay.qkv_format == EMU_QKV_HEAD_INTERLEAVED) {
           auto* b = add(r, EMU_T_QKV, l, 2, (nH / tp + 2 * gl) * hd, H);
           for (int64_t j = 0; j < gl; ++j) {
             const int64_t g = t * gl + j, base = j * (qpg + 2) * hd;
@@ -147,13 +175,13 @@ static int build_side(const emu_layout_t& lay, SideInfo& s, std::vector<std::vec
             b->push_back({lt_layer(l, LK_V), g * hd, hd, 0, H, base + (qpg + 1) * hd, 0});
           }
         } else {
-          add(r, EMU_T_Q, l, 2, nH / tp * hd, H)->push_back({lt_layer(l, LK_Q), t * (nH / tp) * hd, nH / tp * hd, 0, H, 0, 0});
+          add(r, EMU_T_Q, l, 2, nq, H)->push_back({lt_layer(l, LK_Q), t * nq, nq, 0, H, 0, 0});
           add(r, EMU_T_K, l, 2, gl * hd, H)->push_back({lt_layer(l, LK_K), t * gl * hd, gl * hd, 0, H, 0, 0});
           add(r, EMU_T_V, l, 2, gl * hd, H)->push_back({lt_layer(l, LK_V), t * gl * hd, gl * hd, 0, H, 0, 0});
         }
         const int64_t oc = nH * hd / tp;
         add(r, EMU_T_O, l, 2, H, oc)->push_back({lt_layer(l, LK_O), 0, H, t * oc, oc, 0, 0});
-        add(r, EMU_T_MLP_NORM, l, 1, 1, H)->push_back({lt_layer(l, LK_MLP_NORM), 0, 1, 0, H, 0, 0});
+        add(r, EMU_T_MLP_NORM, l, 1, 1, H)->push_back({lt_layer(l, LK_MLP_NORM), 0, 1, 0, H, 0, 0, norm_rep});
         const int64_t il = I / tp;
         if (lay.mlp_format == EMU_GATE_UP_BLOCK) {
           auto* b = add(r, EMU_T_GATE_UP, l, 2, 2 * il, H);
@@ -166,7 +194,7 @@ static int build_side(const emu_layout_t& lay, SideInfo& s, std::vector<std::vec
         add(r, EMU_T_DOWN, l, 2, H, il)->push_back({lt_layer(l, LK_DOWN), 0, H, t * il, il, 0, 0});
       }
       if (p == pp - 1) {
-        add(r, EMU_T_FINAL_NORM, -1, 1, 1, H)->push_back({1 + 9 * L, 0, 1, 0, H, 0, 0});
+        add(r, EMU_T_FINAL_NORM, -1, 1, 1, H)->push_back({1 + 9 * L, 0, 1, 0, H, 0, 0, norm_rep});
         vocab_block(add(r, EMU_T_LM_HEAD, -1, 2, vr, H), 2 + 9 * L, t);
       }
       if (s.tensors.size() - s.rank_first[r] > size_t(kMaxRankTensors))
@@ -193,10 +221,6 @@ static int build_side(const emu_layout_t& lay, SideInfo& s, std::vector<std::vec
 // ------------------------------------------------------------------------------------------------
 // copy map
 // ------------------------------------------------------------------------------------------------
-
-static bool is_norm(int kind) {
-  return kind == EMU_T_ATTN_NORM || kind == EMU_T_MLP_NORM || kind == EMU_T_FINAL_NORM;
-}
 
 struct SrcRef {
   int32_t tensor;
@@ -225,13 +249,12 @@ static int compile(Plan& P, const std::vector<std::vector<Block>>& sb, const std
   const uint64_t ess = uint64_t(elem_size(S.lay.dtype)), esd = uint64_t(elem_size(D.lay.dtype));
   const int nlt = 3 + 9 * S.lay.model.num_layers;
 
-  // source blocks per logical tensor; replicated norms are read from TP rank 0 of their stage
+  // source blocks per logical tensor; replicated data (norms on TP ranks > 0, KV heads past their first
+  // holder) is read from its first holder only
   std::vector<std::vector<SrcRef>> by_lt(nlt);
-  for (size_t i = 0; i < S.tensors.size(); ++i) {
-    const emu_tensor_desc_t& t = S.tensors[i];
-    if (is_norm(t.kind) && t.rank % S.lay.tp != 0) continue;
-    for (const Block& b : sb[i]) by_lt[b.lt].push_back({int32_t(i), b});
-  }
+  for (size_t i = 0; i < S.tensors.size(); ++i)
+    for (const Block& b : sb[i])
+      if (!b.replica) by_lt[b.lt].push_back({int32_t(i), b});
   for (auto& v : by_lt)
     std::sort(v.begin(), v.end(), [](const SrcRef& a, const SrcRef& b) {
       return a.b.lrow0 != b.b.lrow0 ? a.b.lrow0 < b.b.lrow0 : a.b.lcol0 < b.b.lcol0;

@@ -154,6 +154,23 @@ def test_8b_weight_sync_fp32_tp4_to_bf16_tp2pp2(gpu_lib):
     cleanup()
 
 
+def test_8b_kv_replication_uneven_pp(gpu_lib):
+    """TP2 PP2 -> TP16 PP3: every KV head copied to two ranks, 32 layers over 3 stages (11/11/10)."""
+    import torch
+
+    m = emu.Model(*EIGHT_B)
+    p = emu.Plan(emu.Layout(m, 2, 2), emu.Layout(m, 16, 3))
+    ws = p.workspace()
+    S = p.alloc(0)
+    fill_device(p, 0, S, seed=616)
+    D = p.alloc(1, fill=0xA5)
+    p.reshard(ws, S.ptrs, D.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(p, S, D, label="8B TP2PP2 -> TP16PP3")
+    del S, D, ws
+    cleanup()
+
+
 def test_8b_padded_tp8pp4_to_tp2pp2_buckets(gpu_lib):
     import torch
 

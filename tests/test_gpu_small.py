@@ -287,3 +287,12 @@ def test_fp32_to_bf16_special_values(gpu_lib):
     p.reshard(ws, S.ptrs, D.ptrs)
     torch.cuda.synchronize()
     check_reshard(p, S, D, label="fp32 bit patterns -> bf16")
+
+
+def test_kv_replication_and_uneven_pp_small(gpu_lib):
+    m = emu.Model(3, 16, 8, 2, 2, 16, 16)
+    lays = [emu.Layout(m, tp, pp, pad, "bf16", q, g) for tp, pp, pad, (q, g) in
+            itertools.product((1, 2, 4, 8), (1, 2, 3), (0, 2), FORMATS[:2])]
+    for i, src in enumerate(lays):
+        for dst in lays[i % 6::6]:
+            run_pair(src, dst, seed=i)

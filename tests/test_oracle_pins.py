@@ -68,15 +68,18 @@ SENTINEL = np.uint32(0xFFFF_FFFF)
 
 def tagged_source(lay):
     """Source shards whose elements carry (logical id + 1); pad rows hold a sentinel that must never be
-    read; norm replicas on TP ranks other than 0 carry a marked tag that must never be copied."""
+    read; every replica of a logical element held by an earlier rank (norms on TP ranks > 0, replicated
+    KV heads past their first rank) carries a marked tag that must never be copied."""
     out = []
+    seen = set()
     for r, (specs, ids) in enumerate(zip(oracle.rank_inventory(lay), ids_of(lay))):
         per = []
         for s, i in zip(specs, ids):
             a = np.array(i, dtype=np.int64)
             tag = np.where(a < 0, SENTINEL, (a + 1).astype(np.uint32)).astype(np.uint32)
-            if s.kind.endswith("norm") and r % lay.tp != 0:
-                tag = tag | REPLICA
+            rep = np.array([x >= 0 and x in seen for x in i], dtype=bool)
+            tag = np.where(rep, tag | REPLICA, tag)
+            seen.update(x for x in i if x >= 0)
             per.append(tag.reshape(s.shape))
         out.append(per)
     return out
@@ -91,6 +94,9 @@ def expected_tags(lay):
 
 
 MICRO_LAYOUTS = micro_layouts()
+# KV replication (tp up to 4x the KV heads) and uneven pipeline stages (L = 3)
+MICRO_KV = (3, 16, 8, 2, 2, 16, 16)
+KV_LAYOUTS = micro_layouts(MICRO_KV, tps=(1, 2, 4, 8), pps=(1, 2, 3), pads=(0, 2), dtype="fp32")
 
 
 @pytest.mark.parametrize("src", MICRO_LAYOUTS, ids=lambda l: f"tp{l.tp}pp{l.pp}m{l.pad}{l.qkv[0]}{l.mlp[0]}")
@@ -101,18 +107,30 @@ def test_brute_force_all_pairs(src):
         assert_sets_equal(got, expected_tags(dst))
 
 
+@pytest.mark.parametrize("src", KV_LAYOUTS[::2], ids=lambda l: f"tp{l.tp}pp{l.pp}m{l.pad}{l.qkv[0]}{l.mlp[0]}")
+def test_brute_force_kv_replication_and_uneven_pp(src):
+    s = tagged_source(src)
+    for dst in KV_LAYOUTS:
+        got = oracle.reshard(s, src, dst)
+        assert_sets_equal(got, expected_tags(dst))
+
+
 def test_element_ids_cover_model_once():
-    """Each logical element appears exactly once per TP-rank-0 copy: the id formulas form a bijection
-    between non-pad, non-replica shard elements and the logical model."""
-    for lay in MICRO_LAYOUTS[::5]:
+    """The id formulas cover every logical element, and only norms and replicated KV heads appear on more
+    than one rank."""
+    for lay in MICRO_LAYOUTS[::5] + KV_LAYOUTS[::7]:
         total = sum(int(np.prod(s)) if len(s) > 1 else s[0] for _, _, s, _ in oracle.logical_tensors(lay.model))
-        seen = []
+        count = np.zeros(total, dtype=np.int64)
         for r, (specs, ids) in enumerate(zip(oracle.rank_inventory(lay), ids_of(lay))):
             for spec, i in zip(specs, ids):
-                if spec.kind.endswith("norm") and r % lay.tp != 0:
-                    continue
-                seen += [x for x in i if x >= 0]
-        assert sorted(seen) == list(range(total))
+                a = np.array([x for x in i if x >= 0], dtype=np.int64)
+                np.add.at(count, a, 1)
+                if not spec.kind.endswith("norm") and spec.kind not in ("qkv", "k", "v"):
+                    assert len(set(a.tolist())) == a.size
+        assert count.min() == 1
+        if lay.tp <= lay.model.G:
+            # without KV replication only the norms are held more than once (once per TP rank)
+            assert count.max() == lay.tp
 
 
 # ------------------------------------------------------------------------------------------------
@@ -238,10 +256,13 @@ def test_reshard_equals_shard_of_full_on_tiny():
 def test_layout_validation():
     m = oracle.Model(*TINY)
     oracle.check_layout(oracle.Layout(m, 2, 2))
-    with pytest.raises(oracle.UnsupportedLayout):
-        oracle.check_layout(oracle.Layout(m, 4, 1))          # tp > KV heads
+    oracle.check_layout(oracle.Layout(m, 4, 1))              # tp > KV heads: KV heads replicated
     with pytest.raises(oracle.LayoutError):
-        oracle.check_layout(oracle.Layout(m, 1, 3))          # pp does not divide L
+        oracle.check_layout(oracle.Layout(m, 3, 1))          # tp > KV heads, not a multiple of them
+    with pytest.raises(oracle.LayoutError):
+        oracle.check_layout(oracle.Layout(m, 1, 3))          # more stages than layers
+    assert [list(oracle.stage_layers(oracle.Layout(oracle.Model(*MICRO), 1, 3), p)) for p in range(3)] == \
+        [[0, 1], [2], [3]]
     m2 = oracle.Model(4, 16, 8, 2, 4, 12, 21)                # odd vocabulary
     with pytest.raises(oracle.LayoutError):
         oracle.check_layout(oracle.Layout(m2, 2, 1))

@@ -178,7 +178,8 @@ def test_error_codes():
     lib = emu.load()
     m = emu.Model(*TINY)
     assert emu.layout_check(emu.Layout(m, 2, 2)) == 0
-    assert emu.layout_check(emu.Layout(m, 4, 1)) == -4          # tp > KV heads
+    assert emu.layout_check(emu.Layout(m, 4, 1)) == 0           # tp > KV heads: KV replication
+    assert emu.layout_check(emu.Layout(m, 3, 1)) == -2          # tp > KV heads but not a multiple
     assert emu.layout_check(emu.Layout(m, 1, 3)) == -2          # pp does not divide L
     assert emu.layout_check(emu.Layout(emu.Model(2, 256, 4, 64, 2, 688, 1023), 2, 1)) == -2
     assert emu.layout_check(emu.Layout(emu.Model(2, 256, 4, 64, 2, 688, 1023), 2, 1, pad=64)) == 0
@@ -313,3 +314,34 @@ def test_converting_plan_bytes_8b():
     assert p.info["bytes_written"] == 16_061_054_976 and p.info["bytes_read"] == 2 * 16_061_054_976
     assert p.info["converts"] == 1 and p.info["n_general_segments"] == 0
     exact_cover(p)
+
+
+# ------------------------------------------------------------------------------------------------
+# KV-head replication (tp > KV heads) and uneven pipeline stages
+# ------------------------------------------------------------------------------------------------
+
+MICRO_KV = (3, 16, 8, 2, 2, 16, 16)
+
+
+def test_kv_replication_and_uneven_pp_match_oracle():
+    m = emu.Model(*MICRO_KV)
+    lays = [emu.Layout(m, tp, pp, pad, "bf16", q, g)
+            for tp, pp, pad, (q, g) in itertools.product((1, 2, 4, 8), (1, 2, 3), (0, 2), sorted(FMT)[:2])]
+    full = full_model(o_layout(lays[0]).model, 23)
+    for i, src in enumerate(lays):
+        for dst in lays[i % 4::4]:
+            check_pair(src, dst, full)
+
+
+def test_kv_replication_8b_tp16():
+    """Llama-8B shapes at TP16 (each of the 8 KV heads held by two ranks) and an uneven 32-layer PP3."""
+    m = emu.Model(*EIGHT_B)
+    p = emu.Plan(emu.Layout(m, 2, 2), emu.Layout(m, 16, 1, 128))
+    exact_cover(p)
+    descs = p.tensors(1)
+    qkv = [d for d in descs if d["kind"] == "qkv"]
+    assert qkv[0]["shape"] == ((32 // 16 + 2) * 128, 4096)
+    p3 = emu.Plan(emu.Layout(m, 4, 1), emu.Layout(m, 2, 3))
+    exact_cover(p3)
+    layers = [sorted({d["layer"] for d in p3.tensors(1) if d["rank"] == r and d["layer"] >= 0}) for r in (0, 2, 4)]
+    assert layers == [list(range(0, 11)), list(range(11, 22)), list(range(22, 32))]
