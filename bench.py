@@ -201,6 +201,27 @@ def main():
     fused_ok = all(torch.equal(a, b) for a, b in zip(D.bufs, R.bufs))
     fused_bytes = fused.info["bytes_read"] + fused.info["bytes_written"]
 
+    # weight sync from a training stage to a generation stage: fp32 TP4 PP1 master -> bf16 TP2 PP2
+    # (layout change and round-to-nearest-even conversion in one pass)
+    sync = emu.Plan(emu.Layout(model, 4, 1, 0, "fp32"), emu.Layout(model, 2, 2, 0, "bf16"))
+    wsy = sync.workspace(dev)
+    SY = sync.alloc(0, dev)
+    device_fill(SY.tensors, args.seed + 1, ["norm" if d["kind"].endswith("norm") else "weight"
+                                            for d in sync.tensors(0)], "fp32")
+    DY = sync.alloc(1, dev)
+    for _ in range(args.warmup):
+        sync.reshard(wsy, SY.ptrs, DY.ptrs)
+    sev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+    torch.cuda.synchronize()
+    sev[0].record()
+    for k in range(args.steps):
+        sync.reshard(wsy, SY.ptrs, DY.ptrs)
+        sev[k + 1].record()
+    torch.cuda.synchronize()
+    sync_ms = sum(sev[k].elapsed_time(sev[k + 1]) for k in range(args.steps)) / args.steps
+    sync_bytes = sync.info["bytes_read"] + sync.info["bytes_written"]
+    del SY, DY, wsy
+
     # plain device copy of the same destination bytes (torch copy_), as a practical ceiling
     cev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     for b_src, b_dst in zip(D.bufs, R.bufs):
@@ -252,6 +273,8 @@ def main():
         "fused_reshard_to_buckets_GBps": round(fused_bytes / (mean(f_ms) * 1e-3) / 1e9, 1),
         "fused_vs_reshard_plus_pack": round((reshard_avg + mean(p_ms)) / mean(f_ms), 3),
         "fused_outputs_consistent": fused_ok,
+        "weight_sync_fp32_tp4pp1_to_bf16_tp2pp2_ms": round(sync_ms, 4),
+        "weight_sync_GBps": round(sync_bytes / (sync_ms * 1e-3) / 1e9, 1),
         "plan_compile_ms": round(plan_ms, 3),
         "copy_ceiling_GBps": round(copy_bytes / (copy_ms * 1e-3) / 1e9, 1),
         "roofline": {

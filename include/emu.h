@@ -151,7 +151,7 @@ typedef enum {
                                 every eighth tile (default 1) */
   EMU_OPT_NONTEMPORAL = 2,   /* 1 = streaming (non-temporal) loads and stores (default 1) */
   EMU_OPT_LDS_STAGING = 3,   /* 1 = stage each tile through LDS between load and store (default 0) */
-  EMU_OPT_BUCKET_WG_PER_CU = 4 /* pack/unpack grid: workgroups per compute unit (default 16) */
+  EMU_OPT_BUCKET_WG_PER_CU = 4 /* pack/unpack grid: workgroups per compute unit (default 32) */
 } emu_option;
 
 /* Library version (EMU_ABI_VERSION). */

@@ -224,7 +224,7 @@ __device__ __forceinline__ void wg_copy_bytes(const uint8_t* s, uint8_t* d, uint
 #define EMU_BUCKET_WAVES_PER_EU 4
 #endif
 #ifndef EMU_BUCKET_UNROLL
-#define EMU_BUCKET_UNROLL 16
+#define EMU_BUCKET_UNROLL 8
 #endif
 #ifndef EMU_SHIFT_UNROLL
 #define EMU_SHIFT_UNROLL 4

@@ -13,7 +13,10 @@ namespace emu {
 constexpr uint32_t kPlanMagic = 0x454d5550u;  // "EMUP"
 constexpr int kThreads = 256;                 // workgroup size of every kernel (4 wave64s)
 constexpr int kMaxRankTensors = 2048;         // per-rank tensor offsets live in LDS during pack/unpack
-constexpr uint64_t kChunkBytes = 65536;       // pack/unpack work unit, in stream bytes
+#ifndef EMU_CHUNK_BYTES
+#define EMU_CHUNK_BYTES 32768
+#endif
+constexpr uint64_t kChunkBytes = EMU_CHUNK_BYTES;  // pack/unpack work unit, in stream bytes
 constexpr uint64_t kWsAlign = 256;
 
 // Segment execution modes. Every "vec" mode needs src/dst offsets, strides and the run to be

@@ -47,7 +47,7 @@ bool plan_live(const Plan* p) {
   return g_plans.count(p) && p->magic == kPlanMagic;
 }
 
-static std::atomic<int64_t> g_opt[5] = {{4}, {1}, {1}, {0}, {16}};
+static std::atomic<int64_t> g_opt[5] = {{4}, {1}, {1}, {0}, {32}};
 
 int64_t option(int32_t key) { return g_opt[key].load(std::memory_order_relaxed); }
 
