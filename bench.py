@@ -90,6 +90,24 @@ def cpu_baseline(seed, layers):
                       f"input generation excluded"}
 
 
+def dag_planning(emu):
+    """Host-side transition-DAG planning for four model-stages on 1,024 GPUs (8 per node): rollout
+    TP4 -> TP8, reward/reference PP2 -> PP4, actor training PP4 -> PP2 on fewer GPUs, critic training
+    DP 64 -> 80 onto the GPUs the actor releases. Median planning time of 20 runs."""
+    def s(kind, tp, pp, dp, gpus, ttp, tpp, tdp, tg, state):
+        return dict(kind=kind, tp=tp, pp=pp, dp=dp, gpus=list(gpus), tgt_tp=ttp, tgt_pp=tpp, tgt_dp=tdp,
+                    tgt_gpus=list(tg), state_bytes=state)
+    stages = [s(0, 4, 1, 128, range(512), 8, 1, 64, range(512), 16e9),
+              s(1, 4, 2, 32, range(512, 768), 4, 4, 16, range(512, 768), 16e9),
+              s(2, 4, 4, 32, range(512), 4, 2, 48, range(384), 64e9),
+              s(2, 4, 2, 64, range(512, 1024), 4, 2, 80, range(384, 1024), 64e9)]
+    runs = [emu.dag_plan(stages) for _ in range(20)]
+    r = runs[0]
+    return {"gpus": 1024, "primitives": len(r["nodes"]), "edges": len(r["edges"]),
+            "resource_edges": r["n_resource_edges"], "l_tran_s": round(r["l_tran"], 4),
+            "plan_ms": round(sorted(x["plan_ms"] for x in runs)[10], 4)}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -276,6 +294,7 @@ def main():
         "weight_sync_fp32_tp4pp1_to_bf16_tp2pp2_ms": round(sync_ms, 4),
         "weight_sync_GBps": round(sync_bytes / (sync_ms * 1e-3) / 1e9, 1),
         "plan_compile_ms": round(plan_ms, 3),
+        "transition_dag_1024_gpus": dag_planning(emu),
         "copy_ceiling_GBps": round(copy_bytes / (copy_ms * 1e-3) / 1e9, 1),
         "roofline": {
             "bound": "hbm",

@@ -73,7 +73,8 @@ typedef enum {
   EMU_ERR_HIP = -8,         /* the HIP runtime reported an error (message in emu_last_error) */
   EMU_ERR_HANDLE = -9,      /* not a live plan handle (NULL, freed, or foreign) */
   EMU_ERR_RANGE = -10,      /* an index or side argument is out of range */
-  EMU_ERR_ARG = -11         /* another argument is invalid (message in emu_last_error) */
+  EMU_ERR_ARG = -11,        /* another argument is invalid (message in emu_last_error) */
+  EMU_ERR_INFEASIBLE = -12  /* no deadlock-free transition DAG exists for the target plan */
 } emu_status;
 
 typedef enum { EMU_BF16 = 0, EMU_FP32 = 1 } emu_dtype;                       /* 2 / 4 bytes */
@@ -219,6 +220,83 @@ int emu_pack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, uin
 /* The inverse of emu_pack_buckets: buckets -> that side's tensors. */
 int emu_unpack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, uint64_t bucket_bytes,
                        const uint64_t* d_bucket_ptrs, const uint64_t* d_tensor_ptrs, void* hip_stream);
+
+/* ------------------------------------------------------------------------------------------------
+ * Transition-DAG planner (host only). From a current to a target plan of several model-stages: the
+ * Split / Destroy / Extend / Merge primitives that carry each model-stage's EMU collection over through
+ * the largest common layout T_sub, the resource-dependency edges between model-stages that hand GPUs to
+ * each other, and the DAG's critical-path cost L_tran (paper section 6.1, decomposition and DAG
+ * construction; L_tran from bytes, link bandwidth and communicator setup, section 6 introduction).
+ *
+ * Readings implemented (the paper gives no listing):
+ *   - T_sub = (gcd(tp, tgt_tp), gcd(pp, tgt_pp)); a (tp, pp) unit splits into (tp/tps)(pp/pps) sub-units,
+ *     sub-unit (a, b) holding the unit's ranks (a*tps + t', b*pps + p') at its rank (t', p').
+ *   - Sub-units whose GPUs all lie in the target GPU set are kept (first fit, as many as the target
+ *     needs); the others are destroyed, each only after any Extend copying from it.
+ *   - Missing sub-units are extended onto the target GPUs no kept sub-unit holds (ascending ids), each
+ *     copied from a replica on a disjoint GPU set (cyclic first fit).
+ *   - Every (tgt_tp / tps)(tgt_pp / pps) sub-units (kept first, then extended) merge into one target unit.
+ *   - Model-stages of one stage kind run concurrently and hold disjoint GPUs: an Extend onto a GPU
+ *     another such model-stage holds waits for the Destroy that releases it (resource edge), resolved
+ *     in generation -> inference -> training order; if that Destroy depends on the Extend, no
+ *     deadlock-free order exists and emu_dag_plan returns EMU_ERR_INFEASIBLE.
+ *   - Costs: Split = setup + (shard_sub - shard_cur)/bw(unit); Extend = setup + max over rank pairs of
+ *     shard_sub/bw(pair); Merge = shard_target/hbm_bw; Destroy = 0; bw is intra-node when every GPU
+ *     involved sits in one node (id / gpus_per_node), else inter-node. L_tran is the longest path.
+ * ------------------------------------------------------------------------------------------------ */
+
+typedef enum { EMU_STAGE_GENERATION = 0, EMU_STAGE_INFERENCE = 1, EMU_STAGE_TRAINING = 2 } emu_stage_kind;
+typedef enum { EMU_PRIM_SPLIT = 0, EMU_PRIM_DESTROY = 1, EMU_PRIM_EXTEND = 2, EMU_PRIM_MERGE = 3 } emu_primitive;
+
+typedef struct {
+  int32_t kind;                    /* emu_stage_kind */
+  int32_t tp, pp, dp;              /* current layout and number of units */
+  int32_t tgt_tp, tgt_pp, tgt_dp;  /* target */
+  int32_t reserved;
+  const int32_t* gpus;             /* dp*tp*pp current GPU ids, unit-major, rank order r = p*tp + t */
+  const int32_t* tgt_gpus;         /* tgt_dp*tgt_tp*tgt_pp distinct ids: the target GPU set */
+  double state_bytes;              /* logical state (parameters + optimizer) of one replica */
+} emu_stage_transition_t;
+
+typedef struct {
+  int32_t gpus_per_node, reserved;
+  double intra_bw, inter_bw;       /* bytes/s per GPU pair, inside a node / across nodes */
+  double hbm_bw;                   /* bytes/s of a local copy */
+  double setup_s;                  /* communicator setup per collective */
+} emu_link_model_t;
+
+typedef struct {
+  int32_t prim, stage;             /* emu_primitive, model-stage index */
+  int32_t unit;                    /* SPLIT: current unit; DESTROY: sub-unit; EXTEND: new sub-unit slot;
+                                      MERGE: target unit */
+  int32_t src;                     /* EXTEND: sub-unit copied from; otherwise -1 */
+  int32_t gpu_first, n_gpus;       /* the primitive's GPUs: emu_dag_gpus entries [gpu_first, +n_gpus) */
+  double cost_s, start_s, finish_s;
+} emu_dag_node_t;
+
+typedef struct { int32_t from, to, resource, reserved; } emu_dag_edge_t;  /* resource: cross-stage edge */
+
+typedef struct {
+  int32_t n_nodes, n_edges, n_resource_edges, n_gpu_entries;
+  double l_tran_s;                 /* critical-path cost of the transition */
+  double plan_ms;                  /* host time emu_dag_plan spent building the DAG */
+} emu_dag_info_t;
+
+typedef struct emu_dag_s* emu_dag_t;
+
+/* Plan the transition of n_stages model-stages. Returns EMU_ERR_ARG for invalid input (including
+ * overlapping GPU sets of two model-stages of one kind), EMU_ERR_INFEASIBLE when no deadlock-free DAG
+ * exists. Nodes are listed per model-stage in input order (Splits, Destroys, Extends, Merges); edges are
+ * ordered by (to, from). */
+int emu_dag_plan(const emu_stage_transition_t* stages, int32_t n_stages, const emu_link_model_t* links,
+                 emu_dag_t* out);
+int emu_dag_free(emu_dag_t dag);
+int emu_dag_info(emu_dag_t dag, emu_dag_info_t* out);
+int emu_dag_nodes(emu_dag_t dag, int32_t first, int32_t count, emu_dag_node_t* out);
+int emu_dag_edges(emu_dag_t dag, int32_t first, int32_t count, emu_dag_edge_t* out);
+int emu_dag_gpus(emu_dag_t dag, int32_t first, int32_t count, int32_t* out);
+/* GPU ids of target unit `unit` of model-stage `stage`, in rank order (tgt_tp*tgt_pp entries). */
+int emu_dag_target_unit(emu_dag_t dag, int32_t stage, int32_t unit, int32_t* gpus_out);
 
 #ifdef __cplusplus
 }

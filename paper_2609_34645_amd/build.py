@@ -38,7 +38,7 @@ def _run(cmd, verbose):
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     objs = []
-    for src, lang in (("emu_plan.cpp", "c++"), ("emu_exec.hip", "hip")):
+    for src, lang in (("emu_plan.cpp", "c++"), ("emu_transition.cpp", "c++"), ("emu_exec.hip", "hip")):
         obj = os.path.join(BUILD, src + ".o")
         _run([HIPCC, "-x", lang, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
         objs.append(obj)

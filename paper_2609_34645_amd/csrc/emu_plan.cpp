@@ -543,6 +543,7 @@ const char* emu_status_str(int s) {
     case EMU_ERR_HANDLE: return "EMU_ERR_HANDLE";
     case EMU_ERR_RANGE: return "EMU_ERR_RANGE";
     case EMU_ERR_ARG: return "EMU_ERR_ARG";
+    case EMU_ERR_INFEASIBLE: return "EMU_ERR_INFEASIBLE";
     default: return "EMU_ERR_UNKNOWN";
   }
 }

@@ -35,7 +35,9 @@ KINDS = ["embed", "attn_norm", "qkv", "q", "k", "v", "o", "mlp_norm", "gate_up",
 
 STATUS = {0: "EMU_OK", -1: "EMU_ERR_NULL", -2: "EMU_ERR_LAYOUT", -3: "EMU_ERR_MISMATCH",
           -4: "EMU_ERR_UNSUPPORTED", -5: "EMU_ERR_WORKSPACE", -6: "EMU_ERR_BUCKET", -7: "EMU_ERR_ALIGN",
-          -8: "EMU_ERR_HIP", -9: "EMU_ERR_HANDLE", -10: "EMU_ERR_RANGE", -11: "EMU_ERR_ARG"}
+          -8: "EMU_ERR_HIP", -9: "EMU_ERR_HANDLE", -10: "EMU_ERR_RANGE", -11: "EMU_ERR_ARG",
+          -12: "EMU_ERR_INFEASIBLE"}
+ERR_INFEASIBLE = -12
 
 
 class c_model(ctypes.Structure):
@@ -71,6 +73,34 @@ class c_segment(ctypes.Structure):
                 ("src_offset", ctypes.c_uint64), ("dst_offset", ctypes.c_uint64),
                 ("src_stride", ctypes.c_uint64), ("dst_stride", ctypes.c_uint64),
                 ("rows", ctypes.c_uint64), ("run", ctypes.c_uint64), ("src_run", ctypes.c_uint64)]
+
+
+class c_stage_transition(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("tp", ctypes.c_int32), ("pp", ctypes.c_int32), ("dp", ctypes.c_int32),
+                ("tgt_tp", ctypes.c_int32), ("tgt_pp", ctypes.c_int32), ("tgt_dp", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("gpus", ctypes.POINTER(ctypes.c_int32)),
+                ("tgt_gpus", ctypes.POINTER(ctypes.c_int32)), ("state_bytes", ctypes.c_double)]
+
+
+class c_link_model(ctypes.Structure):
+    _fields_ = [("gpus_per_node", ctypes.c_int32), ("reserved", ctypes.c_int32), ("intra_bw", ctypes.c_double),
+                ("inter_bw", ctypes.c_double), ("hbm_bw", ctypes.c_double), ("setup_s", ctypes.c_double)]
+
+
+class c_dag_node(ctypes.Structure):
+    _fields_ = [("prim", ctypes.c_int32), ("stage", ctypes.c_int32), ("unit", ctypes.c_int32), ("src", ctypes.c_int32),
+                ("gpu_first", ctypes.c_int32), ("n_gpus", ctypes.c_int32), ("cost_s", ctypes.c_double),
+                ("start_s", ctypes.c_double), ("finish_s", ctypes.c_double)]
+
+
+class c_dag_edge(ctypes.Structure):
+    _fields_ = [("from_", ctypes.c_int32), ("to", ctypes.c_int32), ("resource", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+class c_dag_info(ctypes.Structure):
+    _fields_ = [("n_nodes", ctypes.c_int32), ("n_edges", ctypes.c_int32), ("n_resource_edges", ctypes.c_int32),
+                ("n_gpu_entries", ctypes.c_int32), ("l_tran_s", ctypes.c_double), ("plan_ms", ctypes.c_double)]
 
 
 class EmuError(RuntimeError):
@@ -110,6 +140,14 @@ def load(path: str = LIB_PATH):
         "emu_bucket_layout": ([P, I32, U64, I32, ctypes.POINTER(U64), ctypes.POINTER(U64)], ctypes.c_int),
         "emu_pack_buckets": ([P, V, I32, U64, V, V, V], ctypes.c_int),
         "emu_unpack_buckets": ([P, V, I32, U64, V, V, V], ctypes.c_int),
+        "emu_dag_plan": ([ctypes.POINTER(c_stage_transition), I32, ctypes.POINTER(c_link_model), ctypes.POINTER(P)],
+                         ctypes.c_int),
+        "emu_dag_free": ([P], ctypes.c_int),
+        "emu_dag_info": ([P, ctypes.POINTER(c_dag_info)], ctypes.c_int),
+        "emu_dag_nodes": ([P, I32, I32, ctypes.POINTER(c_dag_node)], ctypes.c_int),
+        "emu_dag_edges": ([P, I32, I32, ctypes.POINTER(c_dag_edge)], ctypes.c_int),
+        "emu_dag_gpus": ([P, I32, I32, ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
+        "emu_dag_target_unit": ([P, I32, I32, ctypes.POINTER(ctypes.c_int32)], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -331,3 +369,57 @@ def ptr_table(tensors, device=None):
     if bad:
         raise EmuError(-7, f"tensors {bad[:4]} are not 16-byte aligned")
     return torch.tensor(addrs, dtype=torch.int64, device=device or "cuda")
+
+
+# ----------------------------------------------------------------------------------------------------
+# transition-DAG planner (host only)
+# ----------------------------------------------------------------------------------------------------
+
+PRIMS = ["split", "destroy", "extend", "merge"]
+
+
+def dag_plan(stages, gpus_per_node=8, intra_bw=300e9, inter_bw=25e9, hbm_bw=5e12, setup_s=0.05):
+    """Plan a transition (``emu_dag_plan``). ``stages``: sequence of dicts with kind (0 generation,
+    1 inference, 2 training), tp, pp, dp, gpus, tgt_tp, tgt_pp, tgt_dp, tgt_gpus, state_bytes.
+
+    Returns dict(nodes=[dict(prim, stage, unit, src, gpus, cost, start, finish)], edges=[(from, to,
+    resource)], target_units=[[gpu list per target unit] per stage], l_tran, n_resource_edges, plan_ms).
+    Raises EmuError (code ERR_INFEASIBLE when no deadlock-free DAG exists)."""
+    lib = load()
+    n = len(stages)
+    arr = (c_stage_transition * n)()
+    keep = []
+    for i, s in enumerate(stages):
+        g = (ctypes.c_int32 * len(s["gpus"]))(*s["gpus"])
+        tg = (ctypes.c_int32 * len(s["tgt_gpus"]))(*s["tgt_gpus"])
+        keep += [g, tg]
+        arr[i] = c_stage_transition(s["kind"], s["tp"], s["pp"], s["dp"], s["tgt_tp"], s["tgt_pp"], s["tgt_dp"], 0,
+                                    g, tg, float(s["state_bytes"]))
+    links = c_link_model(gpus_per_node, 0, intra_bw, inter_bw, hbm_bw, setup_s)
+    h = ctypes.c_void_p()
+    check(lib.emu_dag_plan(arr, n, ctypes.byref(links), ctypes.byref(h)))
+    try:
+        info = c_dag_info()
+        check(lib.emu_dag_info(h, ctypes.byref(info)))
+        nodes = (c_dag_node * max(1, info.n_nodes))()
+        edges = (c_dag_edge * max(1, info.n_edges))()
+        flat = (ctypes.c_int32 * max(1, info.n_gpu_entries))()
+        check(lib.emu_dag_nodes(h, 0, info.n_nodes, nodes))
+        check(lib.emu_dag_edges(h, 0, info.n_edges, edges))
+        check(lib.emu_dag_gpus(h, 0, info.n_gpu_entries, flat))
+        out_nodes = [dict(prim=nd.prim, stage=nd.stage, unit=nd.unit, src=nd.src,
+                          gpus=list(flat[nd.gpu_first:nd.gpu_first + nd.n_gpus]), cost=nd.cost_s,
+                          start=nd.start_s, finish=nd.finish_s) for nd in nodes[:info.n_nodes]]
+        out_edges = [(ed.from_, ed.to, ed.resource) for ed in edges[:info.n_edges]]
+        units = []
+        for i, s in enumerate(stages):
+            per = []
+            for u in range(s["tgt_dp"]):
+                buf = (ctypes.c_int32 * (s["tgt_tp"] * s["tgt_pp"]))()
+                check(lib.emu_dag_target_unit(h, i, u, buf))
+                per.append(list(buf))
+            units.append(per)
+        return dict(nodes=out_nodes, edges=out_edges, target_units=units, l_tran=info.l_tran_s,
+                    n_resource_edges=info.n_resource_edges, plan_ms=info.plan_ms)
+    finally:
+        lib.emu_dag_free(h)
