@@ -152,7 +152,11 @@ typedef enum {
                                 every eighth tile (default 1) */
   EMU_OPT_NONTEMPORAL = 2,   /* 1 = streaming (non-temporal) loads and stores (default 1) */
   EMU_OPT_LDS_STAGING = 3,   /* 1 = stage each tile through LDS between load and store (default 0) */
-  EMU_OPT_BUCKET_WG_PER_CU = 4 /* pack/unpack grid: workgroups per compute unit (default 32) */
+  EMU_OPT_BUCKET_WG_PER_CU = 4, /* persistent pack/unpack grid: workgroups per compute unit (default 32) */
+  EMU_OPT_BUCKET_TILES = 5   /* 1 = pack/unpack with one workgroup per 16 KB stream chunk (upload-time
+                                chunk map; default); 0 = the persistent kernel that scans each rank's
+                                tensor sizes into LDS (also used when the chunk map cannot encode a side:
+                                more than 4096 ranks or 2^20 tensors on one rank) */
 } emu_option;
 
 /* Library version (EMU_ABI_VERSION). */

@@ -480,6 +480,55 @@ __global__ __launch_bounds__(kThreads, EMU_BUCKET_WAVES_PER_EU) void k_buckets(c
   }
 }
 
+// Tile-per-workgroup variant: one workgroup per 16 KB chunk of one rank's stream (XCD-contiguous
+// order). The upload-time map gives the chunk's rank and the tensor holding its first byte; each wave
+// computes the rank's first bucket, the sum over earlier ranks of ceil(bytes / B), with a wave64
+// reduction (so no barrier is needed). The chunk is then cut at tensor and bucket boundaries as above.
+template <bool UNPACK, bool NT, int U>
+__global__ __launch_bounds__(kThreads, EMU_RESHARD_WAVES_PER_EU) void k_buckets_tile(
+    const uint64_t* __restrict__ stream_off, const uint32_t* __restrict__ rank_first,
+    const uint64_t* __restrict__ rank_bytes, const uint64_t* __restrict__ tile_first,
+    const uint32_t* __restrict__ tile_map, uint32_t ntile, uint64_t B, const uint64_t* __restrict__ tensor_ptrs,
+    const uint64_t* __restrict__ bucket_ptrs) {
+  const uint32_t per = gridDim.x / kXcds;  // the host launches a multiple of kXcds workgroups
+  const uint32_t c = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+  if (c >= ntile) return;
+  const uint32_t m = tile_map[c];
+  const uint32_t r = m >> kMapTensorBits;
+  uint32_t ti = m & ((1u << kMapTensorBits) - 1);
+  const uint32_t t0 = rank_first[r], nt = rank_first[r + 1] - t0;
+  const uint64_t S = rank_bytes[r];
+  const uint64_t start = (c - tile_first[r]) * kTileChunkBytes;
+  const uint64_t end = start + kTileChunkBytes < S ? start + kTileChunkBytes : S;
+  const uint32_t lane = threadIdx.x & 63;
+  uint64_t acc = 0;
+  for (uint32_t q = lane; q < r; q += 64) acc += (rank_bytes[q] + B - 1) / B;
+  const uint64_t bucket0 = uniform64(wave_sum(acc));
+  uint64_t k = start / B;
+  uint64_t kend = (k + 1) * B;
+  uint64_t pos = start;
+  while (pos < end) {
+    const uint64_t toff = stream_off[t0 + ti];
+    const uint64_t tend = ti + 1 < nt ? stream_off[t0 + ti + 1] : S;
+    if (tend <= pos) {  // the chunk moves on into the next tensor (or past an empty one)
+      ++ti;
+      continue;
+    }
+    uint64_t pend = end < tend ? end : tend;
+    if (kend < pend) pend = kend;
+    uint8_t* tp = reinterpret_cast<uint8_t*>(tensor_ptrs[t0 + ti]) + (pos - toff);
+    uint8_t* bp = reinterpret_cast<uint8_t*>(bucket_ptrs[bucket0 + k]) + (pos - k * B);
+    const uint32_t n = uint32_t(pend - pos);
+    if constexpr (UNPACK) wg_copy_bytes<U, kShiftUnroll, NT, false>(bp, tp, n);
+    else wg_copy_bytes<U, kShiftUnroll, NT, false>(tp, bp, n);
+    pos = pend;
+    if (pos == kend) {
+      ++k;
+      kend += B;
+    }
+  }
+}
+
 // ------------------------------------------------------------------------------------------------
 // launch helpers
 // ------------------------------------------------------------------------------------------------
@@ -581,6 +630,21 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
   const uint64_t* cf = reinterpret_cast<const uint64_t*>(w + t.off_chunk_first);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool ntm = option(EMU_OPT_NONTEMPORAL) != 0;
+  if (option(EMU_OPT_BUCKET_TILES) != 0 && t.n_tiles > 0) {
+    const uint64_t* so = reinterpret_cast<const uint64_t*>(w + t.off_stream);
+    const uint64_t* tf = reinterpret_cast<const uint64_t*>(w + t.off_tile_first);
+    const uint32_t* tm = reinterpret_cast<const uint32_t*>(w + t.off_tile_map);
+    const uint32_t nt = uint32_t(t.n_tiles);
+    const dim3 g((nt + kXcds - 1) / kXcds * kXcds);
+    if (unpack) {
+      if (ntm) hipLaunchKernelGGL((k_buckets_tile<true, true, 4>), g, dim3(kThreads), 0, st, so, rf, rb, tf, tm, nt, B, tptr, bptr);
+      else hipLaunchKernelGGL((k_buckets_tile<true, false, 4>), g, dim3(kThreads), 0, st, so, rf, rb, tf, tm, nt, B, tptr, bptr);
+    } else {
+      if (ntm) hipLaunchKernelGGL((k_buckets_tile<false, true, 4>), g, dim3(kThreads), 0, st, so, rf, rb, tf, tm, nt, B, tptr, bptr);
+      else hipLaunchKernelGGL((k_buckets_tile<false, false, 4>), g, dim3(kThreads), 0, st, so, rf, rb, tf, tm, nt, B, tptr, bptr);
+    }
+    return hip_check(unpack ? "emu_unpack_buckets launch" : "emu_pack_buckets launch");
+  }
   if (unpack) {
     if (ntm) hipLaunchKernelGGL((k_buckets<true, true, kBucketUnroll>), dim3(uint32_t(grid)), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);
     else hipLaunchKernelGGL((k_buckets<true, false, kBucketUnroll>), dim3(uint32_t(grid)), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);

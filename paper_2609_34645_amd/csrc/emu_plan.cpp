@@ -47,7 +47,7 @@ bool plan_live(const Plan* p) {
   return g_plans.count(p) && p->magic == kPlanMagic;
 }
 
-static std::atomic<int64_t> g_opt[5] = {{4}, {1}, {1}, {0}, {32}};
+static std::atomic<int64_t> g_opt[6] = {{4}, {1}, {1}, {0}, {32}, {1}};
 
 int64_t option(int32_t key) { return g_opt[key].load(std::memory_order_relaxed); }
 
@@ -473,12 +473,40 @@ static int finalize(Plan& P) {
   uint64_t off = 0;
   w.off_segs = off; off = align(off + P.dsegs.size() * sizeof(DevSeg));
   w.off_tilemap = off; off = align(off + tilemap.size() * 4);
+  // per side: tile chunk -> (rank, tensor) map for the tile-per-workgroup pack/unpack kernel
+  std::vector<uint32_t> tmap[2];
+  std::vector<uint64_t> tfirst[2];
+  for (int sd = 0; sd < 2; ++sd) {
+    const SideInfo& s = P.side[sd];
+    tfirst[sd].assign(s.nranks + 1, 0);
+    bool encodable = s.nranks <= (1 << (32 - kMapTensorBits));
+    for (int r = 0; r < s.nranks && encodable; ++r) {
+      const uint32_t t0 = s.rank_first[r], nt = s.rank_first[r + 1] - t0;
+      if (nt > (1u << kMapTensorBits)) encodable = false;
+      const uint64_t nch = (s.rank_bytes[r] + kTileChunkBytes - 1) / kTileChunkBytes;
+      tfirst[sd][r + 1] = tfirst[sd][r] + nch;
+      uint32_t ti = 0;
+      for (uint64_t j = 0; j < nch && encodable; ++j) {
+        const uint64_t pos = j * kTileChunkBytes;
+        while (ti + 1 < nt && s.tensors[t0 + ti + 1].stream_offset <= pos) ++ti;
+        tmap[sd].push_back((uint32_t(r) << kMapTensorBits) | ti);
+      }
+    }
+    if (!encodable || tmap[sd].size() > 0x7fffffffull) {
+      tmap[sd].clear();
+      std::fill(tfirst[sd].begin(), tfirst[sd].end(), 0);
+    }
+  }
   for (int sd = 0; sd < 2; ++sd) {
     const SideInfo& s = P.side[sd];
     w.side[sd].off_sizes = off; off = align(off + s.tensors.size() * 8);
     w.side[sd].off_rank_first = off; off = align(off + (s.nranks + 1) * 4);
     w.side[sd].off_rank_bytes = off; off = align(off + s.nranks * 8);
     w.side[sd].off_chunk_first = off; off = align(off + (s.nranks + 1) * 8);
+    w.side[sd].off_stream = off; off = align(off + s.tensors.size() * 8);
+    w.side[sd].off_tile_first = off; off = align(off + (s.nranks + 1) * 8);
+    w.side[sd].off_tile_map = off; off = align(off + tmap[sd].size() * 4);
+    w.side[sd].n_tiles = tmap[sd].size();
   }
   w.total = off;
   P.host_ws.assign(w.total, 0);
@@ -492,6 +520,10 @@ static int finalize(Plan& P) {
     std::memcpy(h + w.side[sd].off_rank_first, s.rank_first.data(), s.rank_first.size() * 4);
     std::memcpy(h + w.side[sd].off_rank_bytes, s.rank_bytes.data(), s.rank_bytes.size() * 8);
     std::memcpy(h + w.side[sd].off_chunk_first, s.chunk_first.data(), s.chunk_first.size() * 8);
+    uint64_t* so = reinterpret_cast<uint64_t*>(h + w.side[sd].off_stream);
+    for (size_t i = 0; i < s.tensors.size(); ++i) so[i] = s.tensors[i].stream_offset;
+    std::memcpy(h + w.side[sd].off_tile_first, tfirst[sd].data(), tfirst[sd].size() * 8);
+    if (!tmap[sd].empty()) std::memcpy(h + w.side[sd].off_tile_map, tmap[sd].data(), tmap[sd].size() * 4);
   }
 
   emu_plan_info_t& I = P.info;
@@ -560,6 +592,7 @@ int emu_set_option(int32_t key, int64_t value) {
       if (value < 1 || value > 64) return fail(EMU_ERR_ARG, "workgroups per CU must be in [1, 64]");
       break;
     case EMU_OPT_XCD_REMAP:
+    case EMU_OPT_BUCKET_TILES:
     case EMU_OPT_NONTEMPORAL:
     case EMU_OPT_LDS_STAGING:
       if (value != 0 && value != 1) return fail(EMU_ERR_ARG, "flag must be 0 or 1");
@@ -574,7 +607,7 @@ int emu_set_option(int32_t key, int64_t value) {
 int emu_get_option(int32_t key, int64_t* value) {
   clear_error();
   if (!value) return fail(EMU_ERR_NULL, "value is NULL");
-  if (key < 0 || key > EMU_OPT_BUCKET_WG_PER_CU) return fail(EMU_ERR_RANGE, "unknown option %d", key);
+  if (key < 0 || key > EMU_OPT_BUCKET_TILES) return fail(EMU_ERR_RANGE, "unknown option %d", key);
   *value = option(key);
   return EMU_OK;
 }

@@ -187,6 +187,12 @@ def test_8b_padded_tp8pp4_to_tp2pp2_buckets(gpu_lib):
     check_reshard(p, S, D, label="8B TP8PP4(pad)->TP2PP2")
     _pack_check(p, ws, D, 1 << 28, "buckets 2^28")
     _pack_check(p, ws, D, (1 << 28) - 2, "buckets 2^28-2 (phase-shifted)")
+    emu.set_option(emu.OPT_BUCKET_TILES, 0)
+    try:
+        _pack_check(p, ws, D, 1 << 28, "buckets 2^28, persistent kernel")
+        _pack_check(p, ws, D, (1 << 28) - 2, "buckets 2^28-2, persistent kernel")
+    finally:
+        emu.set_option(emu.OPT_BUCKET_TILES, 1)
     _pack_check(p, ws, D, 1 << 28, "fused reshard->buckets 2^28", S=S)
     _pack_check(p, ws, D, (1 << 28) - 2, "fused reshard->buckets 2^28-2", S=S)
     del D, S, ws

@@ -118,11 +118,11 @@ def test_tiny_split_and_merge_back(gpu_lib):
 
 @pytest.mark.parametrize("opts", [
     {emu.OPT_TILE_VECS: 8}, {emu.OPT_TILE_VECS: 16}, {emu.OPT_XCD_REMAP: 1},
-    {emu.OPT_BUCKET_WG_PER_CU: 1}, {emu.OPT_TILE_VECS: 16, emu.OPT_XCD_REMAP: 1},
+    {emu.OPT_BUCKET_WG_PER_CU: 1}, {emu.OPT_TILE_VECS: 16, emu.OPT_XCD_REMAP: 1}, {emu.OPT_BUCKET_TILES: 1},
     {emu.OPT_NONTEMPORAL: 0}, {emu.OPT_LDS_STAGING: 1}, {emu.OPT_LDS_STAGING: 1, emu.OPT_TILE_VECS: 16},
 ])
 def test_launch_options(gpu_lib, opts):
-    defaults = {k: emu.get_option(k) for k in range(5)}
+    defaults = {k: emu.get_option(k) for k in range(6)}
     try:
         m = emu.Model(*TINY)
         run_pair(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate"), options=opts)
@@ -163,10 +163,17 @@ def test_padded_vocab_zero_fill_and_source_pad_not_read(gpu_lib):
             assert torch.equal(x, y)
 
 
+@pytest.mark.parametrize("tiles", [0, 1], ids=["persistent", "tile_per_wg"])
 @pytest.mark.parametrize("B", [30, 1000, 4094, 65536, 65538, 1 << 20])
-def test_buckets_awkward_sizes(gpu_lib, B):
+def test_buckets_awkward_sizes(gpu_lib, B, tiles):
     m = emu.Model(*TINY)
-    run_pair(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1), bucket_sizes=(B,))
+    old = emu.get_option(emu.OPT_BUCKET_TILES)
+    emu.set_option(emu.OPT_BUCKET_TILES, tiles)
+    try:
+        run_pair(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1), bucket_sizes=(B,))
+        run_pair(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 2, 0, "bf16", "separate", "block"), bucket_sizes=(B,))
+    finally:
+        emu.set_option(emu.OPT_BUCKET_TILES, old)
 
 
 def test_buckets_source_side_and_fp32(gpu_lib):
