@@ -122,6 +122,7 @@ def main():
     ap.add_argument("--nontemporal", type=int, default=None)
     ap.add_argument("--lds", type=int, default=None)
     ap.add_argument("--bucket-wg-per-cu", type=int, default=None)
+    ap.add_argument("--wg-per-cu", type=int, default=None)
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -137,7 +138,7 @@ def main():
     emu.load()
     for opt, v in ((emu.OPT_TILE_VECS, args.tile_vecs), (emu.OPT_XCD_REMAP, args.xcd_remap),
                    (emu.OPT_NONTEMPORAL, args.nontemporal), (emu.OPT_LDS_STAGING, args.lds),
-                   (emu.OPT_BUCKET_WG_PER_CU, args.bucket_wg_per_cu)):
+                   (emu.OPT_BUCKET_WG_PER_CU, args.bucket_wg_per_cu), (emu.OPT_WG_PER_CU, args.wg_per_cu)):
         if v is not None:
             emu.set_option(opt, v)
 
@@ -310,7 +311,9 @@ def main():
                                                       ("xcd_remap", emu.OPT_XCD_REMAP),
                                                       ("nontemporal", emu.OPT_NONTEMPORAL),
                                                       ("lds_staging", emu.OPT_LDS_STAGING),
-                                                      ("bucket_wg_per_cu", emu.OPT_BUCKET_WG_PER_CU))},
+                                                      ("bucket_wg_per_cu", emu.OPT_BUCKET_WG_PER_CU),
+                                                      ("bucket_tiles", emu.OPT_BUCKET_TILES),
+                                                      ("wg_per_cu", emu.OPT_WG_PER_CU))},
         "device": {"name": props.name, "cus": props.multi_processor_count,
                    "hbm_GB": round(props.total_memory / 1e9, 1)},
         "outputs_consistent": ok,

@@ -146,17 +146,24 @@ typedef struct {
 
 /* Tuning knobs (process-wide; change them only while no emu call is running). */
 typedef enum {
-  EMU_OPT_TILE_VECS = 0,     /* 16-byte vectors per thread per tile: 4, 8 or 16 (default 4); read by
-                                emu_plan, so a plan keeps the value it was compiled with */
+  EMU_OPT_TILE_VECS = 0,     /* 16-byte vectors per thread per reshard tile: 1, 2, 4, 8 or 16, or 0 =
+                                automatic (default): 2 (8 KB tiles) for copy plans, 1 (4 KB) for
+                                converting plans. Read by emu_plan, so a plan keeps its tile size */
   EMU_OPT_XCD_REMAP = 1,     /* 1 = give each XCD one contiguous eighth of the reshard tiles instead of
                                 every eighth tile (default 1) */
   EMU_OPT_NONTEMPORAL = 2,   /* 1 = streaming (non-temporal) loads and stores (default 1) */
   EMU_OPT_LDS_STAGING = 3,   /* 1 = stage each tile through LDS between load and store (default 0) */
   EMU_OPT_BUCKET_WG_PER_CU = 4, /* persistent pack/unpack grid: workgroups per compute unit (default 32) */
-  EMU_OPT_BUCKET_TILES = 5   /* 1 = pack/unpack with one workgroup per 16 KB stream chunk (upload-time
+  EMU_OPT_BUCKET_TILES = 5,  /* 1 = pack/unpack with one workgroup per 8 KB stream chunk (upload-time
                                 chunk map; default); 0 = the persistent kernel that scans each rank's
                                 tensor sizes into LDS (also used when the chunk map cannot encode a side:
                                 more than 4096 ranks or 2^20 tensors on one rank) */
+  EMU_OPT_WG_PER_CU = 6      /* reshard and tile pack/unpack kernels: cap on the workgroups resident
+                                per compute unit, 1..8, enforced by reserving LDS per workgroup (the
+                                LDS is split in two halves, so odd caps above 1 round down to even);
+                                0 = no cap; -1 = automatic (default): 6 for 8 KB reshard tiles, 2 for
+                                larger ones, none for 4 KB tiles and for pack/unpack. Bounds the bytes
+                                in flight per CU, which sets how well HBM serves a read/write stream */
 } emu_option;
 
 /* Library version (EMU_ABI_VERSION). */

@@ -17,7 +17,10 @@ constexpr int kMaxRankTensors = 2048;         // per-rank tensor offsets live in
 #define EMU_CHUNK_BYTES 32768
 #endif
 constexpr uint64_t kChunkBytes = EMU_CHUNK_BYTES;  // pack/unpack work unit, in stream bytes
-constexpr uint64_t kTileChunkBytes = 16384;        // unit of the tile-per-workgroup pack/unpack kernel
+#ifndef EMU_TILE_CHUNK_BYTES
+#define EMU_TILE_CHUNK_BYTES 8192
+#endif
+constexpr uint64_t kTileChunkBytes = EMU_TILE_CHUNK_BYTES;  // unit of the tile-per-workgroup pack/unpack kernel
 constexpr uint32_t kMapTensorBits = 20;            // tile map entry: rank << 20 | tensor within the rank
 constexpr uint64_t kWsAlign = 256;
 
@@ -56,7 +59,7 @@ struct SideTables {
   uint64_t off_rank_bytes;   // uint64[n_ranks]     stream length of each rank
   uint64_t off_chunk_first;  // uint64[n_ranks + 1] first pack/unpack chunk of each rank
   uint64_t off_stream;       // uint64[n_tensors]   stream offset of each tensor inside its rank
-  uint64_t off_tile_first;   // uint64[n_ranks + 1] first 16 KB tile chunk of each rank
+  uint64_t off_tile_first;   // uint64[n_ranks + 1] first tile chunk (kTileChunkBytes) of each rank
   uint64_t off_tile_map;     // uint32[n_tile_chunks] rank << 20 | tensor holding the chunk's first byte
   uint64_t n_tiles;          // tile chunks of the side (0 when the map cannot encode it)
 };
@@ -84,7 +87,7 @@ struct Plan {
   SideInfo side[2];
   std::vector<emu_segment_t> segs;  // execution order
   std::vector<DevSeg> dsegs;
-  int tile_vecs = 8;                // 16-byte vectors per thread per tile
+  int tile_vecs = 2;                // 16-byte vectors per thread per tile
   int cvt = CVT_NONE;               // element conversion of the whole plan
   uint64_t tile_bytes = 0;
   uint64_t ntiles = 0;

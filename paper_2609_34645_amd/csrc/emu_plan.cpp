@@ -47,7 +47,7 @@ bool plan_live(const Plan* p) {
   return g_plans.count(p) && p->magic == kPlanMagic;
 }
 
-static std::atomic<int64_t> g_opt[6] = {{4}, {1}, {1}, {0}, {32}, {1}};
+static std::atomic<int64_t> g_opt[7] = {{0}, {1}, {1}, {0}, {32}, {1}, {-1}};
 
 int64_t option(int32_t key) { return g_opt[key].load(std::memory_order_relaxed); }
 
@@ -586,7 +586,11 @@ int emu_set_option(int32_t key, int64_t value) {
   clear_error();
   switch (key) {
     case EMU_OPT_TILE_VECS:
-      if (value != 4 && value != 8 && value != 16) return fail(EMU_ERR_ARG, "tile vectors must be 4, 8 or 16");
+      if (value != 0 && value != 1 && value != 2 && value != 4 && value != 8 && value != 16)
+        return fail(EMU_ERR_ARG, "tile vectors must be 0 (automatic), 1, 2, 4, 8 or 16");
+      break;
+    case EMU_OPT_WG_PER_CU:
+      if (value < -1 || value > 8) return fail(EMU_ERR_ARG, "resident workgroups per CU must be in [-1, 8]");
       break;
     case EMU_OPT_BUCKET_WG_PER_CU:
       if (value < 1 || value > 64) return fail(EMU_ERR_ARG, "workgroups per CU must be in [1, 64]");
@@ -607,7 +611,7 @@ int emu_set_option(int32_t key, int64_t value) {
 int emu_get_option(int32_t key, int64_t* value) {
   clear_error();
   if (!value) return fail(EMU_ERR_NULL, "value is NULL");
-  if (key < 0 || key > EMU_OPT_BUCKET_TILES) return fail(EMU_ERR_RANGE, "unknown option %d", key);
+  if (key < 0 || key > EMU_OPT_WG_PER_CU) return fail(EMU_ERR_RANGE, "unknown option %d", key);
   *value = option(key);
   return EMU_OK;
 }
@@ -630,8 +634,12 @@ int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out) 
   Plan* P = new (std::nothrow) Plan();
   if (!P) return fail(EMU_ERR_ARG, "out of host memory");
   try {
-    P->tile_vecs = int(option(EMU_OPT_TILE_VECS));
     P->cvt = src->dtype == dst->dtype ? CVT_NONE : (src->dtype == EMU_FP32 ? CVT_F32_BF16 : CVT_BF16_F32);
+    // automatic tile size: 8 KB tiles for copies, 4 KB for converting plans (whose tiles read up to
+    // twice their bytes), the sizes that ran fastest on MI355X together with the residency rule of the
+    // launch (EMU_OPT_WG_PER_CU)
+    const int64_t tv = option(EMU_OPT_TILE_VECS);
+    P->tile_vecs = tv > 0 ? int(tv) : (P->cvt == CVT_NONE ? 2 : 1);
     std::vector<std::vector<Block>> sb, db;
     rc = build_side(*src, P->side[0], sb);
     if (!rc) rc = build_side(*dst, P->side[1], db);

@@ -120,9 +120,11 @@ def test_tiny_split_and_merge_back(gpu_lib):
     {emu.OPT_TILE_VECS: 8}, {emu.OPT_TILE_VECS: 16}, {emu.OPT_XCD_REMAP: 1},
     {emu.OPT_BUCKET_WG_PER_CU: 1}, {emu.OPT_TILE_VECS: 16, emu.OPT_XCD_REMAP: 1}, {emu.OPT_BUCKET_TILES: 1},
     {emu.OPT_NONTEMPORAL: 0}, {emu.OPT_LDS_STAGING: 1}, {emu.OPT_LDS_STAGING: 1, emu.OPT_TILE_VECS: 16},
+    {emu.OPT_TILE_VECS: 1}, {emu.OPT_TILE_VECS: 2, emu.OPT_WG_PER_CU: 6}, {emu.OPT_WG_PER_CU: 0},
+    {emu.OPT_WG_PER_CU: 1, emu.OPT_LDS_STAGING: 1}, {emu.OPT_WG_PER_CU: 8, emu.OPT_BUCKET_TILES: 0},
 ])
 def test_launch_options(gpu_lib, opts):
-    defaults = {k: emu.get_option(k) for k in range(6)}
+    defaults = {k: emu.get_option(k) for k in range(7)}
     try:
         m = emu.Model(*TINY)
         run_pair(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate"), options=opts)
