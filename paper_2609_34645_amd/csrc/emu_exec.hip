@@ -232,7 +232,7 @@ __device__ __forceinline__ void wg_copy_bytes(const uint8_t* s, uint8_t* d, uint
 #ifndef EMU_BUCKET_TILE_VECS
 #define EMU_BUCKET_TILE_VECS 2
 #endif
-constexpr int kXcds = 8;           // XCDs of an MI355X; workgroups are dealt to them round-robin
+constexpr int kXcds = int(kXcdCount);  // workgroups are dealt to the XCDs round-robin
 constexpr int kGeneralUnroll = 2;  // byte-granular reshard segments (misaligned runs; rare)
 constexpr int kBucketUnroll = EMU_BUCKET_UNROLL;
 constexpr int kShiftUnroll = EMU_SHIFT_UNROLL;
@@ -348,11 +348,12 @@ __device__ __forceinline__ void run_tile(const DevSeg& g, uint64_t lt, const uin
 
 // One workgroup per tile. With XCD remapping, the round-robin dispatch of workgroups over the 8 XCDs is
 // undone: XCD x (workgroups x, x+8, ...) works through one contiguous eighth of the tile range, so each
-// XCD's L2 sees one stream instead of every eighth tile of all of them.
-template <int U, bool NT, bool LDS, bool XCD, int CVT>
+// XCD's L2 sees one stream instead of every eighth tile of all of them. ZERO instances run the map's
+// zero-fill section, the others its copy section.
+template <int U, bool NT, bool LDS, bool XCD, int CVT, bool ZERO>
 __global__ __launch_bounds__(kThreads, EMU_RESHARD_WAVES_PER_EU) void k_reshard(const DevSeg* __restrict__ segs,
                                                                              const uint32_t* __restrict__ tilemap,
-                                                                             uint64_t tile_base, uint32_t ntiles,
+                                                                             uint64_t tile_base,
                                                                              const uint64_t* __restrict__ src_ptrs,
                                                                              const uint64_t* __restrict__ dst_ptrs) {
   extern __shared__ v4u stage[];
@@ -361,13 +362,17 @@ __global__ __launch_bounds__(kThreads, EMU_RESHARD_WAVES_PER_EU) void k_reshard(
     const uint32_t per = gridDim.x / kXcds;  // the host launches a multiple of kXcds workgroups
     local = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
   }
-  if (local >= ntiles) return;
+  // Each section of the map is padded with kNoSeg to the grid's size, so no bounds check precedes
+  // the map load. Every path of a copy instance reads the source pointer, so its load issues together
+  // with the destination pointer's, right after the descriptor: the chain before the first data load
+  // is kernel arguments, map entry, descriptor, pointers.
   const uint64_t tile = tile_base + local;
   const uint32_t si = tilemap[tile];
+  if (si == kNoSeg) return;
   const DevSeg g = segs[si];
-  const uint64_t lt = tile - g.tile0;
   uint8_t* db = reinterpret_cast<uint8_t*>(dst_ptrs[g.dst_idx]);
-  if (g.mode & SEG_ZERO) {
+  const uint64_t lt = tile - g.tile0;
+  if constexpr (ZERO) {
     run_tile<U, NT, true, LDS, CVT_NONE>(g, lt, nullptr, db, stage);
   } else {
     const uint8_t* sb = reinterpret_cast<const uint8_t*>(src_ptrs[g.src_idx]);
@@ -584,47 +589,60 @@ static int hip_check(const char* what) {
   return EMU_OK;
 }
 
-template <int U, bool NT, bool LDS, bool XCD, int CVT>
-static void launch_reshard(hipStream_t st, const DevSeg* segs, const uint32_t* tm, uint64_t ntiles, const uint64_t* sp,
-                           const uint64_t* dp) {
+// Launches k_reshard over the map section [first, first + count); first is a multiple of kXcds and the
+// section is padded to one.
+template <int U, bool NT, bool LDS, bool XCD, int CVT, bool ZERO>
+static void launch_reshard(hipStream_t st, const DevSeg* segs, const uint32_t* tm, uint64_t first, uint64_t count,
+                           const uint64_t* sp, const uint64_t* dp) {
   const size_t lds = occupancy_lds(LDS ? size_t(kThreads) * U * 16 : 0, uint64_t(kThreads) * U * 16);
   constexpr uint64_t kMaxGrid = 0x7ffffff8ull;  // a multiple of kXcds below the grid-size limit
-  for (uint64_t base = 0; base < ntiles; base += kMaxGrid) {
-    const uint32_t n = uint32_t(ntiles - base < kMaxGrid ? ntiles - base : kMaxGrid);
+  for (uint64_t done = 0; done < count; done += kMaxGrid) {
+    const uint32_t n = uint32_t(count - done < kMaxGrid ? count - done : kMaxGrid);
     const uint32_t grid = XCD ? (n + kXcds - 1) / kXcds * kXcds : n;
-    hipLaunchKernelGGL((k_reshard<U, NT, LDS, XCD, CVT>), dim3(grid), dim3(kThreads), lds, st, segs, tm, base, n, sp,
-                       dp);
+    hipLaunchKernelGGL((k_reshard<U, NT, LDS, XCD, CVT, ZERO>), dim3(grid), dim3(kThreads), lds, st, segs, tm,
+                       first + done, sp, dp);
   }
 }
 
-// Copy plans: every combination of the launch options. Converting plans: no LDS staging.
-template <int U>
-static void dispatch_reshard(int cvt, bool nt_hint, bool lds, bool xcd, hipStream_t st, const DevSeg* segs,
-                             const uint32_t* tm, uint64_t nt, const uint64_t* sp, const uint64_t* dp) {
-  if (cvt != CVT_NONE) {
-    const int key = (cvt == CVT_F32_BF16 ? 0 : 4) | (nt_hint ? 2 : 0) | (xcd ? 1 : 0);
-    switch (key) {
-      case 0: launch_reshard<U, false, false, false, CVT_F32_BF16>(st, segs, tm, nt, sp, dp); break;
-      case 1: launch_reshard<U, false, false, true, CVT_F32_BF16>(st, segs, tm, nt, sp, dp); break;
-      case 2: launch_reshard<U, true, false, false, CVT_F32_BF16>(st, segs, tm, nt, sp, dp); break;
-      case 3: launch_reshard<U, true, false, true, CVT_F32_BF16>(st, segs, tm, nt, sp, dp); break;
-      case 4: launch_reshard<U, false, false, false, CVT_BF16_F32>(st, segs, tm, nt, sp, dp); break;
-      case 5: launch_reshard<U, false, false, true, CVT_BF16_F32>(st, segs, tm, nt, sp, dp); break;
-      case 6: launch_reshard<U, true, false, false, CVT_BF16_F32>(st, segs, tm, nt, sp, dp); break;
-      default: launch_reshard<U, true, false, true, CVT_BF16_F32>(st, segs, tm, nt, sp, dp); break;
-    }
-    return;
-  }
-  const int key = (nt_hint ? 4 : 0) | (lds ? 2 : 0) | (xcd ? 1 : 0);
+// The copy section with the plan's conversion, then the zero-fill section, for every combination of
+// the launch options (converting plans: no LDS staging).
+template <int U, int CVT>
+static void launch_copy(bool nt_hint, bool lds, bool xcd, hipStream_t st, const DevSeg* segs, const uint32_t* tm,
+                        uint64_t first, uint64_t count, const uint64_t* sp, const uint64_t* dp) {
+  constexpr bool kLds = CVT == CVT_NONE;  // staging instances exist for plain copies only
+  const int key = (nt_hint ? 4 : 0) | (lds && kLds ? 2 : 0) | (xcd ? 1 : 0);
   switch (key) {
-    case 0: launch_reshard<U, false, false, false, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
-    case 1: launch_reshard<U, false, false, true, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
-    case 2: launch_reshard<U, false, true, false, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
-    case 3: launch_reshard<U, false, true, true, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
-    case 4: launch_reshard<U, true, false, false, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
-    case 5: launch_reshard<U, true, false, true, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
-    case 6: launch_reshard<U, true, true, false, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
-    default: launch_reshard<U, true, true, true, CVT_NONE>(st, segs, tm, nt, sp, dp); break;
+    case 0: launch_reshard<U, false, false, false, CVT, false>(st, segs, tm, first, count, sp, dp); break;
+    case 1: launch_reshard<U, false, false, true, CVT, false>(st, segs, tm, first, count, sp, dp); break;
+    case 2: launch_reshard<U, false, kLds, false, CVT, false>(st, segs, tm, first, count, sp, dp); break;
+    case 3: launch_reshard<U, false, kLds, true, CVT, false>(st, segs, tm, first, count, sp, dp); break;
+    case 4: launch_reshard<U, true, false, false, CVT, false>(st, segs, tm, first, count, sp, dp); break;
+    case 5: launch_reshard<U, true, false, true, CVT, false>(st, segs, tm, first, count, sp, dp); break;
+    case 6: launch_reshard<U, true, kLds, false, CVT, false>(st, segs, tm, first, count, sp, dp); break;
+    default: launch_reshard<U, true, kLds, true, CVT, false>(st, segs, tm, first, count, sp, dp); break;
+  }
+}
+
+template <int U>
+static void dispatch_reshard(const Plan* P, bool nt_hint, bool lds, bool xcd, hipStream_t st, const DevSeg* segs,
+                             const uint32_t* tm, const uint64_t* sp, const uint64_t* dp) {
+  if (P->ntiles_copy > 0) {
+    const uint64_t n = P->ntiles_copy;
+    switch (P->cvt) {
+      case CVT_F32_BF16: launch_copy<U, CVT_F32_BF16>(nt_hint, lds, xcd, st, segs, tm, 0, n, sp, dp); break;
+      case CVT_BF16_F32: launch_copy<U, CVT_BF16_F32>(nt_hint, lds, xcd, st, segs, tm, 0, n, sp, dp); break;
+      default: launch_copy<U, CVT_NONE>(nt_hint, lds, xcd, st, segs, tm, 0, n, sp, dp); break;
+    }
+  }
+  if (P->ntiles_zero > 0) {
+    const uint64_t z0 = P->zero_tile0, n = P->ntiles_zero;
+    const int key = (nt_hint ? 2 : 0) | (xcd ? 1 : 0);
+    switch (key) {
+      case 0: launch_reshard<U, false, false, false, CVT_NONE, true>(st, segs, tm, z0, n, sp, dp); break;
+      case 1: launch_reshard<U, false, false, true, CVT_NONE, true>(st, segs, tm, z0, n, sp, dp); break;
+      case 2: launch_reshard<U, true, false, false, CVT_NONE, true>(st, segs, tm, z0, n, sp, dp); break;
+      default: launch_reshard<U, true, false, true, CVT_NONE, true>(st, segs, tm, z0, n, sp, dp); break;
+    }
   }
 }
 
@@ -725,11 +743,11 @@ int emu_reshard(emu_plan_t plan, const void* d_workspace, const uint64_t* d_src_
   const bool ntm = option(EMU_OPT_NONTEMPORAL) != 0, lds = option(EMU_OPT_LDS_STAGING) != 0;
   const bool xcd = option(EMU_OPT_XCD_REMAP) != 0;
   switch (P->tile_vecs) {
-    case 1: dispatch_reshard<1>(P->cvt, ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
-    case 2: dispatch_reshard<2>(P->cvt, ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
-    case 4: dispatch_reshard<4>(P->cvt, ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
-    case 16: dispatch_reshard<16>(P->cvt, ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
-    default: dispatch_reshard<8>(P->cvt, ntm, lds, xcd, st, segs, tm, P->ntiles, d_src_ptrs, d_dst_ptrs); break;
+    case 1: dispatch_reshard<1>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;
+    case 2: dispatch_reshard<2>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;
+    case 4: dispatch_reshard<4>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;
+    case 16: dispatch_reshard<16>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;
+    default: dispatch_reshard<8>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;
   }
   return hip_check("emu_reshard launch");
 }

@@ -23,6 +23,8 @@ constexpr uint64_t kChunkBytes = EMU_CHUNK_BYTES;  // pack/unpack work unit, in 
 constexpr uint64_t kTileChunkBytes = EMU_TILE_CHUNK_BYTES;  // unit of the tile-per-workgroup pack/unpack kernel
 constexpr uint32_t kMapTensorBits = 20;            // tile map entry: rank << 20 | tensor within the rank
 constexpr uint64_t kWsAlign = 256;
+constexpr uint32_t kXcdCount = 8;          // XCDs of an MI355X; reshard grids are a multiple of this
+constexpr uint32_t kNoSeg = 0xffffffffu;   // tile map padding entry: the workgroup has no tile
 
 // Segment execution modes. Every "vec" mode needs src/dst offsets, strides and the run to be
 // multiples of 16 bytes (and 16-byte aligned tensor bases, an ABI requirement).
@@ -48,7 +50,7 @@ struct alignas(16) DevSeg {
   uint32_t param;  // SEG_VEC_ROWS: rows per tile; SEG_VEC_ROWCHUNK / SEG_GENERAL: tiles per row
   uint32_t rv;     // SEG_VEC_ROWS: 16-byte vectors per row
   uint32_t magic;  // SEG_VEC_ROWS: ceil(2^32 / rv) for rv > 1 (n / rv == umulhi(n, magic) for n*rv < 2^32)
-  uint64_t tile0;  // index of the segment's first tile
+  uint64_t tile0;  // map index of the segment's first tile
 };
 static_assert(sizeof(DevSeg) == 80, "DevSeg layout");
 
@@ -66,7 +68,8 @@ struct SideTables {
 
 struct WsLayout {
   uint64_t off_segs;     // DevSeg[n_segments]
-  uint64_t off_tilemap;  // uint32[n_tiles]  segment index of every tile
+  uint64_t off_tilemap;  // uint32[]  segment index of every tile: copy tiles, then zero-fill tiles, each
+                         //           section padded with kNoSeg to a multiple of kXcdCount
   SideTables side[2];
   uint64_t total;
 };
@@ -90,7 +93,10 @@ struct Plan {
   int tile_vecs = 2;                // 16-byte vectors per thread per tile
   int cvt = CVT_NONE;               // element conversion of the whole plan
   uint64_t tile_bytes = 0;
-  uint64_t ntiles = 0;
+  uint64_t ntiles = 0;              // copy + zero-fill tiles
+  uint64_t ntiles_copy = 0;         // tiles [0, ntiles_copy) of the map: copy segments
+  uint64_t zero_tile0 = 0;          // tiles [zero_tile0, zero_tile0 + ntiles_zero): zero-fill segments
+  uint64_t ntiles_zero = 0;
   emu_plan_info_t info{};
   WsLayout ws{};
   std::vector<uint8_t> host_ws;     // workspace image uploaded by emu_plan_upload

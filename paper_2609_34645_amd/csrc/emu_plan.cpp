@@ -407,6 +407,7 @@ static int finalize(Plan& P) {
   P.tile_bytes = TB;
   P.dsegs.clear();
   std::vector<uint32_t> tilemap;
+  std::vector<uint64_t> segtiles;  // tiles of each segment
   uint64_t tiles = 0, zero_bytes = 0, written = 0, read = 0;
   int64_t nzero = 0;
   // source alignment the vector paths need: 16 bytes when each destination vector reads one or two
@@ -420,7 +421,6 @@ static int finalize(Plan& P) {
     d.src_stride = g.src_stride; d.dst_stride = g.dst_stride;
     d.rows = g.rows; d.run = g.run;
     d.src_idx = g.src_tensor; d.dst_idx = g.dst_tensor;
-    d.tile0 = tiles;
     const bool zero = g.src_tensor < 0;
     const bool vec = ((g.dst_offset | g.run) % 16 == 0) && (g.rows == 1 || g.dst_stride % 16 == 0) &&
                      (zero || (g.src_offset % salign == 0 && (g.rows == 1 || g.src_stride % salign == 0)));
@@ -457,12 +457,27 @@ static int finalize(Plan& P) {
     }
     written += g.rows * g.run;
     read += g.rows * g.src_run;
-    if (tiles + nt > 0xffffffffull) return fail(EMU_ERR_UNSUPPORTED, "too many tiles");
-    tilemap.insert(tilemap.end(), nt, uint32_t(i));
+    if (tiles + nt > 0xfffffff0ull) return fail(EMU_ERR_UNSUPPORTED, "too many tiles");
     tiles += nt;
+    segtiles.push_back(nt);
     P.dsegs.push_back(d);
   }
   P.ntiles = tiles;
+  // Tile map: the copy segments' tiles, then the zero-fill segments' tiles, which run on their own
+  // kernel instance. Each section is padded with kNoSeg to a whole number of XCD groups, so that every
+  // workgroup of a grid (a multiple of kXcdCount) reads an entry of its own section and the kernel
+  // needs no bounds check before its first load.
+  for (int pass = 0; pass < 2; ++pass) {
+    if (pass == 1) P.zero_tile0 = tilemap.size();
+    for (size_t i = 0; i < P.dsegs.size(); ++i) {
+      if (((P.dsegs[i].mode & SEG_ZERO) != 0) != (pass == 1)) continue;
+      P.dsegs[i].tile0 = tilemap.size();
+      tilemap.insert(tilemap.end(), segtiles[i], uint32_t(i));
+    }
+    if (pass == 0) P.ntiles_copy = tilemap.size();
+    else P.ntiles_zero = tilemap.size() - P.zero_tile0;
+    while (tilemap.size() % kXcdCount) tilemap.push_back(kNoSeg);
+  }
   if (written != P.side[1].total_bytes)
     return fail(EMU_ERR_ARG, "internal: copy map covers %llu of %llu destination bytes",
                 (unsigned long long)written, (unsigned long long)P.side[1].total_bytes);
