@@ -489,43 +489,54 @@ __global__ __launch_bounds__(kThreads, EMU_BUCKET_WAVES_PER_EU) void k_buckets(c
   }
 }
 
-// Tile-per-workgroup variant: one workgroup per 8 KB chunk (kTileChunkBytes) of one rank's stream (XCD-contiguous
-// order). The upload-time map gives the chunk's rank and the tensor holding its first byte; each wave
-// computes the rank's first bucket, the sum over earlier ranks of ceil(bytes / B), with a wave64
-// reduction (so no barrier is needed). The chunk is then cut at tensor and bucket boundaries as above.
+// Tile-per-workgroup variant: one workgroup per 8 KB chunk (kTileChunkBytes) of one rank's stream, in
+// XCD-contiguous order. The upload-time map gives the chunk's rank and the global index of the tensor
+// holding its first byte, so the tensor's stream offset and pointer load in parallel with the rank's
+// record; the map is padded to the grid, so no bounds check precedes it. The rank's first bucket, the
+// sum over earlier ranks of ceil(bytes / B), comes from the host in a kernel argument for the first
+// kArgRanks ranks, else from a wave64 reduction. The chunk is then cut at tensor and bucket boundaries.
+constexpr int kArgRanks = 128;
+struct BucketBases {
+  uint64_t first[kArgRanks];  // first bucket of each rank, for ranks below kArgRanks
+};
+
 template <bool UNPACK, bool NT, int U>
 __global__ __launch_bounds__(kThreads, EMU_RESHARD_WAVES_PER_EU) void k_buckets_tile(
-    const uint64_t* __restrict__ stream_off, const uint32_t* __restrict__ rank_first,
-    const uint64_t* __restrict__ rank_bytes, const uint64_t* __restrict__ tile_first,
-    const uint32_t* __restrict__ tile_map, uint32_t ntile, uint64_t B, const uint64_t* __restrict__ tensor_ptrs,
-    const uint64_t* __restrict__ bucket_ptrs) {
-  const uint32_t per = gridDim.x / kXcds;  // the host launches a multiple of kXcds workgroups
+    const uint64_t* __restrict__ stream_off, const uint64_t* __restrict__ rank_info,
+    const uint64_t* __restrict__ rank_bytes, const uint32_t* __restrict__ tile_map, uint64_t B, int32_t b_shift,
+    const uint64_t* __restrict__ tensor_ptrs, const uint64_t* __restrict__ bucket_ptrs, BucketBases bases) {
+  const uint32_t per = gridDim.x / kXcds;  // the host launches the padded map's length, a multiple of kXcds
   const uint32_t c = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
-  if (c >= ntile) return;
   const uint32_t m = tile_map[c];
+  if (m == kNoSeg) return;
   const uint32_t r = m >> kMapTensorBits;
-  uint32_t ti = m & ((1u << kMapTensorBits) - 1);
-  const uint32_t t0 = rank_first[r], nt = rank_first[r + 1] - t0;
-  const uint64_t S = rank_bytes[r];
-  const uint64_t start = (c - tile_first[r]) * kTileChunkBytes;
+  uint32_t g = m & ((1u << kMapTensorBits) - 1);
+  const uint64_t c0 = rank_info[4 * r], S = rank_info[4 * r + 1];
+  const uint32_t gend = uint32_t(rank_info[4 * r + 2]);
+  uint64_t bucket0;
+  if (r < uint32_t(kArgRanks)) {
+    bucket0 = bases.first[r];
+  } else {
+    const uint32_t lane = threadIdx.x & 63;
+    uint64_t acc = 0;
+    for (uint32_t q = lane; q < r; q += 64) acc += (rank_bytes[q] + B - 1) / B;
+    bucket0 = uniform64(wave_sum(acc));
+  }
+  const uint64_t start = (c - c0) * kTileChunkBytes;
   const uint64_t end = start + kTileChunkBytes < S ? start + kTileChunkBytes : S;
-  const uint32_t lane = threadIdx.x & 63;
-  uint64_t acc = 0;
-  for (uint32_t q = lane; q < r; q += 64) acc += (rank_bytes[q] + B - 1) / B;
-  const uint64_t bucket0 = uniform64(wave_sum(acc));
-  uint64_t k = start / B;
+  uint64_t k = b_shift >= 0 ? start >> b_shift : start / B;
   uint64_t kend = (k + 1) * B;
   uint64_t pos = start;
   while (pos < end) {
-    const uint64_t toff = stream_off[t0 + ti];
-    const uint64_t tend = ti + 1 < nt ? stream_off[t0 + ti + 1] : S;
+    const uint64_t toff = stream_off[g];
+    const uint64_t tend = g + 1 < gend ? stream_off[g + 1] : S;
     if (tend <= pos) {  // the chunk moves on into the next tensor (or past an empty one)
-      ++ti;
+      ++g;
       continue;
     }
     uint64_t pend = end < tend ? end : tend;
     if (kend < pend) pend = kend;
-    uint8_t* tp = reinterpret_cast<uint8_t*>(tensor_ptrs[t0 + ti]) + (pos - toff);
+    uint8_t* tp = reinterpret_cast<uint8_t*>(tensor_ptrs[g]) + (pos - toff);
     uint8_t* bp = reinterpret_cast<uint8_t*>(bucket_ptrs[bucket0 + k]) + (pos - k * B);
     const uint32_t n = uint32_t(pend - pos);
     if constexpr (UNPACK) wg_copy_bytes<U, kShiftUnroll, NT, false>(bp, tp, n);
@@ -681,18 +692,24 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
   const bool ntm = option(EMU_OPT_NONTEMPORAL) != 0;
   if (option(EMU_OPT_BUCKET_TILES) != 0 && t.n_tiles > 0) {
     const uint64_t* so = reinterpret_cast<const uint64_t*>(w + t.off_stream);
-    const uint64_t* tf = reinterpret_cast<const uint64_t*>(w + t.off_tile_first);
+    const uint64_t* ri = reinterpret_cast<const uint64_t*>(w + t.off_rank_info);
     const uint32_t* tm = reinterpret_cast<const uint32_t*>(w + t.off_tile_map);
-    const uint32_t nt = uint32_t(t.n_tiles);
-    const dim3 g((nt + kXcds - 1) / kXcds * kXcds);
+    BucketBases bases;
+    uint64_t acc = 0;
+    for (int r = 0; r < s.nranks && r < kArgRanks; ++r) {
+      bases.first[r] = acc;
+      acc += (s.rank_bytes[r] + B - 1) / B;
+    }
+    const int32_t b_shift = (B & (B - 1)) == 0 ? __builtin_ctzll(B) : -1;
+    const dim3 g(uint32_t(t.n_tiles));  // padded to a multiple of kXcds
     // the bucket kernel's 8 KB chunks run best uncapped, so its automatic setting is no cap
     const size_t lds = option(EMU_OPT_WG_PER_CU) < 0 ? 0 : occupancy_lds(0, kTileChunkBytes);
     if (unpack) {
-      if (ntm) hipLaunchKernelGGL((k_buckets_tile<true, true, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, rf, rb, tf, tm, nt, B, tptr, bptr);
-      else hipLaunchKernelGGL((k_buckets_tile<true, false, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, rf, rb, tf, tm, nt, B, tptr, bptr);
+      if (ntm) hipLaunchKernelGGL((k_buckets_tile<true, true, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
+      else hipLaunchKernelGGL((k_buckets_tile<true, false, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
     } else {
-      if (ntm) hipLaunchKernelGGL((k_buckets_tile<false, true, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, rf, rb, tf, tm, nt, B, tptr, bptr);
-      else hipLaunchKernelGGL((k_buckets_tile<false, false, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, rf, rb, tf, tm, nt, B, tptr, bptr);
+      if (ntm) hipLaunchKernelGGL((k_buckets_tile<false, true, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
+      else hipLaunchKernelGGL((k_buckets_tile<false, false, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
     }
     return hip_check(unpack ? "emu_unpack_buckets launch" : "emu_pack_buckets launch");
   }

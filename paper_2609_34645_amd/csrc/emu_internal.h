@@ -21,7 +21,7 @@ constexpr uint64_t kChunkBytes = EMU_CHUNK_BYTES;  // pack/unpack work unit, in 
 #define EMU_TILE_CHUNK_BYTES 8192
 #endif
 constexpr uint64_t kTileChunkBytes = EMU_TILE_CHUNK_BYTES;  // unit of the tile-per-workgroup pack/unpack kernel
-constexpr uint32_t kMapTensorBits = 20;            // tile map entry: rank << 20 | tensor within the rank
+constexpr uint32_t kMapTensorBits = 20;            // chunk map entry: rank << 20 | global tensor index
 constexpr uint64_t kWsAlign = 256;
 constexpr uint32_t kXcdCount = 8;          // XCDs of an MI355X; reshard grids are a multiple of this
 constexpr uint32_t kNoSeg = 0xffffffffu;   // tile map padding entry: the workgroup has no tile
@@ -61,9 +61,11 @@ struct SideTables {
   uint64_t off_rank_bytes;   // uint64[n_ranks]     stream length of each rank
   uint64_t off_chunk_first;  // uint64[n_ranks + 1] first pack/unpack chunk of each rank
   uint64_t off_stream;       // uint64[n_tensors]   stream offset of each tensor inside its rank
-  uint64_t off_tile_first;   // uint64[n_ranks + 1] first tile chunk (kTileChunkBytes) of each rank
-  uint64_t off_tile_map;     // uint32[n_tile_chunks] rank << 20 | tensor holding the chunk's first byte
-  uint64_t n_tiles;          // tile chunks of the side (0 when the map cannot encode it)
+  uint64_t off_rank_info;    // uint64[n_ranks][4]  {first chunk (kTileChunkBytes), stream bytes,
+                             //                      end of the rank's global tensor range, 0}
+  uint64_t off_tile_map;     // uint32[n_tiles]     rank << 20 | global index of the tensor holding the
+                             //                      chunk's first byte; padded with kNoSeg to kXcdCount
+  uint64_t n_tiles;          // map entries including the padding (0 when the map cannot encode the side)
 };
 
 struct WsLayout {

@@ -488,29 +488,32 @@ static int finalize(Plan& P) {
   uint64_t off = 0;
   w.off_segs = off; off = align(off + P.dsegs.size() * sizeof(DevSeg));
   w.off_tilemap = off; off = align(off + tilemap.size() * 4);
-  // per side: tile chunk -> (rank, tensor) map for the tile-per-workgroup pack/unpack kernel
+  // per side: chunk -> (rank, global tensor) map for the tile-per-workgroup pack/unpack kernel, padded
+  // with kNoSeg to a multiple of kXcdCount (the kernel's grid), and per rank {first chunk, stream
+  // bytes, end of its tensor range}
   std::vector<uint32_t> tmap[2];
-  std::vector<uint64_t> tfirst[2];
+  std::vector<uint64_t> rinfo[2];
   for (int sd = 0; sd < 2; ++sd) {
     const SideInfo& s = P.side[sd];
-    tfirst[sd].assign(s.nranks + 1, 0);
-    bool encodable = s.nranks <= (1 << (32 - kMapTensorBits));
+    rinfo[sd].assign(size_t(s.nranks) * 4, 0);
+    const bool encodable = s.nranks < (1 << (32 - kMapTensorBits)) && s.tensors.size() <= (1u << kMapTensorBits);
+    uint64_t first = 0;
     for (int r = 0; r < s.nranks && encodable; ++r) {
-      const uint32_t t0 = s.rank_first[r], nt = s.rank_first[r + 1] - t0;
-      if (nt > (1u << kMapTensorBits)) encodable = false;
+      const uint32_t t0 = s.rank_first[r], t1 = s.rank_first[r + 1];
       const uint64_t nch = (s.rank_bytes[r] + kTileChunkBytes - 1) / kTileChunkBytes;
-      tfirst[sd][r + 1] = tfirst[sd][r] + nch;
-      uint32_t ti = 0;
-      for (uint64_t j = 0; j < nch && encodable; ++j) {
+      rinfo[sd][4 * r + 0] = first;
+      rinfo[sd][4 * r + 1] = s.rank_bytes[r];
+      rinfo[sd][4 * r + 2] = t1;
+      first += nch;
+      uint32_t g = t0;
+      for (uint64_t j = 0; j < nch; ++j) {
         const uint64_t pos = j * kTileChunkBytes;
-        while (ti + 1 < nt && s.tensors[t0 + ti + 1].stream_offset <= pos) ++ti;
-        tmap[sd].push_back((uint32_t(r) << kMapTensorBits) | ti);
+        while (g + 1 < t1 && s.tensors[g + 1].stream_offset <= pos) ++g;
+        tmap[sd].push_back((uint32_t(r) << kMapTensorBits) | g);
       }
     }
-    if (!encodable || tmap[sd].size() > 0x7fffffffull) {
-      tmap[sd].clear();
-      std::fill(tfirst[sd].begin(), tfirst[sd].end(), 0);
-    }
+    if (!encodable || tmap[sd].size() > 0x7fffff00ull) tmap[sd].clear();
+    while (tmap[sd].size() % kXcdCount) tmap[sd].push_back(kNoSeg);
   }
   for (int sd = 0; sd < 2; ++sd) {
     const SideInfo& s = P.side[sd];
@@ -519,7 +522,7 @@ static int finalize(Plan& P) {
     w.side[sd].off_rank_bytes = off; off = align(off + s.nranks * 8);
     w.side[sd].off_chunk_first = off; off = align(off + (s.nranks + 1) * 8);
     w.side[sd].off_stream = off; off = align(off + s.tensors.size() * 8);
-    w.side[sd].off_tile_first = off; off = align(off + (s.nranks + 1) * 8);
+    w.side[sd].off_rank_info = off; off = align(off + rinfo[sd].size() * 8);
     w.side[sd].off_tile_map = off; off = align(off + tmap[sd].size() * 4);
     w.side[sd].n_tiles = tmap[sd].size();
   }
@@ -537,7 +540,7 @@ static int finalize(Plan& P) {
     std::memcpy(h + w.side[sd].off_chunk_first, s.chunk_first.data(), s.chunk_first.size() * 8);
     uint64_t* so = reinterpret_cast<uint64_t*>(h + w.side[sd].off_stream);
     for (size_t i = 0; i < s.tensors.size(); ++i) so[i] = s.tensors[i].stream_offset;
-    std::memcpy(h + w.side[sd].off_tile_first, tfirst[sd].data(), tfirst[sd].size() * 8);
+    if (!rinfo[sd].empty()) std::memcpy(h + w.side[sd].off_rank_info, rinfo[sd].data(), rinfo[sd].size() * 8);
     if (!tmap[sd].empty()) std::memcpy(h + w.side[sd].off_tile_map, tmap[sd].data(), tmap[sd].size() * 4);
   }
 
