@@ -87,6 +87,8 @@ def check_reshard(plan, src_set, dst_set, groups=None, label=""):
     t0 = time.time()
     n_checked = 0
     for g in gl:
+        if sum(sd[i]["bytes"] for i in by_group[g]) > 1 << 30:
+            say(f"  {label}: checking group {g}")
         cache = {i: host_view(src_set.tensors[i], sd[i], src.dtype) for i in by_group[g]}
         want = oracle.reshard_group(lambda r, j: cache[sf[r] + j], os_, od, g)
         for (r, j), w in want.items():

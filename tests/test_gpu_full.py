@@ -6,6 +6,9 @@
 * 8B, padded vocabulary, TP8 PP4 -> TP2 PP2, packed into 2^28-byte buckets (mid-row bucket boundaries)
   and unpacked on the receiver side: reshard, bucket bytes and unpacked tensors against the oracle;
   again with 2^28 - 2 byte buckets, which put tensor and bucket bytes at different 16-byte phases.
+* Tensors over 4 GiB: a one-layer decoder with a 266,240-row vocabulary at hidden size 8192 in fp32
+  (8.7 GB embedding and LM head), TP1 PP1 -> TP2 PP1, packed into 2^30-byte buckets and unpacked, then
+  converted back to bf16 TP1 PP1: every byte against the oracle.
 * 8B training state, fp32 master + Adam m + v (96 GB in): TP4 PP1 -> TP1 PP1, one launch per tensor
   group, then split back into the source buffers; master checked in full against the oracle, m and v on
   sampled tensor groups, the back transition against a seeded regeneration of the original state.
@@ -21,7 +24,7 @@ import pytest
 import oracle
 from paper_2609_34645_amd import emu
 from tests.gpu_util import check_reshard, fill_device, host_view, o_layout, say
-from tests.shapes import EIGHT_B, ONE_B
+from tests.shapes import EIGHT_B, HUGE_VOCAB, ONE_B
 
 pytestmark = pytest.mark.gpu
 
@@ -196,6 +199,37 @@ def test_8b_padded_tp8pp4_to_tp2pp2_buckets(gpu_lib):
     _pack_check(p, ws, D, 1 << 28, "fused reshard->buckets 2^28", S=S)
     _pack_check(p, ws, D, (1 << 28) - 2, "fused reshard->buckets 2^28-2", S=S)
     del D, S, ws
+    cleanup()
+
+
+def test_tensors_over_4gib(gpu_lib):
+    """fp32 embedding and LM head of 8.7 GB (266,240 x 8192): source tensors, destination shards
+    (4.4 GB), segment runs and bucket positions all pass 2^32 bytes, which only 64-bit offsets reach."""
+    import torch
+
+    m = emu.Model(*HUGE_VOCAB)
+    a, b, c = emu.Layout(m, 1, 1, 0, "fp32"), emu.Layout(m, 2, 1, 0, "fp32"), emu.Layout(m, 1, 1, 0, "bf16")
+    p = emu.Plan(a, b)
+    assert max(d["bytes"] for d in p.tensors(1)) > 1 << 32
+    ws = p.workspace()
+    S = p.alloc(0)
+    fill_device(p, 0, S, seed=606, dtype="fp32")
+    D = p.alloc(1, fill=0xA5)
+    say("  huge vocab: fp32 TP1 -> TP2")
+    p.reshard(ws, S.ptrs, D.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(p, S, D, label="huge vocab fp32 TP1 PP1 -> TP2 PP1")
+    del S
+    cleanup()
+    _pack_check(p, ws, D, 1 << 30, "huge vocab buckets 2^30")
+    q = emu.Plan(b, c)
+    wq = q.workspace()
+    E = q.alloc(1, fill=0x5A)
+    say("  huge vocab: fp32 TP2 -> bf16 TP1")
+    q.reshard(wq, D.ptrs, E.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(q, D, E, label="huge vocab fp32 TP2 PP1 -> bf16 TP1 PP1")
+    del D, E, ws, wq
     cleanup()
 
 

@@ -347,3 +347,21 @@ def test_kv_replication_8b_tp16():
     exact_cover(p3)
     layers = [sorted({d["layer"] for d in p3.tensors(1) if d["rank"] == r and d["layer"] >= 0}) for r in (0, 2, 4)]
     assert layers == [list(range(0, 11)), list(range(11, 22)), list(range(22, 32))]
+
+
+def test_plan_offsets_beyond_4gib():
+    """The one-layer 266,240 x 8192 fp32 vocabulary model: destination shards, segment runs and source
+    offsets pass 2^32 bytes; the map covers every destination byte once (exact cover on the host)."""
+    from tests.shapes import HUGE_VOCAB
+
+    m = emu.Model(*HUGE_VOCAB)
+    plan = emu.Plan(emu.Layout(m, 1, 1, 0, "fp32"), emu.Layout(m, 2, 1, 0, "fp32"))
+    segs = plan.segments()
+    assert max(g["run"] for g in segs) > 1 << 32
+    assert max(g["src_offset"] for g in segs) >= 1 << 32
+    dd = plan.tensors(1)
+    cover = {}
+    for g in segs:
+        cover[g["dst_tensor"]] = cover.get(g["dst_tensor"], 0) + g["rows"] * g["run"]
+    assert all(cover[i] == d["bytes"] for i, d in enumerate(dd))
+    assert plan.info["bytes_written"] == sum(d["bytes"] for d in dd) > 2 * (1 << 32)
