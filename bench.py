@@ -26,6 +26,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 EIGHT_B = (32, 4096, 32, 128, 8, 14336, 128256)  # L, H, nH, hd, G, I, V
+TINY = (2, 256, 4, 64, 2, 688, 1024)
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "reshard_8b_tp2pp2_tp4pp1_pmc.txt")
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_34645_amd", "csrc", "emu_exec.hip")
 
@@ -106,6 +107,47 @@ def cpu_baseline(seed, layers, min_seconds=10.0):
                       f"(bf16, {per_pass / 2 / 1e9:.2f} GB of destination shards per pass), repeated for at "
                       f"least {min_seconds:.0f} s; NumPy, tensor groups spread over a pool of {cores} threads "
                       f"(single_thread: one thread); input generation excluded"}
+
+
+def tiny_latency(emu, iters=200):
+    """Latency of the tiny decoder's Split TP1 PP1 -> TP2 PP1 with pack and unpack into 64 KiB buckets
+    (3.95 MB of destination shards, cache-resident): back-to-back eager calls through the binding, and
+    replays of one HIP graph holding the same three calls. Mean per step over `iters` steps."""
+    import torch
+
+    m = emu.Model(*TINY)
+    plan = emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1))
+    ws = plan.workspace()
+    S, D, R = plan.alloc(0, fill=1), plan.alloc(1), plan.alloc(1)
+    B = 1 << 16
+    bufs, bptrs = plan.alloc_buckets(1, B)
+
+    def step():
+        plan.reshard(ws, S.ptrs, D.ptrs)
+        plan.pack(ws, 1, B, D.ptrs, bptrs)
+        plan.unpack(ws, 1, B, bptrs, R.ptrs)
+
+    def timed(fn):
+        for _ in range(10):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / iters
+
+    eager = timed(step)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
+        step()
+    replay = timed(graph.replay)
+    ok = all(torch.equal(x, y) for x, y in zip(D.tensors, R.tensors))
+    return {"workload": "tiny decoder bf16 TP1PP1->TP2PP1 + pack/unpack at 64 KiB buckets",
+            "destination_bytes": plan.info["bytes_written"], "eager_us_per_step": round(eager, 2),
+            "graph_us_per_step": round(replay, 2), "outputs_consistent": ok}
 
 
 def dag_planning(emu):
@@ -339,6 +381,7 @@ def main():
     }
     del S, D, R, bufs
     torch.cuda.empty_cache()
+    out["tiny_transition_latency"] = tiny_latency(emu)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(args.seed, args.cpu_layers)

@@ -1,9 +1,10 @@
 """GPU parity on small models: every output byte compared with the oracle on the same seeded inputs.
 
-Covers the micro models (which also exercise the byte-granular path: 8-byte o/down runs at TP4),
-the tiny 2-layer decoder's Split TP1 PP1 -> TP2 PP1 and Merge back, format changes, padded vocabularies
-with zero-filled destination pad rows, every launch option, and bucket pack/unpack at awkward bucket
-sizes (including sizes that put source and bucket bytes at different 16-byte phases).
+Covers the micro models (which also exercise the byte-granular path: 8-byte o/down runs at TP4), the
+tiny 2-layer decoder's Split TP1 PP1 -> TP2 PP1 and Merge back, the tiny transition captured in a HIP
+graph and replayed, format changes, padded vocabularies with zero-filled destination pad rows, every
+launch option, and bucket pack/unpack at awkward bucket sizes (including sizes that put source and
+bucket bytes at different 16-byte phases).
 """
 import itertools
 
@@ -114,6 +115,47 @@ def test_tiny_split_and_merge_back(gpu_lib):
     check_reshard(back, B, A2, label="tiny TP2->TP1")
     for x, y in zip(A.tensors, A2.tensors):
         assert torch.equal(x, y)
+
+
+def test_tiny_transition_in_a_hip_graph(gpu_lib):
+    """The library only enqueues kernels on the caller's stream (no allocation, no synchronisation), so
+    reshard + pack + unpack of the tiny decoder can be captured once in a HIP graph and replayed. Each
+    replay runs on new source contents written eagerly between replays, and its destination tensors,
+    buckets and unpacked tensors are checked against the oracle."""
+    import torch
+
+    m = emu.Model(*TINY)
+    a, b = emu.Layout(m, 1, 1), emu.Layout(m, 2, 1)
+    plan = emu.Plan(a, b)
+    ws = plan.workspace()
+    B = 1 << 16
+    S = plan.alloc(0)
+    D, R = plan.alloc(1, fill=0xA5), plan.alloc(1, fill=0x5A)
+    bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77)
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        plan.reshard(ws, S.ptrs, D.ptrs)
+        plan.pack(ws, 1, B, D.ptrs, bptrs)
+        plan.unpack(ws, 1, B, bptrs, R.ptrs)
+    oa, ob = o_layout(a), o_layout(b)
+    for replay, seed in enumerate((21, 22, 23)):
+        upload_shards(oracle.shard(full_model(oa.model, seed), oa), S)
+        for t in D.bufs + R.bufs:
+            t.fill_(replay + 1)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        check_reshard(plan, S, D, label=f"graph replay {replay}")
+        dd = plan.tensors(1)
+        ranks = {}
+        for i, d in enumerate(dd):
+            ranks.setdefault(d["rank"], []).append(host_view(D.tensors[i], d, "bf16"))
+        check_buckets(plan, 1, B, [ranks[r] for r in sorted(ranks)], bufs, label=f"graph replay {replay}")
+        for x, y in zip(D.tensors, R.tensors):
+            assert torch.equal(x, y), f"graph replay {replay}: unpacked tensors differ"
+    del graph
 
 
 @pytest.mark.parametrize("opts", [
