@@ -74,7 +74,8 @@ typedef enum {
   EMU_ERR_HANDLE = -9,      /* not a live plan handle (NULL, freed, or foreign) */
   EMU_ERR_RANGE = -10,      /* an index or side argument is out of range */
   EMU_ERR_ARG = -11,        /* another argument is invalid (message in emu_last_error) */
-  EMU_ERR_INFEASIBLE = -12  /* no deadlock-free transition DAG exists for the target plan */
+  EMU_ERR_INFEASIBLE = -12, /* no deadlock-free transition DAG exists for the target plan */
+  EMU_ERR_OVERLAP = -13     /* pointer tables name overlapping buffers (emu_check_tables) */
 } emu_status;
 
 typedef enum { EMU_BF16 = 0, EMU_FP32 = 1 } emu_dtype;                       /* 2 / 4 bytes */
@@ -223,14 +224,33 @@ int emu_bucket_layout(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, int3
 
 /* Pack one side's tensors into buckets: bucket k of rank r receives bytes [k*B, (k+1)*B) of r's
  * stream. d_tensor_ptrs lists that side's tensors (as for emu_reshard); d_bucket_ptrs lists all
- * buckets, rank 0 first (emu_bucket_layout(..., -1, ...) of them). Tensor stream offsets are computed
- * on the device from the tensor sizes held in the workspace. bucket_bytes must be a positive multiple
- * of the element size. */
+ * buckets, rank 0 first (emu_bucket_layout(..., -1, ...) of them). Tensor stream offsets (exclusive
+ * prefix sums of the ragged tensor sizes) come from the uploaded workspace; each rank's first bucket
+ * index depends on bucket_bytes and is formed per call (on the host for the first 128 ranks, by a
+ * wave64 reduction on the device beyond; the persistent fallback kernel scans the tensor sizes on the
+ * device). bucket_bytes must be a positive multiple of the element size. */
 int emu_pack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, uint64_t bucket_bytes,
                      const uint64_t* d_tensor_ptrs, const uint64_t* d_bucket_ptrs, void* hip_stream);
 /* The inverse of emu_pack_buckets: buckets -> that side's tensors. */
 int emu_unpack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, uint64_t bucket_bytes,
                        const uint64_t* d_bucket_ptrs, const uint64_t* d_tensor_ptrs, void* hip_stream);
+
+/* Host-side checks of pointer tables before an execute call (debug aid; host only, no GPU calls).
+ * The tables are HOST copies of the device pointer tables the execute call will receive.
+ *
+ * emu_check_tables: src_ptrs[n_src_tensors], dst_ptrs[n_dst_tensors] for emu_reshard (for a plan from
+ * emu_plan_to_buckets the destination entries are the buckets). Every entry must be non-zero
+ * (EMU_ERR_NULL) and 16-byte aligned (EMU_ERR_ALIGN), and no destination byte range may overlap
+ * another destination range or a source range (EMU_ERR_OVERLAP); source ranges may overlap each other.
+ *
+ * emu_check_bucket_tables: tensor_ptrs of one side and bucket_ptrs of its buckets of size bucket_bytes
+ * (as for emu_pack_buckets / emu_unpack_buckets). The same conditions, with every tensor and bucket
+ * range pairwise disjoint, since either kind is written by one of the two calls.
+ *
+ * emu_last_error() names the offending entries. Sorting sweep, O(n log n) in the table sizes. */
+int emu_check_tables(emu_plan_t plan, const uint64_t* src_ptrs, const uint64_t* dst_ptrs);
+int emu_check_bucket_tables(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, const uint64_t* tensor_ptrs,
+                            const uint64_t* bucket_ptrs);
 
 /* ------------------------------------------------------------------------------------------------
  * Transition-DAG planner (host only). From a current to a target plan of several model-stages: the

@@ -575,6 +575,60 @@ using namespace emu;
 // C ABI (host part)
 // ------------------------------------------------------------------------------------------------
 
+// ------------------------------------------------------------------------------------------------
+// host-side pointer-table checks
+// ------------------------------------------------------------------------------------------------
+
+namespace {
+
+struct Range {
+  uint64_t lo, hi;  // [lo, hi)
+  bool shared;      // may overlap other shared ranges (reshard sources)
+  const char* what;
+  int64_t index;
+};
+
+int add_ranges(std::vector<Range>& out, const uint64_t* ptrs, const std::vector<uint64_t>& sizes, bool shared,
+               const char* what) {
+  for (size_t i = 0; i < sizes.size(); ++i) {
+    const uint64_t p = ptrs[i];
+    if (p == 0) return emu::fail(EMU_ERR_NULL, "%s %zu has a NULL address", what, i);
+    if (p % 16) return emu::fail(EMU_ERR_ALIGN, "%s %zu at 0x%llx is not 16-byte aligned", what, i, (unsigned long long)p);
+    if (sizes[i] == 0) continue;
+    if (p + sizes[i] < p) return emu::fail(EMU_ERR_ARG, "%s %zu wraps the address space", what, i);
+    out.push_back(Range{p, p + sizes[i], shared, what, int64_t(i)});
+  }
+  return EMU_OK;
+}
+
+// Sweep in address order: a range conflicts with an earlier one that is still open unless both are
+// shared. Holding the furthest-reaching earlier range of each kind is enough to see every conflict.
+int sweep(std::vector<Range>& rs) {
+  std::sort(rs.begin(), rs.end(), [](const Range& a, const Range& b) { return a.lo < b.lo; });
+  const Range* open_shared = nullptr;
+  const Range* open_excl = nullptr;
+  for (const Range& r : rs) {
+    const Range* hit = nullptr;
+    if (open_excl && r.lo < open_excl->hi) hit = open_excl;
+    else if (!r.shared && open_shared && r.lo < open_shared->hi) hit = open_shared;
+    if (hit)
+      return emu::fail(EMU_ERR_OVERLAP, "%s %lld [0x%llx, 0x%llx) overlaps %s %lld [0x%llx, 0x%llx)", r.what,
+                       (long long)r.index, (unsigned long long)r.lo, (unsigned long long)r.hi, hit->what,
+                       (long long)hit->index, (unsigned long long)hit->lo, (unsigned long long)hit->hi);
+    const Range*& slot = r.shared ? open_shared : open_excl;
+    if (!slot || r.hi > slot->hi) slot = &r;
+  }
+  return EMU_OK;
+}
+
+std::vector<uint64_t> tensor_sizes(const emu::SideInfo& s) {
+  std::vector<uint64_t> v(s.tensors.size());
+  for (size_t i = 0; i < v.size(); ++i) v[i] = s.tensors[i].bytes;
+  return v;
+}
+
+}  // namespace
+
 extern "C" {
 
 int emu_version(void) { return EMU_ABI_VERSION; }
@@ -594,6 +648,7 @@ const char* emu_status_str(int s) {
     case EMU_ERR_RANGE: return "EMU_ERR_RANGE";
     case EMU_ERR_ARG: return "EMU_ERR_ARG";
     case EMU_ERR_INFEASIBLE: return "EMU_ERR_INFEASIBLE";
+    case EMU_ERR_OVERLAP: return "EMU_ERR_OVERLAP";
     default: return "EMU_ERR_UNKNOWN";
   }
 }
@@ -773,6 +828,50 @@ int emu_bucket_layout(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, int3
   if (n_buckets) *n_buckets = nb;
   if (stream_bytes) *stream_bytes = sb;
   return EMU_OK;
+}
+
+
+
+int emu_check_tables(emu_plan_t plan, const uint64_t* src_ptrs, const uint64_t* dst_ptrs) {
+  emu::clear_error();
+  const emu::Plan* P = reinterpret_cast<const emu::Plan*>(plan);
+  if (!emu::plan_live(P)) return emu::fail(EMU_ERR_HANDLE, "not a live plan");
+  if (!src_ptrs || !dst_ptrs) return emu::fail(EMU_ERR_NULL, "NULL pointer table");
+  try {
+    std::vector<Range> rs;
+    int rc = add_ranges(rs, src_ptrs, tensor_sizes(P->side[0]), true, "source tensor");
+    if (rc) return rc;
+    rc = add_ranges(rs, dst_ptrs, tensor_sizes(P->side[1]), false, "destination tensor");
+    if (rc) return rc;
+    return sweep(rs);
+  } catch (const std::bad_alloc&) {
+    return emu::fail(EMU_ERR_ARG, "out of host memory");
+  }
+}
+
+int emu_check_bucket_tables(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, const uint64_t* tensor_ptrs,
+                            const uint64_t* bucket_ptrs) {
+  emu::clear_error();
+  const emu::Plan* P = reinterpret_cast<const emu::Plan*>(plan);
+  if (!emu::plan_live(P)) return emu::fail(EMU_ERR_HANDLE, "not a live plan");
+  if (side != 0 && side != 1) return emu::fail(EMU_ERR_RANGE, "side must be 0 or 1");
+  if (!tensor_ptrs || !bucket_ptrs) return emu::fail(EMU_ERR_NULL, "NULL pointer table");
+  if (bucket_bytes == 0) return emu::fail(EMU_ERR_BUCKET, "bucket size is zero");
+  try {
+    const emu::SideInfo& s = P->side[side];
+    std::vector<uint64_t> bsizes;
+    for (int r = 0; r < s.nranks; ++r)
+      for (uint64_t k = 0; k * bucket_bytes < s.rank_bytes[r]; ++k)
+        bsizes.push_back(std::min(bucket_bytes, s.rank_bytes[r] - k * bucket_bytes));
+    std::vector<Range> rs;
+    int rc = add_ranges(rs, tensor_ptrs, tensor_sizes(s), false, "tensor");
+    if (rc) return rc;
+    rc = add_ranges(rs, bucket_ptrs, bsizes, false, "bucket");
+    if (rc) return rc;
+    return sweep(rs);
+  } catch (const std::bad_alloc&) {
+    return emu::fail(EMU_ERR_ARG, "out of host memory");
+  }
 }
 
 }  // extern "C"

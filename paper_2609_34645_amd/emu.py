@@ -37,8 +37,10 @@ KINDS = ["embed", "attn_norm", "qkv", "q", "k", "v", "o", "mlp_norm", "gate_up",
 STATUS = {0: "EMU_OK", -1: "EMU_ERR_NULL", -2: "EMU_ERR_LAYOUT", -3: "EMU_ERR_MISMATCH",
           -4: "EMU_ERR_UNSUPPORTED", -5: "EMU_ERR_WORKSPACE", -6: "EMU_ERR_BUCKET", -7: "EMU_ERR_ALIGN",
           -8: "EMU_ERR_HIP", -9: "EMU_ERR_HANDLE", -10: "EMU_ERR_RANGE", -11: "EMU_ERR_ARG",
-          -12: "EMU_ERR_INFEASIBLE"}
+          -12: "EMU_ERR_INFEASIBLE", -13: "EMU_ERR_OVERLAP"}
+STATUS_CODE = {v: k for k, v in STATUS.items()}
 ERR_INFEASIBLE = -12
+ERR_OVERLAP = -13
 
 
 class c_model(ctypes.Structure):
@@ -141,6 +143,8 @@ def load(path: str = LIB_PATH):
         "emu_bucket_layout": ([P, I32, U64, I32, ctypes.POINTER(U64), ctypes.POINTER(U64)], ctypes.c_int),
         "emu_pack_buckets": ([P, V, I32, U64, V, V, V], ctypes.c_int),
         "emu_unpack_buckets": ([P, V, I32, U64, V, V, V], ctypes.c_int),
+        "emu_check_tables": ([P, ctypes.POINTER(U64), ctypes.POINTER(U64)], ctypes.c_int),
+        "emu_check_bucket_tables": ([P, I32, U64, ctypes.POINTER(U64), ctypes.POINTER(U64)], ctypes.c_int),
         "emu_dag_plan": ([ctypes.POINTER(c_stage_transition), I32, ctypes.POINTER(c_link_model), ctypes.POINTER(P)],
                          ctypes.c_int),
         "emu_dag_free": ([P], ctypes.c_int),
@@ -349,6 +353,16 @@ class Plan:
                                         ctypes.c_void_p(bucket_ptrs.data_ptr()), ctypes.c_void_p(tensor_ptrs.data_ptr()),
                                         _stream_handle(stream)))
 
+    # -- host-side table checks ------------------------------------------------------------------
+    def check_tables(self, src_ptrs, dst_ptrs):
+        """``emu_check_tables`` on host copies of two pointer tables (int sequences or int64 tensors)."""
+        check(load().emu_check_tables(self._h, _u64_array(src_ptrs), _u64_array(dst_ptrs)))
+
+    def check_bucket_tables(self, side, bucket_bytes, tensor_ptrs, bucket_ptrs):
+        """``emu_check_bucket_tables`` on host copies of a side's tensor table and its bucket table."""
+        check(load().emu_check_bucket_tables(self._h, side, bucket_bytes, _u64_array(tensor_ptrs),
+                                             _u64_array(bucket_ptrs)))
+
     def close(self):
         if getattr(self, "_h", None) is not None and _lib is not None:
             check(_lib.emu_plan_free(self._h))
@@ -359,6 +373,14 @@ class Plan:
             self.close()
         except Exception:
             pass
+
+
+def _u64_array(ptrs):
+    """A ctypes uint64 array from a sequence of ints or an int64 tensor (copied to the host)."""
+    if hasattr(ptrs, "cpu"):
+        ptrs = ptrs.cpu().tolist()
+    vals = [int(x) & 0xFFFFFFFFFFFFFFFF for x in ptrs]
+    return (ctypes.c_uint64 * max(1, len(vals)))(*vals)
 
 
 def ptr_table(tensors, device=None):

@@ -31,12 +31,14 @@ def run_pair(src, dst, seed=5, options=None, bucket_sizes=()):
     ws = plan.workspace()
     S = plan.alloc(0, fill=0x5A)
     D = plan.alloc(1, fill=0xA5)
+    plan.check_tables(S.ptrs, D.ptrs)
     upload_shards(oracle.shard(full_model(os_.model, seed, src.dtype), os_), S, tp=src.tp)
     plan.reshard(ws, S.ptrs, D.ptrs)
     torch.cuda.synchronize()
     check_reshard(plan, S, D, label=f"{src.tp}x{src.pp}->{dst.tp}x{dst.pp}")
     for B in bucket_sizes:
         bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77)
+        plan.check_bucket_tables(1, B, D.ptrs, bptrs)
         plan.pack(ws, 1, B, D.ptrs, bptrs)
         R = plan.alloc(1, fill=0x11)
         plan.unpack(ws, 1, B, bptrs, R.ptrs)

@@ -365,3 +365,91 @@ def test_plan_offsets_beyond_4gib():
         cover[g["dst_tensor"]] = cover.get(g["dst_tensor"], 0) + g["rows"] * g["run"]
     assert all(cover[i] == d["bytes"] for i, d in enumerate(dd))
     assert plan.info["bytes_written"] == sum(d["bytes"] for d in dd) > 2 * (1 << 32)
+
+
+# ------------------------------------------------------------------------------------------------
+# host-side pointer-table checks (emu_check_tables / emu_check_bucket_tables)
+# ------------------------------------------------------------------------------------------------
+
+def _packed(sizes, base, gap=256):
+    """Addresses of buffers laid out back to back from `base`, each start rounded up to `gap`."""
+    out, a = [], base
+    for n in sizes:
+        out.append(a)
+        a = (a + n + gap - 1) // gap * gap
+    return out
+
+
+def test_check_tables_accepts_disjoint_and_rejects_each_fault():
+    m = emu.Model(*MICRO)
+    plan = emu.Plan(emu.Layout(m, 2, 2, 2), emu.Layout(m, 4, 1, 2))
+    ss = [d["bytes"] for d in plan.tensors(0)]
+    ds = [d["bytes"] for d in plan.tensors(1)]
+    src, dst = _packed(ss, 1 << 20), _packed(ds, 1 << 30)
+    plan.check_tables(src, dst)
+    plan.check_tables(src, _packed(ds, 1 << 30, gap=16))       # abutting destinations are fine
+    aliased = list(src)
+    aliased[1] = aliased[0]                                     # sources may alias each other
+    plan.check_tables(aliased, dst)
+    cases = [
+        ([0] + src[1:], dst, emu.STATUS_CODE["EMU_ERR_NULL"]),
+        (src, dst[:3] + [dst[3] + 8] + dst[4:], emu.STATUS_CODE["EMU_ERR_ALIGN"]),
+        (src, dst[:1] + [dst[0] + 16] + dst[2:], emu.ERR_OVERLAP),          # destination over destination
+        (src, [src[2] + 16] + dst[1:], emu.ERR_OVERLAP),                    # destination inside a source
+        ([dst[5] - 16] + src[1:], dst, emu.ERR_OVERLAP),                    # source reaching into a destination
+    ]
+    for s_, d_, code in cases:
+        with pytest.raises(emu.EmuError) as e:
+            plan.check_tables(s_, d_)
+        assert e.value.code == code, e.value
+
+
+def test_check_tables_sweep_matches_pairwise_brute_force():
+    """Random tables (aligned ranges placed at random in windows from 2x to 3000x their total size, so
+    that both outcomes are common): the library's sorted sweep reports an overlap exactly when some pair
+    of ranges with at least one destination intersects."""
+    import random
+
+    m = emu.Model(*MICRO)
+    plan = emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1))
+    ss = [d["bytes"] for d in plan.tensors(0)]
+    ds = [d["bytes"] for d in plan.tensors(1)]
+    rng = random.Random(3)
+    seen = {0: 0, emu.ERR_OVERLAP: 0}
+    for _ in range(300):
+        window = int((sum(ss) + sum(ds)) * 10 ** rng.uniform(0.3, 3.5))
+        src = [0x10000 + 16 * rng.randrange(window // 16) for _ in ss]
+        dst = [0x10000 + 16 * rng.randrange(window // 16) for _ in ds]
+        ranges = [(a, a + n, False) for a, n in zip(src, ss)] + [(a, a + n, True) for a, n in zip(dst, ds)]
+        clash = any(x[0] < y[1] and y[0] < x[1] and (x[2] or y[2])
+                    for i, x in enumerate(ranges) for y in ranges[i + 1:])
+        try:
+            plan.check_tables(src, dst)
+            rc = 0
+        except emu.EmuError as e:
+            rc = e.code
+        assert rc == (emu.ERR_OVERLAP if clash else 0)
+        seen[rc] += 1
+    assert min(seen.values()) > 20
+
+
+def test_check_bucket_tables():
+    m = emu.Model(*TINY)
+    plan = emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1))
+    B = 100_000
+    ts = [d["bytes"] for d in plan.tensors(1)]
+    bs = []
+    for r in range(plan.info["n_dst_ranks"]):
+        nb, sb = plan.bucket_layout(1, B, r)
+        bs += [min(B, sb - k * B) for k in range(nb)]
+    tp, bp = _packed(ts, 1 << 24), _packed(bs, 1 << 32, gap=16)
+    plan.check_bucket_tables(1, B, tp, bp)
+    with pytest.raises(emu.EmuError) as e:
+        plan.check_bucket_tables(1, B, tp, bp[:2] + [bp[2] - 16] + bp[3:])   # bucket 2 starts inside bucket 1
+    assert e.value.code == emu.ERR_OVERLAP
+    with pytest.raises(emu.EmuError) as e:
+        plan.check_bucket_tables(1, B, tp, [tp[4]] + bp[1:])                 # a bucket over a tensor
+    assert e.value.code == emu.ERR_OVERLAP
+    with pytest.raises(emu.EmuError) as e:
+        plan.check_bucket_tables(1, 0, tp, bp)
+    assert e.value.code == emu.STATUS_CODE["EMU_ERR_BUCKET"]
