@@ -150,6 +150,61 @@ def tiny_latency(emu, iters=200):
             "graph_us_per_step": round(replay, 2), "outputs_consistent": ok}
 
 
+def variant_timings(emu, seed, reps=5):
+    """Mean launch time of the layout variants on the 8B decoder (bf16), each on fresh buffers:
+    the paper's T_sub route (TP4 PP8 -> TP4 PP2 -> TP8 PP2, section 6.1) against the direct
+    destination-driven TP4 PP8 -> TP8 PP2; KV replication with uneven stages (TP2 PP2 -> TP16 PP3); and
+    a format change to separate q/k/v and gate/up (TP2 PP2 -> TP4 PP1)."""
+    import torch
+
+    from synthetic import device_fill
+
+    model = emu.Model(*EIGHT_B)
+
+    def run(chain):
+        plans = [emu.Plan(a, b) for a, b in chain]
+        wss = [p.workspace() for p in plans]
+        sets = [plans[0].alloc(0)] + [p.alloc(1) for p in plans]
+        device_fill(sets[0].tensors, seed, ["norm" if d["kind"].endswith("norm") else "weight"
+                                            for d in plans[0].tensors(0)], "bf16")
+
+        def once():
+            for p, w, x, y in zip(plans, wss, sets, sets[1:]):
+                p.reshard(w, x.ptrs, y.ptrs)
+
+        once()
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
+        e[0].record()
+        for k in range(reps):
+            once()
+            e[k + 1].record()
+        torch.cuda.synchronize()
+        ms = sum(e[k].elapsed_time(e[k + 1]) for k in range(reps)) / reps
+        moved = sum(p.info["bytes_read"] + p.info["bytes_written"] for p in plans)
+        last = sets[-1]
+        del sets, wss
+        torch.cuda.empty_cache()
+        return ms, moved, last, plans[-1]
+
+    L = lambda tp, pp, **kw: emu.Layout(model, tp, pp, **kw)
+    out = {}
+    d_ms, d_b, d_out, _ = run([(L(4, 8), L(8, 2))])
+    t_ms, t_b, t_out, _ = run([(L(4, 8), L(4, 2)), (L(4, 2), L(8, 2))])
+    same = all(torch.equal(a, b) for a, b in zip(d_out.bufs, t_out.bufs))
+    del d_out, t_out
+    torch.cuda.empty_cache()
+    out["tsub_route_tp4pp8_to_tp8pp2"] = {
+        "direct_ms": round(d_ms, 4), "direct_GBps": round(d_b / (d_ms * 1e-3) / 1e9, 1),
+        "via_tp4pp2_ms": round(t_ms, 4), "via_tp4pp2_bytes_over_direct": round(t_b / d_b, 3),
+        "outputs_equal": same}
+    for name, a, b in (("kv_replication_tp2pp2_to_tp16pp3", L(2, 2), L(16, 3)),
+                       ("formats_fused_tp2pp2_to_separate_tp4pp1", L(2, 2), L(4, 1, qkv="separate", mlp="separate"))):
+        ms, moved, _, _ = run([(a, b)])
+        out[name] = {"ms": round(ms, 4), "GBps": round(moved / (ms * 1e-3) / 1e9, 1)}
+    return out
+
+
 def dag_planning(emu):
     """Host-side transition-DAG planning for four model-stages on 1,024 GPUs (8 per node): rollout
     TP4 -> TP8, reward/reference PP2 -> PP4, actor training PP4 -> PP2 on fewer GPUs, critic training
@@ -382,6 +437,8 @@ def main():
     del S, D, R, bufs
     torch.cuda.empty_cache()
     out["tiny_transition_latency"] = tiny_latency(emu)
+    log("timing the layout variants ...")
+    out["variants_8b"] = variant_timings(emu, args.seed)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(args.seed, args.cpu_layers)
