@@ -155,28 +155,38 @@ __device__ __forceinline__ void wg_vec_copy(const uint8_t* __restrict__ s, uint8
 }
 
 // Workgroup-cooperative copy of nv destination-aligned vectors whose source starts `sh` bytes past
-// the 16-byte aligned address sa (0 < sh < 16): each output vector is cut from two aligned source
-// vectors. The second vector of the last output lies in the granule of the last source byte, so no
-// read leaves the granules the copy's own bytes occupy.
+// the 16-byte aligned address sa (0 < sh < 16): each output vector is cut from two consecutive aligned
+// source vectors. Each lane loads one; the next one comes from the neighbouring lane through a
+// cross-lane shuffle, and only lane 63 and the lanes from the last output on load it themselves. The
+// last output's second vector lies in the granule of the last source byte, so no read leaves the
+// granules the copy's own bytes occupy.
 template <int U, bool NT, int Q>
 __device__ __forceinline__ void wg_shift_copy(const uint8_t* __restrict__ sa, uint8_t* __restrict__ d, uint32_t nv,
                                               uint32_t b) {
-  const uint32_t tid = threadIdx.x;
+  const uint32_t tid = threadIdx.x, lane = tid & 63u;
   constexpr uint32_t TV = uint32_t(kThreads) * U;
 #pragma nounroll
   for (uint32_t base = 0; base < nv; base += TV) {
     const uint32_t last = umin(nv - base, TV) - 1;
-    v4u lo[U], hi[U];
+    v4u lo[U], own[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t o = (base + umin(u * kThreads + tid, last)) * 16u;
-      lo[u] = ld16<NT>(sa, o);
-      hi[u] = ld16<NT>(sa, o + 16u);
+    for (int u = 0; u < U; ++u) lo[u] = ld16<NT>(sa, (base + umin(u * kThreads + tid, last)) * 16u);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {  // issued before any wait, next to the loads above
+      const uint32_t i = u * kThreads + tid;
+      own[u] = v4u{0, 0, 0, 0};
+      if (lane == 63u || i >= last) own[u] = ld16<NT>(sa, (base + umin(i, last) + 1u) * 16u);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const uint32_t i = u * kThreads + tid;
-      if (i <= last) st16<NT>(d, (base + i) * 16u, funnel<Q>(lo[u], hi[u], b));
+      v4u hi;
+      hi.x = __shfl_down(lo[u].x, 1u, 64);
+      hi.y = __shfl_down(lo[u].y, 1u, 64);
+      hi.z = __shfl_down(lo[u].z, 1u, 64);
+      hi.w = __shfl_down(lo[u].w, 1u, 64);
+      if (lane == 63u || i >= last) hi = own[u];
+      if (i <= last) st16<NT>(d, (base + i) * 16u, funnel<Q>(lo[u], hi, b));
     }
   }
 }
