@@ -210,7 +210,7 @@ def test_padded_vocab_zero_fill_and_source_pad_not_read(gpu_lib):
 
 
 @pytest.mark.parametrize("tiles", [0, 1], ids=["persistent", "tile_per_wg"])
-@pytest.mark.parametrize("B", [30, 1000, 4094, 65536, 65538, 1 << 20])
+@pytest.mark.parametrize("B", [30, 1000, 4094, 65536, 65538, 1 << 20, 1 << 26])
 def test_buckets_awkward_sizes(gpu_lib, B, tiles):
     m = emu.Model(*TINY)
     old = emu.get_option(emu.OPT_BUCKET_TILES)
@@ -218,6 +218,20 @@ def test_buckets_awkward_sizes(gpu_lib, B, tiles):
     try:
         run_pair(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1), bucket_sizes=(B,))
         run_pair(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 2, 0, "bf16", "separate", "block"), bucket_sizes=(B,))
+    finally:
+        emu.set_option(emu.OPT_BUCKET_TILES, old)
+
+
+@pytest.mark.parametrize("tiles", [1, 0])
+def test_buckets_of_one_element(gpu_lib, tiles):
+    """The smallest legal bucket, one bf16 element (2 bytes): every tensor boundary and every byte pair
+    is its own piece: 1,680 buckets per rank of the micro model. Buckets larger than a whole rank
+    stream (one short bucket per rank) are covered by the 2^26-byte case above."""
+    m = emu.Model(*MICRO)
+    old = emu.get_option(emu.OPT_BUCKET_TILES)
+    emu.set_option(emu.OPT_BUCKET_TILES, tiles)
+    try:
+        run_pair(emu.Layout(m, 2, 2, 2), emu.Layout(m, 4, 1, 2), bucket_sizes=(2, 6))
     finally:
         emu.set_option(emu.OPT_BUCKET_TILES, old)
 
