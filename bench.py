@@ -28,16 +28,26 @@ HBM_PEAK_GBPS = 8000.0
 EIGHT_B = (32, 4096, 32, 128, 8, 14336, 128256)  # L, H, nH, hd, G, I, V
 TINY = (2, 256, 4, 64, 2, 688, 1024)
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "reshard_8b_tp2pp2_tp4pp1_pmc.txt")
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_34645_amd", "csrc", "emu_exec.hip")
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_34645_amd", "csrc", f)
+               for f in ("emu_exec.hip", "emu_internal.h", "emu_plan.cpp")]
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kernel_hash():
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def code_only(text):
+    """Source text without // comments and blank lines, so that edits to comments keep the hash."""
+    lines = (line.split("//", 1)[0].rstrip() for line in text.splitlines())
+    return "\n".join(line for line in lines if line)
+
+
+def kernel_hash(texts=None):
+    """Hash of the code that decides the kernels' HBM traffic: the kernels and the plan compiler that
+    lays out their tiles and tables (comments excluded)."""
+    if texts is None:
+        texts = [open(p).read() for p in KERNEL_SRCS]
+    return hashlib.sha256("\n".join(code_only(t) for t in texts).encode()).hexdigest()[:16]
 
 
 def measured_traffic():
@@ -51,7 +61,7 @@ def measured_traffic():
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 vals[k.strip()] = v.strip()
-    if vals.get("kernel_source_sha256_16") != kernel_hash():
+    if vals.get("kernel_code_sha256_16") != kernel_hash():
         return None
     try:
         return float(vals["reshard_hbm_bytes_per_launch"])

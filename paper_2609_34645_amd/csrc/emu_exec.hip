@@ -1,9 +1,11 @@
 // Device side of the EMU reshard library for CDNA4 (gfx950): the reshard kernel that executes a
 // compiled copy map, the bucket pack/unpack kernel, and the C ABI entry points that launch them.
 //
-// Both kernels are pure HBM streams: no arithmetic on the data, integer address math only. Every
-// thread moves 16-byte vectors (global_load/store_dwordx4), a tile is kThreads * U vectors, and all U
-// loads of a tile are issued before its stores, so that each CU keeps tens of KB of reads in flight.
+// Both kernels are pure HBM streams: no arithmetic on the data (fp32 <-> bf16 conversion aside),
+// integer address math only. Every thread moves 16-byte vectors (global_load/store_dwordx4), a tile is
+// kThreads * U vectors, and all U loads of a tile are issued before its stores. How many tiles are
+// resident per CU is bounded (EMU_OPT_WG_PER_CU), so that each CU keeps 24-48 KB of loads in flight:
+// enough to cover HBM latency, and few enough that the mixed read/write stream does not congest.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -625,7 +627,7 @@ static void launch_reshard(hipStream_t st, const DevSeg* segs, const uint32_t* t
   }
 }
 
-// The copy section with the plan's conversion, then the zero-fill section, for every combination of
+// The copy section of the map, with the plan's conversion, for every combination of
 // the launch options (converting plans: no LDS staging).
 template <int U, int CVT>
 static void launch_copy(bool nt_hint, bool lds, bool xcd, hipStream_t st, const DevSeg* segs, const uint32_t* tm,
