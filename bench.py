@@ -69,10 +69,13 @@ def measured_traffic():
         return None
 
 
-def cpu_baseline(seed, layers, min_seconds=10.0):
-    """Time the CPU oracle on embedding + the first `layers` layers of the same transition: repeated
-    passes until at least `min_seconds`, once on one thread and once with a thread pool over tensor
-    groups on every host core this process may use (NumPy releases the GIL in its copies)."""
+def cpu_baseline(seed, layers, bucket_bytes, min_seconds=10.0):
+    """Time the CPU oracle on the bench step for a bounded sample: the embedding + the first `layers`
+    layers of the same transition, resharded (oracle.reshard_group per tensor group), then each
+    destination rank's part of the sample packed into buckets and unpacked (oracle.pack/unpack).
+    Repeated passes until at least `min_seconds`, once on one thread and once with a thread pool
+    (tensor groups, then ranks) on every host core this process may use; NumPy releases the GIL in its
+    copies. Algorithmic bytes as on the GPU: 2 x destination bytes for each of the three steps."""
     from concurrent.futures import ThreadPoolExecutor
 
     import numpy as np
@@ -90,33 +93,48 @@ def cpu_baseline(seed, layers, min_seconds=10.0):
             if g in groups:
                 shards[(r, j)] = rng.integers(0, 1 << 16, size=s.shape, dtype=np.uint16)
 
-    def one(g):
-        out = oracle.reshard_group(lambda r, j: shards[(r, j)], src, dst, g)
-        return sum(a.nbytes for a in out.values())
+    def reshard(g):
+        return oracle.reshard_group(lambda r, j: shards[(r, j)], src, dst, g)
 
-    def timed(run_pass):
+    def pack_unpack(tensors):
+        buckets = oracle.pack(tensors, bucket_bytes)
+        back = oracle.unpack(buckets, tensors)
+        return sum(a.nbytes for a in back)
+
+    def one_pass(mapper):
+        out = {}
+        for part in mapper(reshard, groups):
+            out.update(part)
+        by_rank = {}
+        for (r, j) in sorted(out):
+            by_rank.setdefault(r, []).append(out[(r, j)])
+        moved = sum(a.nbytes for a in out.values())
+        assert sum(mapper(pack_unpack, [by_rank[r] for r in sorted(by_rank)])) == moved
+        return 6 * moved
+
+    def timed(mapper):
         t = time.perf_counter()
-        passes, out_bytes = 0, 0
+        passes, alg = 0, 0
         while passes < 1 or (time.perf_counter() - t < min_seconds and passes < 50):
-            out_bytes += run_pass()
+            alg += one_pass(mapper)
             passes += 1
-        return time.perf_counter() - t, passes, out_bytes
+        return time.perf_counter() - t, passes, alg
 
-    dt1, p1, b1 = timed(lambda: sum(one(g) for g in groups))
+    dt1, p1, a1 = timed(lambda f, xs: [f(x) for x in xs])
     cores = len(os.sched_getaffinity(0))
     with ThreadPoolExecutor(max_workers=cores) as pool:
-        dtn, pn, bn = timed(lambda: sum(pool.map(one, groups)))
-    single = 2 * b1 / dt1 / 1e9
-    multi = 2 * bn / dtn / 1e9
-    per_pass = 2 * b1 // p1
-    return {"value": round(multi, 3), "unit": "GB/s", "cores": cores, "kind": "oracle",
+        dtn, pn, an = timed(lambda f, xs: list(pool.map(f, xs)))
+    per_pass = a1 // p1
+    return {"value": round(an / dtn / 1e9, 3), "unit": "GB/s", "cores": cores, "kind": "oracle",
             "seconds": round(dtn, 3), "passes": pn, "algorithmic_bytes_per_pass": per_pass,
-            "single_thread": {"value": round(single, 3), "cores": 1, "seconds": round(dt1, 3), "passes": p1},
+            "single_thread": {"value": round(a1 / dt1 / 1e9, 3), "cores": 1, "seconds": round(dt1, 3),
+                              "passes": p1},
             "host_cpu_count": os.cpu_count(),
-            "sample": f"TP2PP2->TP4PP1 reshard of the embedding + layers 0-{layers - 1} of the 8B decoder "
-                      f"(bf16, {per_pass / 2 / 1e9:.2f} GB of destination shards per pass), repeated for at "
-                      f"least {min_seconds:.0f} s; NumPy, tensor groups spread over a pool of {cores} threads "
-                      f"(single_thread: one thread); input generation excluded"}
+            "sample": f"the bench step on the embedding + layers 0-{layers - 1} of the 8B decoder: TP2PP2->TP4PP1 "
+                      f"reshard ({per_pass / 6 / 1e9:.2f} GB of destination shards), then each destination rank's "
+                      f"part packed into {bucket_bytes}-byte buckets and unpacked; repeated for at least "
+                      f"{min_seconds:.0f} s; NumPy, work spread over a pool of {cores} threads (single_thread: "
+                      f"one thread); input generation excluded"}
 
 
 def tiny_latency(emu, iters=200):
@@ -451,7 +469,7 @@ def main():
     out["variants_8b"] = variant_timings(emu, args.seed)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample ...")
-        out["cpu_baseline"] = cpu_baseline(args.seed, args.cpu_layers)
+        out["cpu_baseline"] = cpu_baseline(args.seed, args.cpu_layers, B)
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)
