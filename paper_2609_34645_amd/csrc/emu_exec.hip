@@ -52,6 +52,13 @@ __device__ __forceinline__ v2u ld8(const uint8_t* base, uint32_t off) {
   else return *p;
 }
 
+template <bool NT>
+__device__ __forceinline__ void st8(uint8_t* base, uint32_t off, v2u v) {
+  gv2u* p = (gv2u*)((gu8*)base + off);
+  if constexpr (NT) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+
 // fp32 bits -> bf16 bits: round to nearest, ties to even; a NaN keeps its sign and top payload bits and
 // gets the quiet bit (so that a NaN whose payload sits in the low half never turns into infinity).
 __device__ __forceinline__ uint32_t bf16_rne(uint32_t u) {
@@ -324,23 +331,78 @@ __device__ __forceinline__ void tile_run(const uint8_t* s, uint8_t* d, uint32_t 
   }
 }
 
+// fp32 -> bf16 tiles, in source vectors: a tile of cnt destination vectors reads 2 * cnt source vectors
+// of four fp32 each and writes 2 * cnt eight-byte halves. Each lane loads whole source vectors,
+// consecutive across the lanes, and stores the four converted elements (8 bytes), so every load and
+// every store instruction covers one contiguous span. Reading a destination vector's two source
+// vectors in one lane instead makes every load instruction touch twice the cache lines it uses.
+__device__ __forceinline__ v2u to_bf16x4(v4u a) {
+  return v2u{bf16_rne(a.x) | (bf16_rne(a.y) << 16), bf16_rne(a.z) | (bf16_rne(a.w) << 16)};
+}
+
+template <int U, bool NT>
+__device__ __forceinline__ void tile_run_f32_bf16(const uint8_t* s, uint8_t* d, uint32_t cnt) {
+  const uint32_t tid = threadIdx.x;
+  const uint32_t last = 2 * cnt - 1;
+  v4u a[2 * U];
+#pragma unroll
+  for (int k = 0; k < 2 * U; ++k) a[k] = ld16<NT>(s, umin(k * kThreads + tid, last) * 16u);
+#pragma unroll
+  for (int k = 0; k < 2 * U; ++k) {
+    const uint32_t i = k * kThreads + tid;
+    if (i <= last) st8<NT>(d, i * 8u, to_bf16x4(a[k]));
+  }
+}
+
+// Short rows: half n of the tile is in row n / (2 rv), at half n % (2 rv) of that row; the row comes
+// from the host's magic number for rv applied to n / 2.
+template <int U, bool NT>
+__device__ __forceinline__ void tile_rows_f32_bf16(const DevSeg& g, uint64_t lt, const uint8_t* sb, uint8_t* db) {
+  const uint32_t tid = threadIdx.x;
+  const uint64_t row0 = lt * g.param;
+  const uint32_t nrows = uint32_t(g.rows - row0 < g.param ? g.rows - row0 : g.param);
+  const uint32_t rv = g.rv, h = 2 * rv, mg = g.magic;
+  const uint32_t last = nrows * h - 1;
+  const uint32_t ss = uint32_t(g.src_stride), ds = uint32_t(g.dst_stride);
+  const uint8_t* s = sb + g.src_off + row0 * g.src_stride;
+  uint8_t* d = db + g.dst_off + row0 * g.dst_stride;
+  v4u a[2 * U];
+#pragma unroll
+  for (int k = 0; k < 2 * U; ++k) {
+    const uint32_t n = umin(k * kThreads + tid, last);
+    const uint32_t q = rv > 1 ? __umulhi(n >> 1, mg) : (n >> 1);
+    a[k] = ld16<NT>(s, q * ss + (n - q * h) * 16u);
+  }
+#pragma unroll
+  for (int k = 0; k < 2 * U; ++k) {
+    const uint32_t n = k * kThreads + tid;
+    const uint32_t q = rv > 1 ? __umulhi(n >> 1, mg) : (n >> 1);
+    if (n <= last) st8<NT>(d, q * ds + (n - q * h) * 8u, to_bf16x4(a[k]));
+  }
+}
+
 template <int U, bool NT, bool ZERO, bool LDS, int CVT>
 __device__ __forceinline__ void run_tile(const DevSeg& g, uint64_t lt, const uint8_t* sb, uint8_t* db, v4u* stage) {
   constexpr uint64_t TV = uint64_t(kThreads) * U;
   constexpr uint64_t SV = kSrcVecBytes<CVT>;
   const uint32_t mode = g.mode & SEG_MODE_MASK;
+  constexpr bool kHalves = CVT == CVT_F32_BF16 && !ZERO;
   if (mode == SEG_VEC_1D) {
     const uint64_t nv = g.run / 16, v0 = lt * TV;
     const uint32_t cnt = uint32_t(nv - v0 < TV ? nv - v0 : TV);
-    tile_run<U, NT, ZERO, LDS, CVT>(ZERO ? nullptr : sb + g.src_off + v0 * SV, db + g.dst_off + v0 * 16, cnt, stage);
+    if constexpr (kHalves) tile_run_f32_bf16<U, NT>(sb + g.src_off + v0 * SV, db + g.dst_off + v0 * 16, cnt);
+    else tile_run<U, NT, ZERO, LDS, CVT>(ZERO ? nullptr : sb + g.src_off + v0 * SV, db + g.dst_off + v0 * 16, cnt, stage);
   } else if (mode == SEG_VEC_ROWS) {
-    tile_rows<U, NT, ZERO, LDS, CVT>(g, lt, sb, db, stage);
+    if constexpr (kHalves) tile_rows_f32_bf16<U, NT>(g, lt, sb, db);
+    else tile_rows<U, NT, ZERO, LDS, CVT>(g, lt, sb, db, stage);
   } else if (mode == SEG_VEC_ROWCHUNK) {
     const uint64_t row = lt / g.param, ch = lt - row * g.param;
     const uint64_t nv = g.run / 16, v0 = ch * TV;
     const uint32_t cnt = uint32_t(nv - v0 < TV ? nv - v0 : TV);
-    tile_run<U, NT, ZERO, LDS, CVT>(ZERO ? nullptr : sb + g.src_off + row * g.src_stride + v0 * SV,
-                                    db + g.dst_off + row * g.dst_stride + v0 * 16, cnt, stage);
+    const uint8_t* s = ZERO ? nullptr : sb + g.src_off + row * g.src_stride + v0 * SV;
+    uint8_t* d = db + g.dst_off + row * g.dst_stride + v0 * 16;
+    if constexpr (kHalves) tile_run_f32_bf16<U, NT>(s, d, cnt);
+    else tile_run<U, NT, ZERO, LDS, CVT>(s, d, cnt, stage);
   } else {  // SEG_GENERAL: misaligned runs, moved at a small unroll so that this rare path does not set
             // the kernel's register budget
     const uint64_t row = lt / g.param, ch = lt - row * g.param;
