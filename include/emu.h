@@ -67,7 +67,8 @@ typedef enum {
   EMU_ERR_MISMATCH = -3,    /* source and destination describe different models */
   EMU_ERR_UNSUPPORTED = -4, /* valid by definition but not implemented (pack/unpack of a side with more
                                than 2048 tensors on one rank; more than 2^32 tiles) */
-  EMU_ERR_WORKSPACE = -5,   /* workspace too small or not 256-byte aligned */
+  EMU_ERR_WORKSPACE = -5,   /* workspace too small, not 256-byte aligned, or not holding this plan's
+                               upload (emu_plan_upload) */
   EMU_ERR_BUCKET = -6,      /* bucket size zero or not a multiple of the element size */
   EMU_ERR_ALIGN = -7,       /* a device pointer argument is not 16-byte aligned */
   EMU_ERR_HIP = -8,         /* the HIP runtime reported an error (message in emu_last_error) */
@@ -207,7 +208,10 @@ int emu_tensor_info(emu_plan_t plan, int32_t side, int32_t index, emu_tensor_des
 int emu_plan_segments(emu_plan_t plan, int64_t first, int64_t count, emu_segment_t* out);
 
 /* Enqueue the host-to-device copy of the plan's tables into the caller's workspace (at least
- * info.workspace_bytes, 256-byte aligned). The plan must outlive the copy. */
+ * info.workspace_bytes, 256-byte aligned). The plan must outlive the copy. The library records that
+ * this address now holds this plan's tables: execute calls of the plan accept only a workspace so
+ * recorded (EMU_ERR_WORKSPACE otherwise, before anything is launched), and an upload of another plan to
+ * the same address replaces the record. */
 int emu_plan_upload(emu_plan_t plan, void* d_workspace, uint64_t workspace_bytes, void* hip_stream);
 
 /* Execute the reshard (section 5.2 (a)/(b), the local layout change of section 6.2):

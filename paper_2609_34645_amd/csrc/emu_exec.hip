@@ -751,6 +751,8 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
       return fail(EMU_ERR_UNSUPPORTED, "rank %d has more than %d tensors on this side", r, kMaxRankTensors);
   const uint64_t nchunks = s.chunk_first[s.nranks];
   if (nchunks == 0) return EMU_OK;
+  if (!ws_current(ws, P))
+    return fail(EMU_ERR_WORKSPACE, "workspace %p holds no upload of this plan (fill it with emu_plan_upload)", ws);
   const int cus = device_cus();
   if (cus <= 0) return fail(EMU_ERR_HIP, "cannot query the current device");
   const uint64_t want = uint64_t(cus) * uint64_t(option(EMU_OPT_BUCKET_WG_PER_CU));
@@ -815,6 +817,7 @@ int emu_plan_upload(emu_plan_t plan, void* d_workspace, uint64_t workspace_bytes
   const hipError_t e = hipMemcpyAsync(d_workspace, P->host_ws.data(), P->host_ws.size(), hipMemcpyHostToDevice,
                                       static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return fail(EMU_ERR_HIP, "workspace upload: %s", hipGetErrorString(e));
+  ws_register(d_workspace, P);
   return EMU_OK;
 }
 
@@ -827,6 +830,9 @@ int emu_reshard(emu_plan_t plan, const void* d_workspace, const uint64_t* d_src_
   if (misaligned(d_workspace, kWsAlign)) return fail(EMU_ERR_WORKSPACE, "workspace not %llu-byte aligned", (unsigned long long)kWsAlign);
   if (misaligned(d_src_ptrs, 8) || misaligned(d_dst_ptrs, 8)) return fail(EMU_ERR_ALIGN, "pointer tables must be 8-byte aligned");
   if (P->ntiles == 0) return EMU_OK;
+  if (!ws_current(d_workspace, P))
+    return fail(EMU_ERR_WORKSPACE, "workspace %p holds no upload of this plan (fill it with emu_plan_upload)",
+                d_workspace);
   const uint8_t* w = static_cast<const uint8_t*>(d_workspace);
   const DevSeg* segs = reinterpret_cast<const DevSeg*>(w + P->ws.off_segs);
   const uint32_t* tm = reinterpret_cast<const uint32_t*>(w + P->ws.off_tilemap);

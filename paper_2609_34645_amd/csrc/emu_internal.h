@@ -110,4 +110,11 @@ void clear_error();
 bool plan_live(const Plan* p);
 int64_t option(int32_t key);
 
+// Workspace registry (emu_plan.cpp): which plan's tables were last uploaded to each workspace address.
+// Execute calls refuse a workspace that holds no upload of their plan, so that a forgotten upload or a
+// workspace overwritten by another plan's upload is an error instead of a kernel reading foreign tables.
+void ws_register(const void* ws, const Plan* p);
+bool ws_current(const void* ws, const Plan* p);
+void ws_forget(const Plan* p);
+
 }  // namespace emu

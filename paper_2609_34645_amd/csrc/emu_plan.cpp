@@ -16,6 +16,7 @@
 #include <cstring>
 #include <mutex>
 #include <new>
+#include <unordered_map>
 #include <unordered_set>
 
 #include "emu_internal.h"
@@ -45,6 +46,25 @@ bool plan_live(const Plan* p) {
   if (!p) return false;
   std::lock_guard<std::mutex> lk(g_plans_mu);
   return g_plans.count(p) && p->magic == kPlanMagic;
+}
+
+static std::mutex g_ws_mu;
+static std::unordered_map<const void*, const Plan*> g_ws;
+
+void ws_register(const void* ws, const Plan* p) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  g_ws[ws] = p;
+}
+
+bool ws_current(const void* ws, const Plan* p) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  const auto it = g_ws.find(ws);
+  return it != g_ws.end() && it->second == p;
+}
+
+void ws_forget(const Plan* p) {
+  std::lock_guard<std::mutex> lk(g_ws_mu);
+  for (auto it = g_ws.begin(); it != g_ws.end();) it = it->second == p ? g_ws.erase(it) : std::next(it);
 }
 
 static std::atomic<int64_t> g_opt[7] = {{0}, {1}, {1}, {0}, {32}, {1}, {-1}};
@@ -771,6 +791,7 @@ int emu_plan_free(emu_plan_t plan) {
     if (!P || !g_plans.count(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
     g_plans.erase(P);
   }
+  ws_forget(P);
   P->magic = 0;
   delete P;
   return EMU_OK;

@@ -281,6 +281,22 @@ def test_execute_errors(gpu_lib):
     with pytest.raises(emu.EmuError) as e:
         emu.ptr_table([S.bufs[0][1:]])
     assert e.value.code == -7
+    # workspace registry: refused on the host, before anything is launched
+    fresh = torch.empty(p.info["workspace_bytes"], dtype=torch.uint8, device="cuda")
+    with pytest.raises(emu.EmuError) as e:
+        p.reshard(fresh, S.ptrs, D.ptrs)                  # never uploaded
+    assert e.value.code == -5 and "emu_plan_upload" in str(e.value)
+    with pytest.raises(emu.EmuError) as e:
+        p.pack(fresh, 1, 1 << 16, D.ptrs, D.ptrs)
+    assert e.value.code == -5
+    q = emu.Plan(emu.Layout(m, 2, 1), emu.Layout(m, 1, 1))
+    assert q.info["workspace_bytes"] <= ws.numel()
+    q.upload(ws)                                          # another plan's tables now fill p's workspace
+    with pytest.raises(emu.EmuError) as e:
+        p.reshard(ws, S.ptrs, D.ptrs)
+    assert e.value.code == -5
+    p.upload(ws)
+    p.reshard(ws, S.ptrs, D.ptrs)                         # accepted again after p's own upload
     torch.cuda.synchronize()
 
 
