@@ -413,6 +413,10 @@ def dag_plan(stages, gpus_per_node=8, intra_bw=300e9, inter_bw=25e9, hbm_bw=5e12
     arr = (c_stage_transition * n)()
     keep = []
     for i, s in enumerate(stages):
+        # the C call reads dp*tp*pp (tgt_dp*tgt_tp*tgt_pp) ids; shorter lists would be read past their end
+        if len(s["gpus"]) != s["dp"] * s["tp"] * s["pp"] or \
+                len(s["tgt_gpus"]) != s["tgt_dp"] * s["tgt_tp"] * s["tgt_pp"]:
+            raise EmuError(-11, f"stage {i}: GPU lists must hold dp*tp*pp ids (current and target)")
         g = (ctypes.c_int32 * len(s["gpus"]))(*s["gpus"])
         tg = (ctypes.c_int32 * len(s["tgt_gpus"]))(*s["tgt_gpus"])
         keep += [g, tg]

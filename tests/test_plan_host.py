@@ -453,3 +453,38 @@ def test_check_bucket_tables():
     with pytest.raises(emu.EmuError) as e:
         plan.check_bucket_tables(1, 0, tp, bp)
     assert e.value.code == emu.STATUS_CODE["EMU_ERR_BUCKET"]
+
+
+def test_layout_validation_and_inventory_match_oracle_random():
+    """Random small models and layouts, valid or not (tp up to 8 with and without KV replication, pp up
+    to L + 1, uneven stages, pad multiples, both formats, both element types): emu_layout_check accepts
+    exactly the layouts oracle.check_layout accepts, and for those the library's per-rank tensor inventory
+    (rank, kind, layer, shape, bytes, canonical order) is the oracle's."""
+    import random
+
+    rng = random.Random(17)
+    seen = {True: 0, False: 0}
+    for _ in range(500):
+        nH = rng.choice([2, 4, 6, 8])
+        G = rng.choice([g for g in (1, 2, 3, 4, 8) if nH % g == 0])
+        L = rng.randint(1, 5)
+        shape = (L, rng.choice([8, 16, 24]), nH, rng.choice([2, 4]), G, rng.choice([6, 8, 16, 24]),
+                 rng.choice([8 * rng.randint(1, 5), rng.randint(6, 40)]))
+        args = (rng.choice([1, 1, 2, 2, 3, 4, 8]), rng.randint(1, L + 1), rng.choice([0, 0, 1, 2, 3]),
+                rng.choice(["bf16", "fp32"]), rng.choice(["interleaved", "separate"]), rng.choice(["block", "separate"]))
+        lay = emu.Layout(emu.Model(*shape), *args)
+        ol = o_layout(lay)
+        try:
+            oracle.check_layout(ol)
+            valid = True
+        except oracle.LayoutError:
+            valid = False
+        assert (emu.layout_check(lay) == 0) == valid, (shape, args)
+        seen[valid] += 1
+        if not valid:
+            continue
+        got = [(d["rank"], d["kind"], d["layer"], tuple(d["shape"]), d["bytes"]) for d in emu.Plan(lay, lay).tensors(0)]
+        want = [(r, s.kind, s.layer, tuple(s.shape), s.numel * ol.esize)
+                for r, specs in enumerate(oracle.rank_inventory(ol)) for s in specs]
+        assert got == want, (shape, args)
+    assert min(seen.values()) > 100, seen

@@ -89,3 +89,54 @@ def test_1024_gpu_scenario_and_planning_time():
           f"({got['n_resource_edges']} resource), L_tran {got['l_tran']:.3f} s; "
           f"planning {lib_ms:.3f} ms (library, median of 20) vs {oracle_ms:.1f} ms (oracle)")
     assert lib_ms < 200
+
+
+def test_fuzz_malformed_and_random_inputs_same_verdict():
+    """Random valid scenarios, about a third of them then malformed in one way (a zero or negative
+    degree, a GPU list one id too long or too short, a repeated GPU id, a GPU shared with another
+    model-stage of the same kind): the library never crashes, and its verdict (a DAG, EMU_ERR_ARG or
+    EMU_ERR_INFEASIBLE) is the oracle's (a DAG, ValueError or Infeasible); where both plan, the DAGs are
+    identical."""
+    rng = random.Random(29)
+    seen = {"ok": 0, "arg": 0, "infeasible": 0}
+    for _ in range(600):
+        stages = random_scenario(rng)
+        if rng.random() < 0.35:
+            s = rng.choice(stages)
+            how = rng.randrange(4)
+            if how == 0:
+                setattr(s, rng.choice(["tp", "pp", "dp", "tgt_tp", "tgt_pp", "tgt_dp"]), rng.choice([0, -1]))
+            elif how == 1:
+                lst = rng.choice([s.gpus, s.tgt_gpus])
+                if rng.random() < 0.5 or len(lst) < 2:
+                    lst.append(99)
+                else:
+                    lst.pop()
+            elif how == 2 and len(s.gpus) > 1:
+                s.gpus[1] = s.gpus[0]
+            else:
+                other = st(s.kind, 1, 1, 1, [s.gpus[0]], 1, 1, 1, [50], state=64.0)
+                stages.append(other)
+        try:
+            want = plan(stages, L)
+            verdict = "ok"
+        except ValueError:
+            verdict = "arg"
+        except Infeasible:
+            verdict = "infeasible"
+        try:
+            got = lib_plan(stages)
+            got_v = "ok"
+        except emu.EmuError as e:
+            got_v = {emu.STATUS_CODE["EMU_ERR_ARG"]: "arg", emu.ERR_INFEASIBLE: "infeasible"}[e.code]
+        assert got_v == verdict, stages
+        if verdict == "ok":
+            assert got["l_tran"] == want.l_tran and len(got["nodes"]) == len(want.nodes)
+        seen[verdict] += 1
+    assert min(seen.values()) >= 20, seen
+
+
+def test_negative_gpu_ids_rejected():
+    with pytest.raises(emu.EmuError) as e:
+        lib_plan([st(2, 1, 1, 1, [-3], 1, 1, 1, [0])])
+    assert e.value.code == emu.STATUS_CODE["EMU_ERR_ARG"]
