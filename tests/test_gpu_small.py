@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 FORMATS = [("interleaved", "block"), ("separate", "separate"), ("interleaved", "separate")]
 
 
-def run_pair(src, dst, seed=5, options=None, bucket_sizes=()):
+def run_pair(src, dst, seed=5, options=None, bucket_sizes=(), fused=False):
     import torch
 
     for k, v in (options or {}).items():
@@ -50,6 +50,15 @@ def run_pair(src, dst, seed=5, options=None, bucket_sizes=()):
         check_buckets(plan, 1, B, [ranks[r] for r in sorted(ranks)], bufs, label=f"B={B}")
         for a, b in zip(D.tensors, R.tensors):
             assert torch.equal(a, b)
+        if fused:  # source shards straight into buckets: the same buckets as reshard + pack
+            fp = emu.Plan(src, dst, bucket_bytes=B)
+            fws = fp.workspace()
+            fbufs, fbptrs = plan.alloc_buckets(1, B, fill=0x33)
+            fp.check_tables(S.ptrs, fbptrs)
+            fp.reshard(fws, S.ptrs, fbptrs)
+            torch.cuda.synchronize()
+            for k, (a, b) in enumerate(zip(bufs, fbufs)):
+                assert torch.equal(a, b), f"fused bucket {k} differs (B={B})"
     return plan
 
 
@@ -82,7 +91,8 @@ def random_valid_layout(rng, model, dtype):
 
 def test_random_layout_pairs(gpu_lib):
     """400 random valid layout pairs on random small models, each with a random bucket size: reshard,
-    pack and unpack bit-exact against the oracle. Of the 400: 206 have byte-granular segments (odd widths
+    pack and unpack bit-exact against the oracle, and the fused source -> bucket plan giving the same
+    buckets. Of the 400: 206 have byte-granular segments (odd widths
     put runs at every 16-byte phase), 203 convert between fp32 and bf16, 133 zero-fill pad rows, 177
     replicate KV heads and 141 have uneven pipeline stages."""
     import random
@@ -97,7 +107,7 @@ def test_random_layout_pairs(gpu_lib):
         src = random_valid_layout(rng, model, rng.choice(["bf16", "fp32"]))
         dst = random_valid_layout(rng, model, rng.choice(["bf16", "fp32"]))
         es = 2 if dst.dtype == "bf16" else 4
-        run_pair(src, dst, seed=n, bucket_sizes=(es * rng.randint(1, 700),))
+        run_pair(src, dst, seed=n, bucket_sizes=(es * rng.randint(1, 700),), fused=True)
         n += 1
     say(f"  {n} random layout pairs bit-exact")
 
