@@ -27,6 +27,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0
 EIGHT_B = (32, 4096, 32, 128, 8, 14336, 128256)  # L, H, nH, hd, G, I, V
 TINY = (2, 256, 4, 64, 2, 688, 1024)
+ONE_B = (16, 2048, 32, 64, 8, 8192, 128256)
 PMC_SUMMARY = os.path.join(ROOT, "profiles", "reshard_8b_tp2pp2_tp4pp1_pmc.txt")
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_34645_amd", "csrc", f)
                for f in ("emu_exec.hip", "emu_internal.h", "emu_plan.cpp")]
@@ -233,6 +234,125 @@ def variant_timings(emu, seed, reps=5):
     return out
 
 
+def bench_other_config(args, emu, torch, cfg):
+    """The other workloads, one step each, timed like the default line:
+    1 tiny bf16: Split TP1 PP1 -> TP2 PP1 and Merge back (cache-resident: latency);
+    2 1B bf16: TP4 PP1 -> TP2 PP1;
+    4 8B fp32 training state (master, Adam m, Adam v): TP4 PP1 -> TP1 PP1, one launch per tensor group,
+      then split back, again one launch per group;
+    5 8B bf16, vocabulary padded to a multiple of 128 per TP rank: TP8 PP4 -> TP2 PP2, pack into
+      2^28-byte buckets, unpack into a receiver set."""
+    from synthetic import device_fill
+
+    def dists(plan, side):
+        return ["norm" if d["kind"].endswith("norm") else "weight" for d in plan.tensors(side)]
+
+    calls = []        # (plan, workspace, fn(stream) -> None) in step order, the dominant one first
+    keep = []
+    if cfg in (1, 2):
+        shape, a, b = (TINY, (1, 1), (2, 1)) if cfg == 1 else (ONE_B, (4, 1), (2, 1))
+        m = emu.Model(*shape)
+        fwd = emu.Plan(emu.Layout(m, *a), emu.Layout(m, *b))
+        S, D = fwd.alloc(0), fwd.alloc(1)
+        device_fill(S.tensors, args.seed, dists(fwd, 0), "bf16")
+        wf = fwd.workspace()
+        calls.append(("reshard", fwd, lambda: fwd.reshard(wf, S.ptrs, D.ptrs)))
+        if cfg == 1:
+            back = emu.Plan(emu.Layout(m, *b), emu.Layout(m, *a))
+            wb = back.workspace()
+            A2 = back.alloc(1)
+            calls.append(("reshard back", back, lambda: back.reshard(wb, D.ptrs, A2.ptrs)))
+            keep.append(A2)
+        keep += [S, D]
+        workload = ("tiny decoder bf16: Split TP1PP1->TP2PP1, then Merge back" if cfg == 1 else
+                    "1B decoder bf16: reshard TP4PP1->TP2PP1")
+        model_s = "L2 H256 4x64 heads 2 KV MLP688 V1024" if cfg == 1 else "L16 H2048 32x64 heads 8 KV MLP8192 V128256"
+    elif cfg == 4:
+        m = emu.Model(*EIGHT_B)
+        fwd = emu.Plan(emu.Layout(m, 4, 1, 0, "fp32"), emu.Layout(m, 1, 1, 0, "fp32"))
+        back = emu.Plan(emu.Layout(m, 1, 1, 0, "fp32"), emu.Layout(m, 4, 1, 0, "fp32"))
+        wf, wb = fwd.workspace(), back.workspace()
+        for gi, dist in enumerate(("weight", "adam_m", "adam_v")):
+            S, D = fwd.alloc(0), fwd.alloc(1)
+            device_fill(S.tensors, args.seed + gi, [dist] * len(S.tensors), "fp32")
+            keep += [S, D]
+            calls.append((f"group {gi} TP4->TP1", fwd, lambda S=S, D=D: fwd.reshard(wf, S.ptrs, D.ptrs)))
+        for gi in range(3):
+            S, D = keep[2 * gi], keep[2 * gi + 1]
+            calls.append((f"group {gi} TP1->TP4", back, lambda S=S, D=D: back.reshard(wb, D.ptrs, S.ptrs)))
+        workload = "8B training state fp32 (master, Adam m, Adam v): TP4PP1->TP1PP1 and back, one launch per group"
+        model_s = "L32 H4096 32x128 heads 8 KV MLP14336 V128256"
+    elif cfg == 5:
+        m = emu.Model(*EIGHT_B)
+        plan = emu.Plan(emu.Layout(m, 8, 4, 128), emu.Layout(m, 2, 2))
+        ws = plan.workspace()
+        S, D, R = plan.alloc(0), plan.alloc(1), plan.alloc(1)
+        device_fill(S.tensors, args.seed, dists(plan, 0), "bf16")
+        B = args.bucket_bytes
+        bufs, bptrs = plan.alloc_buckets(1, B)
+        keep += [S, D, R, bufs]
+        calls += [("reshard", plan, lambda: plan.reshard(ws, S.ptrs, D.ptrs)),
+                  ("pack", plan, lambda: plan.pack(ws, 1, B, D.ptrs, bptrs)),
+                  ("unpack", plan, lambda: plan.unpack(ws, 1, B, bptrs, R.ptrs))]
+        workload = "8B decoder bf16, vocab padded to TP*128: reshard TP8PP4->TP2PP2 + pack into 2^28-byte buckets + unpack"
+        model_s = "L32 H4096 32x128 heads 8 KV MLP14336 V128256"
+    else:
+        raise SystemExit(f"unknown config {cfg}")
+    torch.cuda.synchronize()
+
+    def nbytes(name, plan):
+        if name in ("pack", "unpack"):
+            return 2 * plan.bucket_layout(1, args.bucket_bytes, -1)[1]
+        return plan.info["bytes_read"] + plan.info["bytes_written"]
+
+    for _ in range(args.warmup):
+        for _n, _p, fn in calls:
+            fn()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        evs[k][0].record()
+        for j, (_n, _p, fn) in enumerate(calls):
+            fn()
+            evs[k][j + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = [sorted(e[j].elapsed_time(e[j + 1]) for e in evs) for j in range(len(calls))]
+    step_bytes = sum(nbytes(n, p) for n, p, _ in calls)
+    ms_per_step = wall * 1e3 / args.steps
+    r_ms = per[0]
+    r_avg = sum(r_ms) / len(r_ms)
+    r_bytes = nbytes(calls[0][0], calls[0][1])
+    achieved = r_bytes / (r_avg * 1e-3) / 1e9
+    props = torch.cuda.get_device_properties(0)
+    out = {
+        "metric": "reshard HBM GB/s (bytes read+written) and ms per transition, % of HBM peak",
+        "value": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 2),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic (seeded device draws: N(0,0.02) weights, 1+N(0,0.02) norms, Adam m N(0,1e-3), "
+                "v |N(0,1e-6)|)",
+        "config": {"workload": workload, "model": model_s, "bytes_per_step": step_bytes,
+                   "parallelism": "none (1 GPU holds all ranks' shards)", "config_id": cfg},
+        "launches": [{"name": n, "mean_ms": round(sum(t) / len(t), 4), "median_ms": round(t[len(t) // 2], 4),
+                      "GBps": round(nbytes(n, p) / (sum(t) / len(t) * 1e-3) / 1e9, 1)}
+                     for (n, p, _), t in zip(calls, per)],
+        "roofline": {"bound": "hbm", "kernel": "k_reshard", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "algorithmic_bytes_per_launch": r_bytes},
+        "device": {"name": props.name, "cus": props.multi_processor_count,
+                   "hbm_GB": round(props.total_memory / 1e9, 1)},
+        "seed": args.seed,
+        "cpu_baseline": None,
+    }
+    if cfg == 1:
+        out["note"] = "3.95 MB of destination shards: cache-resident and latency-bound; read ms_per_step, not GB/s"
+    del keep
+    return out
+
+
 def dag_planning(emu):
     """Host-side transition-DAG planning for four model-stages on 1,024 GPUs (8 per node): rollout
     TP4 -> TP8, reward/reference PP2 -> PP4, actor training PP4 -> PP2 on fewer GPUs, critic training
@@ -254,6 +374,9 @@ def dag_planning(emu):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5],
+                    help="workload: 1 tiny, 2 1B, 3 8B (default: the headline line), 4 8B fp32 training state, "
+                         "5 8B padded vocabulary with buckets")
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--bucket-bytes", type=int, default=1 << 28)
@@ -286,6 +409,9 @@ def main():
             emu.set_option(opt, v)
 
     torch.cuda.set_device(0)
+    if args.config != 3:
+        print(json.dumps(bench_other_config(args, emu, torch, args.config)), flush=True)
+        return
     dev = torch.device("cuda", 0)
     props = torch.cuda.get_device_properties(dev)
     model = emu.Model(*EIGHT_B)
