@@ -367,6 +367,37 @@ def test_plan_offsets_beyond_4gib():
     assert plan.info["bytes_written"] == sum(d["bytes"] for d in dd) > 2 * (1 << 32)
 
 
+# Llama-shaped 70B and 405B decoders (L, H, heads, head_dim, KV heads, MLP, vocab): host-only plans
+SEVENTY_B = (80, 8192, 64, 128, 8, 28672, 128256)
+FOUR_O_FIVE_B = (126, 16384, 128, 128, 8, 53248, 128256)
+
+
+def test_large_model_plans():
+    """Plans beyond one GPU's memory compile and stay exact: the 70B decoder TP8 PP1 -> TP4 PP2 (141 GB of
+    shards, about 18M tiles) covers every destination byte once, with the oracle's per-rank inventory;
+    the 405B decoder TP8 PP2 -> TP16 PP1 (KV heads replicated to two ranks each; about 106M tiles)
+    reads and writes exactly its destination shards, whose sizes are the oracle's."""
+    m70 = emu.Model(*SEVENTY_B)
+    a, b = emu.Layout(m70, 8, 1), emu.Layout(m70, 4, 2)
+    plan = emu.Plan(a, b)
+    exact_cover(plan)
+    ob = o_layout(b)
+    want = [(r, s.kind, s.layer, tuple(s.shape), s.numel * ob.esize)
+            for r, specs in enumerate(oracle.rank_inventory(ob)) for s in specs]
+    got = [(d["rank"], d["kind"], d["layer"], tuple(d["shape"]), d["bytes"]) for d in plan.tensors(1)]
+    assert got == want
+    assert plan.info["bytes_read"] == plan.info["bytes_written"] == sum(w[4] for w in want) == 141_115_326_464
+    assert plan.info["n_tiles"] * plan.info["tile_bytes"] >= plan.info["bytes_written"]
+
+    m405 = emu.Model(*FOUR_O_FIVE_B)
+    a, b = emu.Layout(m405, 8, 2), emu.Layout(m405, 16, 1)
+    plan = emu.Plan(a, b)
+    ob = o_layout(b)
+    dst = sum(s.numel * ob.esize for specs in oracle.rank_inventory(ob) for s in specs)
+    assert plan.info["bytes_read"] == plan.info["bytes_written"] == plan.info["dst_bytes"] == dst
+    assert plan.info["n_tiles"] > 1 << 26 and plan.info["zero_fill_bytes"] == 0
+
+
 # ------------------------------------------------------------------------------------------------
 # host-side pointer-table checks (emu_check_tables / emu_check_bucket_tables)
 # ------------------------------------------------------------------------------------------------
