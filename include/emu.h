@@ -65,8 +65,8 @@ typedef enum {
   EMU_ERR_NULL = -1,        /* a required pointer argument is NULL */
   EMU_ERR_LAYOUT = -2,      /* a layout does not divide its model (invalid EMU layout) */
   EMU_ERR_MISMATCH = -3,    /* source and destination describe different models */
-  EMU_ERR_UNSUPPORTED = -4, /* valid by definition but not implemented (pack/unpack of a side with more
-                               than 2048 tensors on one rank; more than 2^32 tiles) */
+  EMU_ERR_UNSUPPORTED = -4, /* valid by definition but not implemented (emu_plan: a layout with more
+                               than 2048 tensors on one rank, or a map of more than 2^32 tiles) */
   EMU_ERR_WORKSPACE = -5,   /* workspace too small, not 256-byte aligned, or not holding this plan's
                                upload (emu_plan_upload) */
   EMU_ERR_BUCKET = -6,      /* bucket size zero or not a multiple of the element size */
@@ -159,7 +159,7 @@ typedef enum {
   EMU_OPT_BUCKET_TILES = 5,  /* 1 = pack/unpack with one workgroup per 8 KB stream chunk (upload-time
                                 chunk map; default); 0 = the persistent kernel that scans each rank's
                                 tensor sizes into LDS (also used when the chunk map cannot encode a side:
-                                more than 4096 ranks or 2^20 tensors on one rank) */
+                                4096 or more ranks, or more than 2^20 tensors on the side) */
   EMU_OPT_WG_PER_CU = 6      /* reshard and tile pack/unpack kernels: cap on the workgroups resident
                                 per compute unit, 1..8, enforced by reserving LDS per workgroup (the
                                 LDS is split in two halves, so odd caps above 1 round down to even);

@@ -187,6 +187,11 @@ def test_error_codes():
     with pytest.raises(emu.EmuError) as e:
         emu.Plan(emu.Layout(m, 1, 1), emu.Layout(emu.Model(*MICRO), 1, 1))
     assert e.value.code == -3
+    deep = emu.Model(400, 16, 2, 8, 2, 16, 16)                  # 2,403 tensors on one rank at PP1
+    with pytest.raises(emu.EmuError) as e:
+        emu.Plan(emu.Layout(deep, 1, 2), emu.Layout(deep, 1, 1))
+    assert e.value.code == -4
+    assert emu.Plan(emu.Layout(deep, 1, 2), emu.Layout(deep, 2, 2)).info["n_dst_tensors"] == 2 * (2 * 6 * 200 + 3)
     plan = emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1))
     with pytest.raises(emu.EmuError) as e:
         plan.bucket_layout(1, 0)
