@@ -148,9 +148,10 @@ typedef struct {
 
 /* Tuning knobs (process-wide; change them only while no emu call is running). */
 typedef enum {
-  EMU_OPT_TILE_VECS = 0,     /* 16-byte vectors per thread per reshard tile: 1, 2, 4, 8 or 16, or 0 =
-                                automatic (default): 2 (8 KB tiles) for copy plans, 1 (4 KB) for
-                                converting plans. Read by emu_plan, so a plan keeps its tile size */
+  EMU_OPT_TILE_VECS = 0,     /* 16-byte vectors per thread per reshard tile (the reshard runs 64
+                                threads per workgroup): 1, 2, 4, 8 or 16 (1 to 16 KB tiles), or 0 =
+                                automatic (default): 4 (4 KB tiles). Read by emu_plan, so a plan
+                                keeps its tile size */
   EMU_OPT_XCD_REMAP = 1,     /* 1 = give each XCD one contiguous eighth of the reshard tiles instead of
                                 every eighth tile (default 1) */
   EMU_OPT_NONTEMPORAL = 2,   /* 1 = streaming (non-temporal) loads and stores (default 1) */
@@ -161,11 +162,12 @@ typedef enum {
                                 tensor sizes into LDS (also used when the chunk map cannot encode a side:
                                 4096 or more ranks, or more than 2^20 tensors on the side) */
   EMU_OPT_WG_PER_CU = 6      /* reshard and tile pack/unpack kernels: cap on the workgroups resident
-                                per compute unit, 1..8, enforced by reserving LDS per workgroup (the
+                                per compute unit, 1..32, enforced by reserving LDS per workgroup (the
                                 LDS is split in two halves, so odd caps above 1 round down to even);
-                                0 = no cap; -1 = automatic (default): 6 for 8 KB reshard tiles, 2 for
-                                larger ones, none for 4 KB tiles and for pack/unpack. Bounds the bytes
-                                in flight per CU, which sets how well HBM serves a read/write stream */
+                                0 = no cap; -1 = automatic (default): 48 KB of reshard tiles (12 of
+                                4 KB, 6 of 8 KB; at least 2, no cap from 32 up), no cap for
+                                pack/unpack. Bounds the bytes in flight per CU, which sets how well
+                                HBM serves a read/write stream */
 } emu_option;
 
 /* Library version (EMU_ABI_VERSION). */

@@ -3,9 +3,11 @@
 //
 // Both kernels are pure HBM streams: no arithmetic on the data (fp32 <-> bf16 conversion aside),
 // integer address math only. Every thread moves 16-byte vectors (global_load/store_dwordx4), a tile is
-// kThreads * U vectors, and all U loads of a tile are issued before its stores. How many tiles are
-// resident per CU is bounded (EMU_OPT_WG_PER_CU), so that each CU keeps 24-48 KB of loads in flight:
-// enough to cover HBM latency, and few enough that the mixed read/write stream does not congest.
+// threads * U vectors, and all U loads of a tile are issued before its stores. How many tiles are
+// resident per CU is bounded (EMU_OPT_WG_PER_CU), so that each CU keeps about 48 KB of loads in
+// flight: enough to cover HBM latency, and few enough that the mixed read/write stream does not
+// congest. The reshard runs one wave64 per workgroup, so that each tile's address computation (map
+// entry, descriptor, pointers) is done once rather than once per wave.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -106,9 +108,9 @@ __device__ __forceinline__ v4u cook(const Raw<CVT>& r) {
 }
 
 // Element-wise conversion of n destination elements (misaligned converting segments; rare).
-template <int CVT>
+template <int NTH, int CVT>
 __device__ void wg_convert_elems(const uint8_t* s, uint8_t* d, uint32_t n) {
-  for (uint32_t i = threadIdx.x; i < n; i += kThreads) {
+  for (uint32_t i = threadIdx.x; i < n; i += NTH) {
     if constexpr (CVT == CVT_F32_BF16) {
       const uint32_t u = *(const __attribute__((address_space(1))) uint32_t*)((const gu8*)s + 4u * i);
       *(__attribute__((address_space(1))) uint16_t*)((gu8*)d + 2u * i) = uint16_t(bf16_rne(u));
@@ -142,10 +144,10 @@ __device__ __forceinline__ v4u funnel(v4u lo, v4u hi, uint32_t b) {
 // nv * 16 must fit in 32 bits: offsets are 32-bit from uniform base pointers. Lanes past the end load
 // the last valid vector again (so every load is unconditional and all U are in flight together) and
 // skip their store.
-template <int U, bool NT, bool ZERO>
+template <int NTH, int U, bool NT, bool ZERO>
 __device__ __forceinline__ void wg_vec_copy(const uint8_t* __restrict__ s, uint8_t* __restrict__ d, uint32_t nv) {
   const uint32_t tid = threadIdx.x;
-  constexpr uint32_t TV = uint32_t(kThreads) * U;
+  constexpr uint32_t TV = uint32_t(NTH) * U;
 #pragma nounroll
   for (uint32_t base = 0; base < nv; base += TV) {
     const uint32_t last = umin(nv - base, TV) - 1;
@@ -153,11 +155,11 @@ __device__ __forceinline__ void wg_vec_copy(const uint8_t* __restrict__ s, uint8
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if constexpr (ZERO) r[u] = v4u{0, 0, 0, 0};
-      else r[u] = ld16<NT>(s, (base + umin(u * kThreads + tid, last)) * 16u);
+      else r[u] = ld16<NT>(s, (base + umin(u * NTH + tid, last)) * 16u);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const uint32_t i = u * kThreads + tid;
+      const uint32_t i = u * NTH + tid;
       if (i <= last) st16<NT>(d, (base + i) * 16u, r[u]);
     }
   }
@@ -169,26 +171,26 @@ __device__ __forceinline__ void wg_vec_copy(const uint8_t* __restrict__ s, uint8
 // cross-lane shuffle, and only lane 63 and the lanes from the last output on load it themselves. The
 // last output's second vector lies in the granule of the last source byte, so no read leaves the
 // granules the copy's own bytes occupy.
-template <int U, bool NT, int Q>
+template <int NTH, int U, bool NT, int Q>
 __device__ __forceinline__ void wg_shift_copy(const uint8_t* __restrict__ sa, uint8_t* __restrict__ d, uint32_t nv,
                                               uint32_t b) {
   const uint32_t tid = threadIdx.x, lane = tid & 63u;
-  constexpr uint32_t TV = uint32_t(kThreads) * U;
+  constexpr uint32_t TV = uint32_t(NTH) * U;
 #pragma nounroll
   for (uint32_t base = 0; base < nv; base += TV) {
     const uint32_t last = umin(nv - base, TV) - 1;
     v4u lo[U], own[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) lo[u] = ld16<NT>(sa, (base + umin(u * kThreads + tid, last)) * 16u);
+    for (int u = 0; u < U; ++u) lo[u] = ld16<NT>(sa, (base + umin(u * NTH + tid, last)) * 16u);
 #pragma unroll
     for (int u = 0; u < U; ++u) {  // issued before any wait, next to the loads above
-      const uint32_t i = u * kThreads + tid;
+      const uint32_t i = u * NTH + tid;
       own[u] = v4u{0, 0, 0, 0};
       if (lane == 63u || i >= last) own[u] = ld16<NT>(sa, (base + umin(i, last) + 1u) * 16u);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const uint32_t i = u * kThreads + tid;
+      const uint32_t i = u * NTH + tid;
       v4u hi;
       hi.x = __shfl_down(lo[u].x, 1u, 64);
       hi.y = __shfl_down(lo[u].y, 1u, 64);
@@ -204,7 +206,7 @@ __device__ __forceinline__ void wg_shift_copy(const uint8_t* __restrict__ sa, ui
 // The destination drives the split: a head up to the first 16-byte boundary, a vector body and a
 // tail, the head and tail moved byte by byte. UA is the unroll of the co-aligned body, US that of the
 // realigned body (which holds two source vectors per output vector).
-template <int UA, int US, bool NT, bool ZERO>
+template <int NTH, int UA, int US, bool NT, bool ZERO>
 __device__ __forceinline__ void wg_copy_bytes(const uint8_t* s, uint8_t* d, uint32_t n) {
   const uint32_t tid = threadIdx.x;
   const uint32_t head0 = (16u - uint32_t(reinterpret_cast<uintptr_t>(d) & 15)) & 15u;
@@ -215,25 +217,25 @@ __device__ __forceinline__ void wg_copy_bytes(const uint8_t* s, uint8_t* d, uint
   if (tid < tail) d[head + nv * 16u + tid] = ZERO ? 0 : s[head + nv * 16u + tid];
   if (nv == 0) return;
   if constexpr (ZERO) {
-    wg_vec_copy<UA, NT, true>(nullptr, d + head, nv);
+    wg_vec_copy<NTH, UA, NT, true>(nullptr, d + head, nv);
   } else {
     const uint32_t sh = uint32_t(reinterpret_cast<uintptr_t>(s + head) & 15);
     if (sh == 0) {
-      wg_vec_copy<UA, NT, false>(s + head, d + head, nv);
+      wg_vec_copy<NTH, UA, NT, false>(s + head, d + head, nv);
     } else {
       const uint8_t* sa = s + head - sh;
       switch (sh >> 2) {
-        case 0: wg_shift_copy<US, NT, 0>(sa, d + head, nv, sh & 3); break;
-        case 1: wg_shift_copy<US, NT, 1>(sa, d + head, nv, sh & 3); break;
-        case 2: wg_shift_copy<US, NT, 2>(sa, d + head, nv, sh & 3); break;
-        default: wg_shift_copy<US, NT, 3>(sa, d + head, nv, sh & 3); break;
+        case 0: wg_shift_copy<NTH, US, NT, 0>(sa, d + head, nv, sh & 3); break;
+        case 1: wg_shift_copy<NTH, US, NT, 1>(sa, d + head, nv, sh & 3); break;
+        case 2: wg_shift_copy<NTH, US, NT, 2>(sa, d + head, nv, sh & 3); break;
+        default: wg_shift_copy<NTH, US, NT, 3>(sa, d + head, nv, sh & 3); break;
       }
     }
   }
 }
 
 // ------------------------------------------------------------------------------------------------
-// reshard kernel: one tile = kThreads * U destination vectors of one segment
+// reshard kernel: one tile = kReshardThreads * U destination vectors of one segment
 // ------------------------------------------------------------------------------------------------
 
 #ifndef EMU_RESHARD_WAVES_PER_EU
@@ -262,10 +264,10 @@ __device__ __forceinline__ void stage_through_lds(v4u (&r)[U], v4u* stage) {
   if constexpr (LDS) {
     const uint32_t tid = threadIdx.x;
 #pragma unroll
-    for (int u = 0; u < U; ++u) stage[u * kThreads + tid] = r[u];
+    for (int u = 0; u < U; ++u) stage[u * kReshardThreads + tid] = r[u];
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < U; ++u) r[u] = stage[u * kThreads + tid];
+    for (int u = 0; u < U; ++u) r[u] = stage[u * kReshardThreads + tid];
     __syncthreads();
   }
 }
@@ -291,7 +293,7 @@ __device__ __forceinline__ void tile_rows(const DevSeg& g, uint64_t lt, const ui
     Raw<CVT> raw[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const uint32_t n = umin(u * kThreads + tid, last);
+      const uint32_t n = umin(u * kReshardThreads + tid, last);
       const uint32_t q = rv > 1 ? __umulhi(n, mg) : n;
       raw[u] = ld_raw<CVT, NT>(s, q * ss + (n - q * rv) * kSrcVecBytes<CVT>);
     }
@@ -301,13 +303,13 @@ __device__ __forceinline__ void tile_rows(const DevSeg& g, uint64_t lt, const ui
   stage_through_lds<U, LDS>(r, stage);
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    const uint32_t n = u * kThreads + tid;
+    const uint32_t n = u * kReshardThreads + tid;
     const uint32_t q = rv > 1 ? __umulhi(n, mg) : n;
     if (n <= last) st16<NT>(d, q * ds + (n - q * rv) * 16u, r[u]);
   }
 }
 
-// A contiguous run of cnt (1 <= cnt <= kThreads * U) destination vectors.
+// A contiguous run of cnt (1 <= cnt <= kReshardThreads * U) destination vectors.
 template <int U, bool NT, bool ZERO, bool LDS, int CVT>
 __device__ __forceinline__ void tile_run(const uint8_t* s, uint8_t* d, uint32_t cnt, v4u* stage) {
   const uint32_t tid = threadIdx.x;
@@ -319,14 +321,14 @@ __device__ __forceinline__ void tile_run(const uint8_t* s, uint8_t* d, uint32_t 
   } else {
     Raw<CVT> raw[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) raw[u] = ld_raw<CVT, NT>(s, umin(u * kThreads + tid, last) * kSrcVecBytes<CVT>);
+    for (int u = 0; u < U; ++u) raw[u] = ld_raw<CVT, NT>(s, umin(u * kReshardThreads + tid, last) * kSrcVecBytes<CVT>);
 #pragma unroll
     for (int u = 0; u < U; ++u) r[u] = cook<CVT>(raw[u]);
   }
   stage_through_lds<U, LDS>(r, stage);
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    const uint32_t i = u * kThreads + tid;
+    const uint32_t i = u * kReshardThreads + tid;
     if (i <= last) st16<NT>(d, i * 16u, r[u]);
   }
 }
@@ -346,10 +348,10 @@ __device__ __forceinline__ void tile_run_f32_bf16(const uint8_t* s, uint8_t* d, 
   const uint32_t last = 2 * cnt - 1;
   v4u a[2 * U];
 #pragma unroll
-  for (int k = 0; k < 2 * U; ++k) a[k] = ld16<NT>(s, umin(k * kThreads + tid, last) * 16u);
+  for (int k = 0; k < 2 * U; ++k) a[k] = ld16<NT>(s, umin(k * kReshardThreads + tid, last) * 16u);
 #pragma unroll
   for (int k = 0; k < 2 * U; ++k) {
-    const uint32_t i = k * kThreads + tid;
+    const uint32_t i = k * kReshardThreads + tid;
     if (i <= last) st8<NT>(d, i * 8u, to_bf16x4(a[k]));
   }
 }
@@ -369,13 +371,13 @@ __device__ __forceinline__ void tile_rows_f32_bf16(const DevSeg& g, uint64_t lt,
   v4u a[2 * U];
 #pragma unroll
   for (int k = 0; k < 2 * U; ++k) {
-    const uint32_t n = umin(k * kThreads + tid, last);
+    const uint32_t n = umin(k * kReshardThreads + tid, last);
     const uint32_t q = rv > 1 ? __umulhi(n >> 1, mg) : (n >> 1);
     a[k] = ld16<NT>(s, q * ss + (n - q * h) * 16u);
   }
 #pragma unroll
   for (int k = 0; k < 2 * U; ++k) {
-    const uint32_t n = k * kThreads + tid;
+    const uint32_t n = k * kReshardThreads + tid;
     const uint32_t q = rv > 1 ? __umulhi(n >> 1, mg) : (n >> 1);
     if (n <= last) st8<NT>(d, q * ds + (n - q * h) * 8u, to_bf16x4(a[k]));
   }
@@ -383,7 +385,7 @@ __device__ __forceinline__ void tile_rows_f32_bf16(const DevSeg& g, uint64_t lt,
 
 template <int U, bool NT, bool ZERO, bool LDS, int CVT>
 __device__ __forceinline__ void run_tile(const DevSeg& g, uint64_t lt, const uint8_t* sb, uint8_t* db, v4u* stage) {
-  constexpr uint64_t TV = uint64_t(kThreads) * U;
+  constexpr uint64_t TV = uint64_t(kReshardThreads) * U;
   constexpr uint64_t SV = kSrcVecBytes<CVT>;
   const uint32_t mode = g.mode & SEG_MODE_MASK;
   constexpr bool kHalves = CVT == CVT_F32_BF16 && !ZERO;
@@ -410,12 +412,12 @@ __device__ __forceinline__ void run_tile(const DevSeg& g, uint64_t lt, const uin
     const uint32_t n = uint32_t(g.run - b0 < TV * 16 ? g.run - b0 : TV * 16);
     uint8_t* d = db + g.dst_off + row * g.dst_stride + b0;
     if constexpr (CVT == CVT_NONE || ZERO) {
-      wg_copy_bytes<kGeneralUnroll, kGeneralUnroll, NT, ZERO>(ZERO ? nullptr : sb + g.src_off + row * g.src_stride + b0,
+      wg_copy_bytes<kReshardThreads, kGeneralUnroll, kGeneralUnroll, NT, ZERO>(ZERO ? nullptr : sb + g.src_off + row * g.src_stride + b0,
                                                               d, n);
     } else {
       constexpr uint32_t esd = CVT == CVT_F32_BF16 ? 2u : 4u;  // destination element bytes
       constexpr uint32_t ess = CVT == CVT_F32_BF16 ? 4u : 2u;  // source element bytes
-      wg_convert_elems<CVT>(sb + g.src_off + row * g.src_stride + b0 / esd * ess, d, n / esd);
+      wg_convert_elems<kReshardThreads, CVT>(sb + g.src_off + row * g.src_stride + b0 / esd * ess, d, n / esd);
     }
   }
 }
@@ -425,7 +427,7 @@ __device__ __forceinline__ void run_tile(const DevSeg& g, uint64_t lt, const uin
 // XCD's L2 sees one stream instead of every eighth tile of all of them. ZERO instances run the map's
 // zero-fill section, the others its copy section.
 template <int U, bool NT, bool LDS, bool XCD, int CVT, bool ZERO>
-__global__ __launch_bounds__(kThreads, EMU_RESHARD_WAVES_PER_EU) void k_reshard(const DevSeg* __restrict__ segs,
+__global__ __launch_bounds__(kReshardThreads, EMU_RESHARD_WAVES_PER_EU) void k_reshard(const DevSeg* __restrict__ segs,
                                                                              const uint32_t* __restrict__ tilemap,
                                                                              uint64_t tile_base,
                                                                              const uint64_t* __restrict__ src_ptrs,
@@ -552,8 +554,8 @@ __global__ __launch_bounds__(kThreads, EMU_BUCKET_WAVES_PER_EU) void k_buckets(c
       uint8_t* tp = reinterpret_cast<uint8_t*>(tensor_ptrs[t0 + ti]) + (pos - toff);
       uint8_t* bp = reinterpret_cast<uint8_t*>(bucket_ptrs[bucket0 + k]) + (pos - k * B);
       const uint32_t n = uint32_t(pend - pos);
-      if constexpr (UNPACK) wg_copy_bytes<U, kShiftUnroll, NT, false>(bp, tp, n);
-      else wg_copy_bytes<U, kShiftUnroll, NT, false>(tp, bp, n);
+      if constexpr (UNPACK) wg_copy_bytes<kThreads, U, kShiftUnroll, NT, false>(bp, tp, n);
+      else wg_copy_bytes<kThreads, U, kShiftUnroll, NT, false>(tp, bp, n);
       pos = pend;
       if (pos == kend) {
         ++k;
@@ -613,8 +615,8 @@ __global__ __launch_bounds__(kThreads, EMU_RESHARD_WAVES_PER_EU) void k_buckets_
     uint8_t* tp = reinterpret_cast<uint8_t*>(tensor_ptrs[g]) + (pos - toff);
     uint8_t* bp = reinterpret_cast<uint8_t*>(bucket_ptrs[bucket0 + k]) + (pos - k * B);
     const uint32_t n = uint32_t(pend - pos);
-    if constexpr (UNPACK) wg_copy_bytes<U, kShiftUnroll, NT, false>(bp, tp, n);
-    else wg_copy_bytes<U, kShiftUnroll, NT, false>(tp, bp, n);
+    if constexpr (UNPACK) wg_copy_bytes<kThreads, U, kShiftUnroll, NT, false>(bp, tp, n);
+    else wg_copy_bytes<kThreads, U, kShiftUnroll, NT, false>(tp, bp, n);
     pos = pend;
     if (pos == kend) {
       ++k;
@@ -650,15 +652,19 @@ static int device_cus() {
 
 // Dynamic LDS for a tile kernel that needs `need` bytes and moves `tile_bytes` per workgroup pass.
 // A residency cap of c workgroups per CU (EMU_OPT_WG_PER_CU) is enforced by reserving the CU's LDS
-// divided by c, in whole KB; the kernels never touch the reserved bytes. The CU's LDS is allocated in
-// two halves and a workgroup's block lies in one half, so the resident count is 2 * floor(c / 2) for
-// c >= 2 (c = 1 keeps one). The cap bounds the bytes in flight per CU: on MI355X a copy stream runs
-// fastest with about 32-48 KB in flight per CU and drops by about 8% at 128 KB (8 workgroups of
-// 16 KB tiles), where the HBM read/write mix degrades. Automatic (-1): 6 workgroups for 8 KB tiles,
-// 2 for larger tiles, no cap for smaller ones (8 resident 4 KB tiles are 32 KB already).
+// divided by c, rounded down to whole KB; the kernels never touch the reserved bytes. The CU's LDS is
+// allocated in two halves and a workgroup's block lies in one half, so the resident count is
+// 2 * floor(c / 2) for c >= 2 (c = 1 keeps one). The cap bounds the bytes in flight per CU: on MI355X
+// a copy stream runs fastest with about 24-48 KB in flight per CU and drops by about 8% at 128 KB,
+// where the HBM read/write mix degrades. Automatic (-1): kAutoFlightBytes / tile_bytes workgroups
+// (12 for the reshard's 4 KB tiles, 6 for 8 KB), at least 2, and no cap from 32 up.
+constexpr uint64_t kAutoFlightBytes = 48 * 1024;
 static size_t occupancy_lds(size_t need, uint64_t tile_bytes) {
   int64_t cap = option(EMU_OPT_WG_PER_CU);
-  if (cap < 0) cap = tile_bytes <= 4096 ? 0 : tile_bytes <= 8192 ? 6 : 2;
+  if (cap < 0) {
+    cap = int64_t(kAutoFlightBytes / (tile_bytes ? tile_bytes : 1));
+    cap = cap < 2 ? 2 : cap >= 32 ? 0 : cap;
+  }
   if (cap == 0) return need;
   const int per_cu = device_attr(hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, 1);
   const int per_wg = device_attr(hipDeviceAttributeMaxSharedMemoryPerBlock, 2);
@@ -679,12 +685,12 @@ static int hip_check(const char* what) {
 template <int U, bool NT, bool LDS, bool XCD, int CVT, bool ZERO>
 static void launch_reshard(hipStream_t st, const DevSeg* segs, const uint32_t* tm, uint64_t first, uint64_t count,
                            const uint64_t* sp, const uint64_t* dp) {
-  const size_t lds = occupancy_lds(LDS ? size_t(kThreads) * U * 16 : 0, uint64_t(kThreads) * U * 16);
+  const size_t lds = occupancy_lds(LDS ? size_t(kReshardThreads) * U * 16 : 0, uint64_t(kReshardThreads) * U * 16);
   constexpr uint64_t kMaxGrid = 0x7ffffff8ull;  // a multiple of kXcds below the grid-size limit
   for (uint64_t done = 0; done < count; done += kMaxGrid) {
     const uint32_t n = uint32_t(count - done < kMaxGrid ? count - done : kMaxGrid);
     const uint32_t grid = XCD ? (n + kXcds - 1) / kXcds * kXcds : n;
-    hipLaunchKernelGGL((k_reshard<U, NT, LDS, XCD, CVT, ZERO>), dim3(grid), dim3(kThreads), lds, st, segs, tm,
+    hipLaunchKernelGGL((k_reshard<U, NT, LDS, XCD, CVT, ZERO>), dim3(grid), dim3(kReshardThreads), lds, st, segs, tm,
                        first + done, sp, dp);
   }
 }

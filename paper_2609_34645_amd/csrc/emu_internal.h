@@ -11,7 +11,8 @@
 namespace emu {
 
 constexpr uint32_t kPlanMagic = 0x454d5550u;  // "EMUP"
-constexpr int kThreads = 256;                 // workgroup size of every kernel (4 wave64s)
+constexpr int kThreads = 256;                 // workgroup size of the pack/unpack kernels (4 wave64s)
+constexpr int kReshardThreads = 64;           // workgroup size of the reshard kernel (one wave64)
 constexpr int kMaxRankTensors = 2048;         // per-rank tensor offsets live in LDS during pack/unpack
 #ifndef EMU_CHUNK_BYTES
 #define EMU_CHUNK_BYTES 32768

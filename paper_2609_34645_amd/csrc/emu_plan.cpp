@@ -422,7 +422,7 @@ static int to_buckets(Plan& P, uint64_t B) {
 // Device segments, tiles and the workspace image.
 static int finalize(Plan& P) {
   const int U = P.tile_vecs;
-  const uint64_t TV = uint64_t(kThreads) * U;  // vectors per tile
+  const uint64_t TV = uint64_t(kReshardThreads) * U;  // vectors per tile
   const uint64_t TB = TV * 16;                 // bytes per tile
   P.tile_bytes = TB;
   P.dsegs.clear();
@@ -683,7 +683,7 @@ int emu_set_option(int32_t key, int64_t value) {
         return fail(EMU_ERR_ARG, "tile vectors must be 0 (automatic), 1, 2, 4, 8 or 16");
       break;
     case EMU_OPT_WG_PER_CU:
-      if (value < -1 || value > 8) return fail(EMU_ERR_ARG, "resident workgroups per CU must be in [-1, 8]");
+      if (value < -1 || value > 32) return fail(EMU_ERR_ARG, "resident workgroups per CU must be in [-1, 32]");
       break;
     case EMU_OPT_BUCKET_WG_PER_CU:
       if (value < 1 || value > 64) return fail(EMU_ERR_ARG, "workgroups per CU must be in [1, 64]");
@@ -728,11 +728,11 @@ int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out) 
   if (!P) return fail(EMU_ERR_ARG, "out of host memory");
   try {
     P->cvt = src->dtype == dst->dtype ? CVT_NONE : (src->dtype == EMU_FP32 ? CVT_F32_BF16 : CVT_BF16_F32);
-    // automatic tile size: 8 KB tiles for copies, 4 KB for converting plans (whose tiles read up to
-    // twice their bytes), the sizes that ran fastest on MI355X together with the residency rule of the
+    // automatic tile size: 4 KB (4 vectors per lane of the one-wave workgroup), the size that ran
+    // fastest on MI355X for copying and converting plans together with the residency rule of the
     // launch (EMU_OPT_WG_PER_CU)
     const int64_t tv = option(EMU_OPT_TILE_VECS);
-    P->tile_vecs = tv > 0 ? int(tv) : (P->cvt == CVT_NONE ? 2 : 1);
+    P->tile_vecs = tv > 0 ? int(tv) : 4;
     std::vector<std::vector<Block>> sb, db;
     rc = build_side(*src, P->side[0], sb);
     if (!rc) rc = build_side(*dst, P->side[1], db);

@@ -207,6 +207,8 @@ def test_tiny_transition_in_a_hip_graph(gpu_lib):
     {emu.OPT_NONTEMPORAL: 0}, {emu.OPT_LDS_STAGING: 1}, {emu.OPT_LDS_STAGING: 1, emu.OPT_TILE_VECS: 16},
     {emu.OPT_TILE_VECS: 1}, {emu.OPT_TILE_VECS: 2, emu.OPT_WG_PER_CU: 6}, {emu.OPT_WG_PER_CU: 0},
     {emu.OPT_WG_PER_CU: 1, emu.OPT_LDS_STAGING: 1}, {emu.OPT_WG_PER_CU: 8, emu.OPT_BUCKET_TILES: 0},
+    {emu.OPT_WG_PER_CU: 12}, {emu.OPT_WG_PER_CU: 24, emu.OPT_TILE_VECS: 2},
+    {emu.OPT_WG_PER_CU: 32, emu.OPT_TILE_VECS: 1}, {emu.OPT_TILE_VECS: 4, emu.OPT_LDS_STAGING: 1},
 ])
 def test_launch_options(gpu_lib, opts):
     defaults = {k: emu.get_option(k) for k in range(7)}

@@ -215,7 +215,7 @@ def test_error_codes():
     assert b"live plan" in lib.emu_last_error()
     assert lib.emu_set_option(0, 5) == -11
     assert lib.emu_set_option(99, 1) == -10
-    assert lib.emu_set_option(emu.OPT_WG_PER_CU, 9) == -11 and lib.emu_set_option(emu.OPT_WG_PER_CU, -2) == -11
+    assert lib.emu_set_option(emu.OPT_WG_PER_CU, 33) == -11 and lib.emu_set_option(emu.OPT_WG_PER_CU, -2) == -11
     assert lib.emu_set_option(7, 0) == -10
     for s in range(-11, 1):
         assert lib.emu_status_str(s).startswith(b"EMU_")
