@@ -157,7 +157,7 @@ typedef enum {
   EMU_OPT_NONTEMPORAL = 2,   /* 1 = streaming (non-temporal) loads and stores (default 1) */
   EMU_OPT_LDS_STAGING = 3,   /* 1 = stage each tile through LDS between load and store (default 0) */
   EMU_OPT_BUCKET_WG_PER_CU = 4, /* persistent pack/unpack grid: workgroups per compute unit (default 32) */
-  EMU_OPT_BUCKET_TILES = 5,  /* 1 = pack/unpack with one workgroup per 8 KB stream chunk (upload-time
+  EMU_OPT_BUCKET_TILES = 5,  /* 1 = pack/unpack with one workgroup per 4 KB stream chunk (upload-time
                                 chunk map; default); 0 = the persistent kernel that scans each rank's
                                 tensor sizes into LDS (also used when the chunk map cannot encode a side:
                                 4096 or more ranks, or more than 2^20 tensors on the side) */
@@ -165,9 +165,9 @@ typedef enum {
                                 per compute unit, 1..32, enforced by reserving LDS per workgroup (the
                                 LDS is split in two halves, so odd caps above 1 round down to even);
                                 0 = no cap; -1 = automatic (default): 48 KB of reshard tiles (12 of
-                                4 KB, 6 of 8 KB; at least 2, no cap from 32 up), no cap for
-                                pack/unpack. Bounds the bytes in flight per CU, which sets how well
-                                HBM serves a read/write stream */
+                                4 KB, 6 of 8 KB) and 64 KB of pack/unpack chunks (16 of 4 KB); at
+                                least 2, no cap from 32 up. Bounds the bytes in flight per CU, which
+                                sets how well HBM serves a read/write stream */
 } emu_option;
 
 /* Library version (EMU_ABI_VERSION). */

@@ -4,10 +4,10 @@
 // Both kernels are pure HBM streams: no arithmetic on the data (fp32 <-> bf16 conversion aside),
 // integer address math only. Every thread moves 16-byte vectors (global_load/store_dwordx4), a tile is
 // threads * U vectors, and all U loads of a tile are issued before its stores. How many tiles are
-// resident per CU is bounded (EMU_OPT_WG_PER_CU), so that each CU keeps about 48 KB of loads in
-// flight: enough to cover HBM latency, and few enough that the mixed read/write stream does not
-// congest. The reshard runs one wave64 per workgroup, so that each tile's address computation (map
-// entry, descriptor, pointers) is done once rather than once per wave.
+// resident per CU is bounded (EMU_OPT_WG_PER_CU), so that each CU keeps 48-64 KB of loads in flight:
+// enough to cover HBM latency, and few enough that the mixed read/write stream does not congest. Both
+// tile kernels run one wave64 per workgroup, so that each tile's address computation (map entry,
+// descriptor or rank record, pointers) is done once rather than once per wave.
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -251,13 +251,17 @@ __device__ __forceinline__ void wg_copy_bytes(const uint8_t* s, uint8_t* d, uint
 #define EMU_SHIFT_UNROLL 4
 #endif
 #ifndef EMU_BUCKET_TILE_VECS
-#define EMU_BUCKET_TILE_VECS 2
+#define EMU_BUCKET_TILE_VECS 4
+#endif
+#ifndef EMU_BUCKET_TILE_THREADS
+#define EMU_BUCKET_TILE_THREADS 64
 #endif
 constexpr int kXcds = int(kXcdCount);  // workgroups are dealt to the XCDs round-robin
 constexpr int kGeneralUnroll = 2;  // byte-granular reshard segments (misaligned runs; rare)
 constexpr int kBucketUnroll = EMU_BUCKET_UNROLL;
 constexpr int kShiftUnroll = EMU_SHIFT_UNROLL;
 constexpr int kBucketTileVecs = EMU_BUCKET_TILE_VECS;  // vectors per thread per pass of k_buckets_tile
+constexpr int kBucketTileThreads = EMU_BUCKET_TILE_THREADS;  // workgroup size of k_buckets_tile
 
 template <int U, bool LDS>
 __device__ __forceinline__ void stage_through_lds(v4u (&r)[U], v4u* stage) {
@@ -565,7 +569,7 @@ __global__ __launch_bounds__(kThreads, EMU_BUCKET_WAVES_PER_EU) void k_buckets(c
   }
 }
 
-// Tile-per-workgroup variant: one workgroup per 8 KB chunk (kTileChunkBytes) of one rank's stream, in
+// Tile-per-workgroup variant: one workgroup per 4 KB chunk (kTileChunkBytes) of one rank's stream, in
 // XCD-contiguous order. The upload-time map gives the chunk's rank and the global index of the tensor
 // holding its first byte, so the tensor's stream offset and pointer load in parallel with the rank's
 // record; the map is padded to the grid, so no bounds check precedes it. The rank's first bucket, the
@@ -577,7 +581,7 @@ struct BucketBases {
 };
 
 template <bool UNPACK, bool NT, int U>
-__global__ __launch_bounds__(kThreads, EMU_RESHARD_WAVES_PER_EU) void k_buckets_tile(
+__global__ __launch_bounds__(kBucketTileThreads, EMU_RESHARD_WAVES_PER_EU) void k_buckets_tile(
     const uint64_t* __restrict__ stream_off, const uint64_t* __restrict__ rank_info,
     const uint64_t* __restrict__ rank_bytes, const uint32_t* __restrict__ tile_map, uint64_t B, int32_t b_shift,
     const uint64_t* __restrict__ tensor_ptrs, const uint64_t* __restrict__ bucket_ptrs, BucketBases bases) {
@@ -615,8 +619,8 @@ __global__ __launch_bounds__(kThreads, EMU_RESHARD_WAVES_PER_EU) void k_buckets_
     uint8_t* tp = reinterpret_cast<uint8_t*>(tensor_ptrs[g]) + (pos - toff);
     uint8_t* bp = reinterpret_cast<uint8_t*>(bucket_ptrs[bucket0 + k]) + (pos - k * B);
     const uint32_t n = uint32_t(pend - pos);
-    if constexpr (UNPACK) wg_copy_bytes<kThreads, U, kShiftUnroll, NT, false>(bp, tp, n);
-    else wg_copy_bytes<kThreads, U, kShiftUnroll, NT, false>(tp, bp, n);
+    if constexpr (UNPACK) wg_copy_bytes<kBucketTileThreads, U, kShiftUnroll, NT, false>(bp, tp, n);
+    else wg_copy_bytes<kBucketTileThreads, U, kShiftUnroll, NT, false>(tp, bp, n);
     pos = pend;
     if (pos == kend) {
       ++k;
@@ -655,14 +659,16 @@ static int device_cus() {
 // divided by c, rounded down to whole KB; the kernels never touch the reserved bytes. The CU's LDS is
 // allocated in two halves and a workgroup's block lies in one half, so the resident count is
 // 2 * floor(c / 2) for c >= 2 (c = 1 keeps one). The cap bounds the bytes in flight per CU: on MI355X
-// a copy stream runs fastest with about 24-48 KB in flight per CU and drops by about 8% at 128 KB,
-// where the HBM read/write mix degrades. Automatic (-1): kAutoFlightBytes / tile_bytes workgroups
-// (12 for the reshard's 4 KB tiles, 6 for 8 KB), at least 2, and no cap from 32 up.
-constexpr uint64_t kAutoFlightBytes = 48 * 1024;
-static size_t occupancy_lds(size_t need, uint64_t tile_bytes) {
+// a copy stream runs fastest with about 24-64 KB in flight per CU and drops by about 8% at 128 KB,
+// where the HBM read/write mix degrades. Automatic (-1): flight / tile_bytes workgroups, at least 2,
+// and no cap from 32 up. The reshard runs best with 48 KB in flight (12 of its 4 KB tiles); the
+// pack/unpack kernel, whose per-chunk setup is longer, with 64 KB (16 of its 4 KB chunks).
+constexpr uint64_t kReshardFlightBytes = 48 * 1024;
+constexpr uint64_t kBucketFlightBytes = 64 * 1024;
+static size_t occupancy_lds(size_t need, uint64_t tile_bytes, uint64_t flight) {
   int64_t cap = option(EMU_OPT_WG_PER_CU);
   if (cap < 0) {
-    cap = int64_t(kAutoFlightBytes / (tile_bytes ? tile_bytes : 1));
+    cap = int64_t(flight / (tile_bytes ? tile_bytes : 1));
     cap = cap < 2 ? 2 : cap >= 32 ? 0 : cap;
   }
   if (cap == 0) return need;
@@ -685,7 +691,8 @@ static int hip_check(const char* what) {
 template <int U, bool NT, bool LDS, bool XCD, int CVT, bool ZERO>
 static void launch_reshard(hipStream_t st, const DevSeg* segs, const uint32_t* tm, uint64_t first, uint64_t count,
                            const uint64_t* sp, const uint64_t* dp) {
-  const size_t lds = occupancy_lds(LDS ? size_t(kReshardThreads) * U * 16 : 0, uint64_t(kReshardThreads) * U * 16);
+  const size_t lds = occupancy_lds(LDS ? size_t(kReshardThreads) * U * 16 : 0, uint64_t(kReshardThreads) * U * 16,
+                                   kReshardFlightBytes);
   constexpr uint64_t kMaxGrid = 0x7ffffff8ull;  // a multiple of kXcds below the grid-size limit
   for (uint64_t done = 0; done < count; done += kMaxGrid) {
     const uint32_t n = uint32_t(count - done < kMaxGrid ? count - done : kMaxGrid);
@@ -784,14 +791,13 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
     }
     const int32_t b_shift = (B & (B - 1)) == 0 ? __builtin_ctzll(B) : -1;
     const dim3 g(uint32_t(t.n_tiles));  // padded to a multiple of kXcds
-    // the bucket kernel's 8 KB chunks run best uncapped, so its automatic setting is no cap
-    const size_t lds = option(EMU_OPT_WG_PER_CU) < 0 ? 0 : occupancy_lds(0, kTileChunkBytes);
+    const size_t lds = occupancy_lds(0, kTileChunkBytes, kBucketFlightBytes);
     if (unpack) {
-      if (ntm) hipLaunchKernelGGL((k_buckets_tile<true, true, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
-      else hipLaunchKernelGGL((k_buckets_tile<true, false, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
+      if (ntm) hipLaunchKernelGGL((k_buckets_tile<true, true, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
+      else hipLaunchKernelGGL((k_buckets_tile<true, false, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
     } else {
-      if (ntm) hipLaunchKernelGGL((k_buckets_tile<false, true, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
-      else hipLaunchKernelGGL((k_buckets_tile<false, false, kBucketTileVecs>), g, dim3(kThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
+      if (ntm) hipLaunchKernelGGL((k_buckets_tile<false, true, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
+      else hipLaunchKernelGGL((k_buckets_tile<false, false, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
     }
     return hip_check(unpack ? "emu_unpack_buckets launch" : "emu_pack_buckets launch");
   }

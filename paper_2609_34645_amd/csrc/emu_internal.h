@@ -11,7 +11,7 @@
 namespace emu {
 
 constexpr uint32_t kPlanMagic = 0x454d5550u;  // "EMUP"
-constexpr int kThreads = 256;                 // workgroup size of the pack/unpack kernels (4 wave64s)
+constexpr int kThreads = 256;                 // workgroup size of the persistent pack/unpack kernel (4 wave64s)
 constexpr int kReshardThreads = 64;           // workgroup size of the reshard kernel (one wave64)
 constexpr int kMaxRankTensors = 2048;         // per-rank tensor offsets live in LDS during pack/unpack
 #ifndef EMU_CHUNK_BYTES
@@ -19,7 +19,7 @@ constexpr int kMaxRankTensors = 2048;         // per-rank tensor offsets live in
 #endif
 constexpr uint64_t kChunkBytes = EMU_CHUNK_BYTES;  // pack/unpack work unit, in stream bytes
 #ifndef EMU_TILE_CHUNK_BYTES
-#define EMU_TILE_CHUNK_BYTES 8192
+#define EMU_TILE_CHUNK_BYTES 4096
 #endif
 constexpr uint64_t kTileChunkBytes = EMU_TILE_CHUNK_BYTES;  // unit of the tile-per-workgroup pack/unpack kernel
 constexpr uint32_t kMapTensorBits = 20;            // chunk map entry: rank << 20 | global tensor index
