@@ -426,7 +426,6 @@ static int finalize(Plan& P) {
   const uint64_t TB = TV * 16;                 // bytes per tile
   P.tile_bytes = TB;
   P.dsegs.clear();
-  std::vector<uint32_t> tilemap;
   std::vector<uint64_t> segtiles;  // tiles of each segment
   uint64_t tiles = 0, zero_bytes = 0, written = 0, read = 0;
   int64_t nzero = 0;
@@ -486,55 +485,42 @@ static int finalize(Plan& P) {
   // Tile map: the copy segments' tiles, then the zero-fill segments' tiles, which run on their own
   // kernel instance. Each section is padded with kNoSeg to a whole number of XCD groups, so that every
   // workgroup of a grid (a multiple of kXcdCount) reads an entry of its own section and the kernel
-  // needs no bounds check before its first load.
+  // needs no bounds check before its first load. Here each segment gets its first map index; the map
+  // is written straight into the workspace image below.
+  uint64_t nmap = 0;
   for (int pass = 0; pass < 2; ++pass) {
-    if (pass == 1) P.zero_tile0 = tilemap.size();
+    if (pass == 1) P.zero_tile0 = nmap;
     for (size_t i = 0; i < P.dsegs.size(); ++i) {
       if (((P.dsegs[i].mode & SEG_ZERO) != 0) != (pass == 1)) continue;
-      P.dsegs[i].tile0 = tilemap.size();
-      tilemap.insert(tilemap.end(), segtiles[i], uint32_t(i));
+      P.dsegs[i].tile0 = nmap;
+      nmap += segtiles[i];
     }
-    if (pass == 0) P.ntiles_copy = tilemap.size();
-    else P.ntiles_zero = tilemap.size() - P.zero_tile0;
-    while (tilemap.size() % kXcdCount) tilemap.push_back(kNoSeg);
+    if (pass == 0) P.ntiles_copy = nmap;
+    else P.ntiles_zero = nmap - P.zero_tile0;
+    nmap = (nmap + kXcdCount - 1) / kXcdCount * kXcdCount;
   }
   if (written != P.side[1].total_bytes)
     return fail(EMU_ERR_ARG, "internal: copy map covers %llu of %llu destination bytes",
                 (unsigned long long)written, (unsigned long long)P.side[1].total_bytes);
+
+  // Per side, for the tile-per-workgroup pack/unpack kernel: a chunk -> (rank, global tensor) map,
+  // padded with kNoSeg to a multiple of kXcdCount (the kernel's grid), and per rank {first chunk,
+  // stream bytes, end of its tensor range}. A side the map cannot encode gets an empty map.
+  uint64_t nchunk[2] = {0, 0};
+  for (int sd = 0; sd < 2; ++sd) {
+    const SideInfo& s = P.side[sd];
+    const bool encodable = s.nranks < (1 << (32 - kMapTensorBits)) && s.tensors.size() <= (1u << kMapTensorBits);
+    uint64_t n = 0;
+    for (int r = 0; r < s.nranks; ++r) n += (s.rank_bytes[r] + kTileChunkBytes - 1) / kTileChunkBytes;
+    nchunk[sd] = encodable && n <= 0x7fffff00ull ? (n + kXcdCount - 1) / kXcdCount * kXcdCount : 0;
+  }
 
   // workspace image
   auto align = [](uint64_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; };
   WsLayout& w = P.ws;
   uint64_t off = 0;
   w.off_segs = off; off = align(off + P.dsegs.size() * sizeof(DevSeg));
-  w.off_tilemap = off; off = align(off + tilemap.size() * 4);
-  // per side: chunk -> (rank, global tensor) map for the tile-per-workgroup pack/unpack kernel, padded
-  // with kNoSeg to a multiple of kXcdCount (the kernel's grid), and per rank {first chunk, stream
-  // bytes, end of its tensor range}
-  std::vector<uint32_t> tmap[2];
-  std::vector<uint64_t> rinfo[2];
-  for (int sd = 0; sd < 2; ++sd) {
-    const SideInfo& s = P.side[sd];
-    rinfo[sd].assign(size_t(s.nranks) * 4, 0);
-    const bool encodable = s.nranks < (1 << (32 - kMapTensorBits)) && s.tensors.size() <= (1u << kMapTensorBits);
-    uint64_t first = 0;
-    for (int r = 0; r < s.nranks && encodable; ++r) {
-      const uint32_t t0 = s.rank_first[r], t1 = s.rank_first[r + 1];
-      const uint64_t nch = (s.rank_bytes[r] + kTileChunkBytes - 1) / kTileChunkBytes;
-      rinfo[sd][4 * r + 0] = first;
-      rinfo[sd][4 * r + 1] = s.rank_bytes[r];
-      rinfo[sd][4 * r + 2] = t1;
-      first += nch;
-      uint32_t g = t0;
-      for (uint64_t j = 0; j < nch; ++j) {
-        const uint64_t pos = j * kTileChunkBytes;
-        while (g + 1 < t1 && s.tensors[g + 1].stream_offset <= pos) ++g;
-        tmap[sd].push_back((uint32_t(r) << kMapTensorBits) | g);
-      }
-    }
-    if (!encodable || tmap[sd].size() > 0x7fffff00ull) tmap[sd].clear();
-    while (tmap[sd].size() % kXcdCount) tmap[sd].push_back(kNoSeg);
-  }
+  w.off_tilemap = off; off = align(off + nmap * 4);
   for (int sd = 0; sd < 2; ++sd) {
     const SideInfo& s = P.side[sd];
     w.side[sd].off_sizes = off; off = align(off + s.tensors.size() * 8);
@@ -542,15 +528,17 @@ static int finalize(Plan& P) {
     w.side[sd].off_rank_bytes = off; off = align(off + s.nranks * 8);
     w.side[sd].off_chunk_first = off; off = align(off + (s.nranks + 1) * 8);
     w.side[sd].off_stream = off; off = align(off + s.tensors.size() * 8);
-    w.side[sd].off_rank_info = off; off = align(off + rinfo[sd].size() * 8);
-    w.side[sd].off_tile_map = off; off = align(off + tmap[sd].size() * 4);
-    w.side[sd].n_tiles = tmap[sd].size();
+    w.side[sd].off_rank_info = off; off = align(off + size_t(s.nranks) * 4 * 8);
+    w.side[sd].off_tile_map = off; off = align(off + nchunk[sd] * 4);
+    w.side[sd].n_tiles = nchunk[sd];
   }
   w.total = off;
   P.host_ws.assign(w.total, 0);
   uint8_t* h = P.host_ws.data();
   if (!P.dsegs.empty()) std::memcpy(h + w.off_segs, P.dsegs.data(), P.dsegs.size() * sizeof(DevSeg));
-  if (!tilemap.empty()) std::memcpy(h + w.off_tilemap, tilemap.data(), tilemap.size() * 4);
+  uint32_t* tm = reinterpret_cast<uint32_t*>(h + w.off_tilemap);
+  std::fill_n(tm, nmap, kNoSeg);
+  for (size_t i = 0; i < P.dsegs.size(); ++i) std::fill_n(tm + P.dsegs[i].tile0, segtiles[i], uint32_t(i));
   for (int sd = 0; sd < 2; ++sd) {
     const SideInfo& s = P.side[sd];
     uint64_t* sz = reinterpret_cast<uint64_t*>(h + w.side[sd].off_sizes);
@@ -560,8 +548,25 @@ static int finalize(Plan& P) {
     std::memcpy(h + w.side[sd].off_chunk_first, s.chunk_first.data(), s.chunk_first.size() * 8);
     uint64_t* so = reinterpret_cast<uint64_t*>(h + w.side[sd].off_stream);
     for (size_t i = 0; i < s.tensors.size(); ++i) so[i] = s.tensors[i].stream_offset;
-    if (!rinfo[sd].empty()) std::memcpy(h + w.side[sd].off_rank_info, rinfo[sd].data(), rinfo[sd].size() * 8);
-    if (!tmap[sd].empty()) std::memcpy(h + w.side[sd].off_tile_map, tmap[sd].data(), tmap[sd].size() * 4);
+    if (nchunk[sd] == 0) continue;
+    uint64_t* ri = reinterpret_cast<uint64_t*>(h + w.side[sd].off_rank_info);
+    uint32_t* cm = reinterpret_cast<uint32_t*>(h + w.side[sd].off_tile_map);
+    uint64_t first = 0;
+    for (int r = 0; r < s.nranks; ++r) {
+      const uint32_t t0 = s.rank_first[r], t1 = s.rank_first[r + 1];
+      const uint64_t nch = (s.rank_bytes[r] + kTileChunkBytes - 1) / kTileChunkBytes;
+      ri[4 * r + 0] = first;
+      ri[4 * r + 1] = s.rank_bytes[r];
+      ri[4 * r + 2] = t1;
+      uint32_t g = t0;
+      for (uint64_t j = 0; j < nch; ++j) {
+        const uint64_t pos = j * kTileChunkBytes;
+        while (g + 1 < t1 && s.tensors[g + 1].stream_offset <= pos) ++g;
+        cm[first + j] = (uint32_t(r) << kMapTensorBits) | g;
+      }
+      first += nch;
+    }
+    std::fill(cm + first, cm + nchunk[sd], kNoSeg);
   }
 
   emu_plan_info_t& I = P.info;
