@@ -165,9 +165,10 @@ typedef enum {
                                 per compute unit, 1..32, enforced by reserving LDS per workgroup (the
                                 LDS is split in two halves, so odd caps above 1 round down to even);
                                 0 = no cap; -1 = automatic (default): 48 KB of reshard tiles (12 of
-                                4 KB, 6 of 8 KB) and 64 KB of pack/unpack chunks (16 of 4 KB); at
-                                least 2, no cap from 32 up. Bounds the bytes in flight per CU, which
-                                sets how well HBM serves a read/write stream */
+                                4 KB, 6 of 8 KB), 40 KB for fp32 -> bf16 plans, 64 KB for bf16 ->
+                                fp32 plans, and 64 KB of pack/unpack chunks (16 of 4 KB); at least 2,
+                                no cap from 32 up. Bounds the bytes in flight per CU, which sets how
+                                well HBM serves a read/write stream */
 } emu_option;
 
 /* Library version (EMU_ABI_VERSION). */

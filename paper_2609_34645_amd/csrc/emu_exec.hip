@@ -661,9 +661,12 @@ static int device_cus() {
 // 2 * floor(c / 2) for c >= 2 (c = 1 keeps one). The cap bounds the bytes in flight per CU: on MI355X
 // a copy stream runs fastest with about 24-64 KB in flight per CU and drops by about 8% at 128 KB,
 // where the HBM read/write mix degrades. Automatic (-1): flight / tile_bytes workgroups, at least 2,
-// and no cap from 32 up. The reshard runs best with 48 KB in flight (12 of its 4 KB tiles); the
-// pack/unpack kernel, whose per-chunk setup is longer, with 64 KB (16 of its 4 KB chunks).
-constexpr uint64_t kReshardFlightBytes = 48 * 1024;
+// and no cap from 32 up, with `flight` in destination bytes. Measured optima at 4 KB tiles: a copying
+// reshard 12 tiles (48 KB), fp32 -> bf16 10 (40 KB; each tile reads twice what it writes), bf16 ->
+// fp32 16 (64 KB; each reads half), all about 100-120 KB of reads and writes together; the
+// pack/unpack kernel, whose per-chunk setup is longer, 16 of its 4 KB chunks (64 KB).
+template <int CVT>
+constexpr uint64_t kReshardFlightBytes = CVT == CVT_F32_BF16 ? 40 * 1024 : CVT == CVT_BF16_F32 ? 64 * 1024 : 48 * 1024;
 constexpr uint64_t kBucketFlightBytes = 64 * 1024;
 static size_t occupancy_lds(size_t need, uint64_t tile_bytes, uint64_t flight) {
   int64_t cap = option(EMU_OPT_WG_PER_CU);
@@ -692,7 +695,7 @@ template <int U, bool NT, bool LDS, bool XCD, int CVT, bool ZERO>
 static void launch_reshard(hipStream_t st, const DevSeg* segs, const uint32_t* tm, uint64_t first, uint64_t count,
                            const uint64_t* sp, const uint64_t* dp) {
   const size_t lds = occupancy_lds(LDS ? size_t(kReshardThreads) * U * 16 : 0, uint64_t(kReshardThreads) * U * 16,
-                                   kReshardFlightBytes);
+                                   kReshardFlightBytes<CVT>);
   constexpr uint64_t kMaxGrid = 0x7ffffff8ull;  // a multiple of kXcds below the grid-size limit
   for (uint64_t done = 0; done < count; done += kMaxGrid) {
     const uint32_t n = uint32_t(count - done < kMaxGrid ? count - done : kMaxGrid);
