@@ -279,6 +279,21 @@ def test_buckets_of_one_element(gpu_lib, tiles):
         emu.set_option(emu.OPT_BUCKET_TILES, old)
 
 
+@pytest.mark.parametrize("tiles", [1, 0], ids=["tile_per_wg", "persistent"])
+def test_buckets_beyond_128_ranks(gpu_lib, tiles):
+    """256 destination ranks (TP16 PP16): ranks past the first 128 find their first bucket with the
+    on-device wave64 reduction instead of the host's kernel argument, and odd bucket sizes give the
+    ranks different bucket counts; the fused plan must produce the same buckets."""
+    m = emu.Model(16, 32, 16, 2, 16, 32, 32)
+    old = emu.get_option(emu.OPT_BUCKET_TILES)
+    emu.set_option(emu.OPT_BUCKET_TILES, tiles)
+    try:
+        plan = run_pair(emu.Layout(m, 1, 1), emu.Layout(m, 16, 16), bucket_sizes=(6, 64, 1000), fused=True)
+        assert plan.info["n_dst_ranks"] == 256
+    finally:
+        emu.set_option(emu.OPT_BUCKET_TILES, old)
+
+
 def test_buckets_source_side_and_fp32(gpu_lib):
     import torch
 
