@@ -392,7 +392,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the reshard is the local step each rank runs, and this build "
+        print("bench.py measures one GPU only: the reshard is the local step each rank runs, and the library "
               "has no multi-GPU path. Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
