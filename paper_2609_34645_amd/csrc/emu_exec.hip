@@ -276,19 +276,13 @@ __device__ __forceinline__ void stage_through_lds(v4u (&r)[U], v4u* stage) {
   }
 }
 
-// SEG_VEC_ROWS: `param` whole rows of rv vectors per tile. Vector n of the tile is at row n / rv
-// (a multiply-high by the host-computed magic number) and column n % rv; the host keeps
-// param * stride below 2^31 so that offsets stay 32-bit.
+// Rows of rv vectors at strides ss and ds bytes from s and d, read in row-major vector order: the tile
+// holds vectors r0 .. r0 + last of that order. Vector n is in row n / rv (a multiply-high by the host's
+// magic number) at column n % rv; the host keeps every in-tile byte offset below 2^31.
 template <int U, bool NT, bool ZERO, bool LDS, int CVT>
-__device__ __forceinline__ void tile_rows(const DevSeg& g, uint64_t lt, const uint8_t* sb, uint8_t* db,
-                                          v4u* stage) {
+__device__ __forceinline__ void tile_rows(const uint8_t* s, uint8_t* d, uint32_t r0, uint32_t last, uint32_t rv,
+                                          uint32_t mg, uint32_t ss, uint32_t ds, v4u* stage) {
   const uint32_t tid = threadIdx.x;
-  const uint64_t row0 = lt * g.param;
-  const uint32_t nrows = uint32_t(g.rows - row0 < g.param ? g.rows - row0 : g.param);
-  const uint32_t last = nrows * g.rv - 1;
-  const uint32_t ss = uint32_t(g.src_stride), ds = uint32_t(g.dst_stride), rv = g.rv, mg = g.magic;
-  const uint8_t* s = ZERO ? nullptr : sb + g.src_off + row0 * g.src_stride;
-  uint8_t* d = db + g.dst_off + row0 * g.dst_stride;
   v4u r[U];
   if constexpr (ZERO) {
 #pragma unroll
@@ -297,7 +291,7 @@ __device__ __forceinline__ void tile_rows(const DevSeg& g, uint64_t lt, const ui
     Raw<CVT> raw[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const uint32_t n = umin(u * kReshardThreads + tid, last);
+      const uint32_t n = r0 + umin(u * kReshardThreads + tid, last);
       const uint32_t q = rv > 1 ? __umulhi(n, mg) : n;
       raw[u] = ld_raw<CVT, NT>(s, q * ss + (n - q * rv) * kSrcVecBytes<CVT>);
     }
@@ -307,9 +301,10 @@ __device__ __forceinline__ void tile_rows(const DevSeg& g, uint64_t lt, const ui
   stage_through_lds<U, LDS>(r, stage);
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    const uint32_t n = u * kReshardThreads + tid;
+    const uint32_t i = u * kReshardThreads + tid;
+    const uint32_t n = r0 + i;
     const uint32_t q = rv > 1 ? __umulhi(n, mg) : n;
-    if (n <= last) st16<NT>(d, q * ds + (n - q * rv) * 16u, r[u]);
+    if (i <= last) st16<NT>(d, q * ds + (n - q * rv) * 16u, r[u]);
   }
 }
 
@@ -360,30 +355,27 @@ __device__ __forceinline__ void tile_run_f32_bf16(const uint8_t* s, uint8_t* d, 
   }
 }
 
-// Short rows: half n of the tile is in row n / (2 rv), at half n % (2 rv) of that row; the row comes
-// from the host's magic number for rv applied to n / 2.
+// The same rows converted: destination vectors r0 .. r0 + last, moved as halves (four fp32 read, four
+// bf16 written). Half n of the tile belongs to destination vector r0 + n / 2, in row (r0 + n / 2) / rv;
+// its column in halves is 2 r0 + n less twice the row's first vector.
 template <int U, bool NT>
-__device__ __forceinline__ void tile_rows_f32_bf16(const DevSeg& g, uint64_t lt, const uint8_t* sb, uint8_t* db) {
+__device__ __forceinline__ void tile_rows_f32_bf16(const uint8_t* s, uint8_t* d, uint32_t r0, uint32_t last,
+                                                   uint32_t rv, uint32_t mg, uint32_t ss, uint32_t ds) {
   const uint32_t tid = threadIdx.x;
-  const uint64_t row0 = lt * g.param;
-  const uint32_t nrows = uint32_t(g.rows - row0 < g.param ? g.rows - row0 : g.param);
-  const uint32_t rv = g.rv, h = 2 * rv, mg = g.magic;
-  const uint32_t last = nrows * h - 1;
-  const uint32_t ss = uint32_t(g.src_stride), ds = uint32_t(g.dst_stride);
-  const uint8_t* s = sb + g.src_off + row0 * g.src_stride;
-  uint8_t* d = db + g.dst_off + row0 * g.dst_stride;
+  const uint32_t lasth = 2 * last + 1, h = 2 * rv;
   v4u a[2 * U];
 #pragma unroll
   for (int k = 0; k < 2 * U; ++k) {
-    const uint32_t n = umin(k * kReshardThreads + tid, last);
+    const uint32_t n = 2 * r0 + umin(k * kReshardThreads + tid, lasth);
     const uint32_t q = rv > 1 ? __umulhi(n >> 1, mg) : (n >> 1);
     a[k] = ld16<NT>(s, q * ss + (n - q * h) * 16u);
   }
 #pragma unroll
   for (int k = 0; k < 2 * U; ++k) {
-    const uint32_t n = k * kReshardThreads + tid;
+    const uint32_t i = k * kReshardThreads + tid;
+    const uint32_t n = 2 * r0 + i;
     const uint32_t q = rv > 1 ? __umulhi(n >> 1, mg) : (n >> 1);
-    if (n <= last) st8<NT>(d, q * ds + (n - q * h) * 8u, to_bf16x4(a[k]));
+    if (i <= lasth) st8<NT>(d, q * ds + (n - q * h) * 8u, to_bf16x4(a[k]));
   }
 }
 
@@ -398,9 +390,27 @@ __device__ __forceinline__ void run_tile(const DevSeg& g, uint64_t lt, const uin
     const uint32_t cnt = uint32_t(nv - v0 < TV ? nv - v0 : TV);
     if constexpr (kHalves) tile_run_f32_bf16<U, NT>(sb + g.src_off + v0 * SV, db + g.dst_off + v0 * 16, cnt);
     else tile_run<U, NT, ZERO, LDS, CVT>(ZERO ? nullptr : sb + g.src_off + v0 * SV, db + g.dst_off + v0 * 16, cnt, stage);
-  } else if (mode == SEG_VEC_ROWS) {
-    if constexpr (kHalves) tile_rows_f32_bf16<U, NT>(g, lt, sb, db);
-    else tile_rows<U, NT, ZERO, LDS, CVT>(g, lt, sb, db, stage);
+  } else if (mode == SEG_VEC_FLAT || mode == SEG_VEC_ROWS) {
+    // FLAT: vectors [lt * TV, lt * TV + TV) of the rows' row-major order, starting in row row0 at
+    // column r0. ROWS: `param` whole rows per tile.
+    uint64_t row0;
+    uint32_t r0, last;
+    if (mode == SEG_VEC_FLAT) {
+      const uint32_t n0 = uint32_t(lt) * uint32_t(TV);  // below param = rows * rv < 2^32
+      const uint32_t q0 = g.rv > 1 ? __umulhi(n0, g.magic) : n0;
+      row0 = q0;
+      r0 = n0 - q0 * g.rv;
+      last = umin(g.param - n0, uint32_t(TV)) - 1;
+    } else {
+      row0 = lt * g.param;
+      r0 = 0;
+      last = uint32_t(g.rows - row0 < g.param ? g.rows - row0 : g.param) * g.rv - 1;
+    }
+    const uint8_t* s = ZERO ? nullptr : sb + g.src_off + row0 * g.src_stride;
+    uint8_t* d = db + g.dst_off + row0 * g.dst_stride;
+    const uint32_t ss = uint32_t(g.src_stride), ds = uint32_t(g.dst_stride);
+    if constexpr (kHalves) tile_rows_f32_bf16<U, NT>(s, d, r0, last, g.rv, g.magic, ss, ds);
+    else tile_rows<U, NT, ZERO, LDS, CVT>(s, d, r0, last, g.rv, g.magic, ss, ds, stage);
   } else if (mode == SEG_VEC_ROWCHUNK) {
     const uint64_t row = lt / g.param, ch = lt - row * g.param;
     const uint64_t nv = g.run / 16, v0 = ch * TV;

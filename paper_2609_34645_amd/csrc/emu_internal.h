@@ -34,6 +34,8 @@ enum SegMode : uint32_t {
   SEG_VEC_ROWS = 1,      // rows shorter than a tile; a tile is `param` whole rows
   SEG_VEC_ROWCHUNK = 2,  // rows longer than a tile; a tile is one slice of one row
   SEG_GENERAL = 3,       // any byte alignment; a tile is one slice of one row, copied bytewise
+  SEG_VEC_FLAT = 4,      // rows of any length; a tile is a fixed slice of the rows' vectors in row-major
+                         // order, so rows wrap inside a tile and only a segment's last tile is partial
 };
 constexpr uint32_t SEG_MODE_MASK = 0xff;
 constexpr uint32_t SEG_ZERO = 0x100;  // no source: write zeros
@@ -48,9 +50,11 @@ struct alignas(16) DevSeg {
   uint64_t rows, run;
   int32_t src_idx, dst_idx;
   uint32_t mode;   // SegMode | SEG_ZERO
-  uint32_t param;  // SEG_VEC_ROWS: rows per tile; SEG_VEC_ROWCHUNK / SEG_GENERAL: tiles per row
-  uint32_t rv;     // SEG_VEC_ROWS: 16-byte vectors per row
-  uint32_t magic;  // SEG_VEC_ROWS: ceil(2^32 / rv) for rv > 1 (n / rv == umulhi(n, magic) for n*rv < 2^32)
+  uint32_t param;  // SEG_VEC_ROWS: rows per tile; SEG_VEC_ROWCHUNK / SEG_GENERAL: tiles per row;
+                   // SEG_VEC_FLAT: rows * rv, the segment's vectors
+  uint32_t rv;     // SEG_VEC_ROWS / SEG_VEC_FLAT: 16-byte vectors per row
+  uint32_t magic;  // SEG_VEC_ROWS / SEG_VEC_FLAT: ceil(2^32 / rv) for rv > 1 (n / rv == umulhi(n, magic)
+                   // for n * rv < 2^32)
   uint64_t tile0;  // map index of the segment's first tile
 };
 static_assert(sizeof(DevSeg) == 80, "DevSeg layout");

@@ -420,6 +420,17 @@ static int to_buckets(Plan& P, uint64_t B) {
 }
 
 // Device segments, tiles and the workspace image.
+// Whether a 2D vector segment can run as SEG_VEC_FLAT with tiles of TV vectors: the kernel finds the
+// row of vector n (n below rows * rv) as umulhi(n, ceil(2^32 / rv)), exact while n * rv < 2^32, and
+// keeps in-tile byte offsets in 31 bits: a tile spans at most 2 + TV / rv rows.
+static bool flat_ok(const emu_segment_t& g, uint64_t TV) {
+  const uint64_t rv = g.run / 16;
+  if (g.rows < 2 || rv == 0 || g.rows > 0xffffffffull) return false;
+  if (rv > 0xffffffffull / rv || g.rows > 0xffffffffull / (rv * rv)) return false;  // rows * rv * rv < 2^32
+  const uint64_t stride = std::max(g.src_stride, g.dst_stride);
+  return stride < (1ull << 31) / (2 + TV / rv);
+}
+
 static int finalize(Plan& P) {
   const int U = P.tile_vecs;
   const uint64_t TV = uint64_t(kReshardThreads) * U;  // vectors per tile
@@ -454,6 +465,12 @@ static int finalize(Plan& P) {
     } else if (g.rows == 1) {
       d.mode = SEG_VEC_1D;
       nt = (g.run + TB - 1) / TB;
+    } else if (flat_ok(g, TV)) {
+      d.mode = SEG_VEC_FLAT;
+      d.rv = uint32_t(g.run / 16);
+      d.param = uint32_t(g.rows * d.rv);
+      d.magic = d.rv > 1 ? uint32_t(((1ull << 32) + d.rv - 1) / d.rv) : 0u;
+      nt = (d.param + TV - 1) / TV;
     } else if (g.run <= TB) {
       d.mode = SEG_VEC_ROWS;
       d.rv = uint32_t(g.run / 16);
