@@ -161,7 +161,7 @@ typedef enum {
                                 chunk map; default); 0 = the persistent kernel that scans each rank's
                                 tensor sizes into LDS (also used when the chunk map cannot encode a side:
                                 4096 or more ranks, or more than 2^20 tensors on the side) */
-  EMU_OPT_WG_PER_CU = 6      /* reshard and tile pack/unpack kernels: cap on the workgroups resident
+  EMU_OPT_WG_PER_CU = 6,     /* reshard and tile pack/unpack kernels: cap on the workgroups resident
                                 per compute unit, 1..32, enforced by reserving LDS per workgroup (the
                                 LDS is split in two halves, so odd caps above 1 round down to even);
                                 0 = no cap; -1 = automatic (default): 48 KB of reshard tiles (12 of
@@ -169,6 +169,9 @@ typedef enum {
                                 fp32 plans, and 64 KB of pack/unpack chunks (16 of 4 KB); at least 2,
                                 no cap from 32 up. Bounds the bytes in flight per CU, which sets how
                                 well HBM serves a read/write stream */
+  EMU_OPT_ROW_WRAP = 7       /* 1 = tile 2D segments as one row-major vector sequence, rows wrapping
+                                inside a tile, wherever the kernel's row arithmetic is exact (default);
+                                0 = whole rows per tile, or slices of one row. Read by emu_plan */
 } emu_option;
 
 /* Library version (EMU_ABI_VERSION). */

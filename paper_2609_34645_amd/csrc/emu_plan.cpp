@@ -67,7 +67,7 @@ void ws_forget(const Plan* p) {
   for (auto it = g_ws.begin(); it != g_ws.end();) it = it->second == p ? g_ws.erase(it) : std::next(it);
 }
 
-static std::atomic<int64_t> g_opt[7] = {{0}, {1}, {1}, {0}, {32}, {1}, {-1}};
+static std::atomic<int64_t> g_opt[8] = {{0}, {1}, {1}, {0}, {32}, {1}, {-1}, {1}};
 
 int64_t option(int32_t key) { return g_opt[key].load(std::memory_order_relaxed); }
 
@@ -444,6 +444,7 @@ static int finalize(Plan& P) {
   // whole source vectors, 8 bytes when it reads half of one (bf16 -> fp32)
   const uint64_t salign = P.cvt == CVT_BF16_F32 ? 8 : 16;
   int32_t ngeneral = 0;
+  const bool row_wrap = option(EMU_OPT_ROW_WRAP) != 0;
   for (size_t i = 0; i < P.segs.size(); ++i) {
     const emu_segment_t& g = P.segs[i];
     DevSeg d{};
@@ -465,7 +466,7 @@ static int finalize(Plan& P) {
     } else if (g.rows == 1) {
       d.mode = SEG_VEC_1D;
       nt = (g.run + TB - 1) / TB;
-    } else if (flat_ok(g, TV)) {
+    } else if (row_wrap && flat_ok(g, TV)) {
       d.mode = SEG_VEC_FLAT;
       d.rv = uint32_t(g.run / 16);
       d.param = uint32_t(g.rows * d.rv);
@@ -712,6 +713,7 @@ int emu_set_option(int32_t key, int64_t value) {
       break;
     case EMU_OPT_XCD_REMAP:
     case EMU_OPT_BUCKET_TILES:
+    case EMU_OPT_ROW_WRAP:
     case EMU_OPT_NONTEMPORAL:
     case EMU_OPT_LDS_STAGING:
       if (value != 0 && value != 1) return fail(EMU_ERR_ARG, "flag must be 0 or 1");
@@ -726,7 +728,7 @@ int emu_set_option(int32_t key, int64_t value) {
 int emu_get_option(int32_t key, int64_t* value) {
   clear_error();
   if (!value) return fail(EMU_ERR_NULL, "value is NULL");
-  if (key < 0 || key > EMU_OPT_WG_PER_CU) return fail(EMU_ERR_RANGE, "unknown option %d", key);
+  if (key < 0 || key > EMU_OPT_ROW_WRAP) return fail(EMU_ERR_RANGE, "unknown option %d", key);
   *value = option(key);
   return EMU_OK;
 }

@@ -29,7 +29,7 @@ DTYPES = {"bf16": BF16, "fp32": FP32}
 ESIZE = {BF16: 2, FP32: 4}
 
 (OPT_TILE_VECS, OPT_XCD_REMAP, OPT_NONTEMPORAL, OPT_LDS_STAGING, OPT_BUCKET_WG_PER_CU, OPT_BUCKET_TILES,
- OPT_WG_PER_CU) = range(7)
+ OPT_WG_PER_CU, OPT_ROW_WRAP) = range(8)
 
 KINDS = ["embed", "attn_norm", "qkv", "q", "k", "v", "o", "mlp_norm", "gate_up", "gate", "up", "down",
          "final_norm", "lm_head", "bucket"]

@@ -89,15 +89,25 @@ def random_valid_layout(rng, model, dtype):
             return lay
 
 
-def test_random_layout_pairs(gpu_lib):
+@pytest.mark.parametrize("row_wrap", [1, 0], ids=["row_wrap", "whole_rows"])
+def test_random_layout_pairs(gpu_lib, row_wrap):
     """400 random valid layout pairs on random small models, each with a random bucket size: reshard,
     pack and unpack bit-exact against the oracle, and the fused source -> bucket plan giving the same
     buckets. Of the 400: 206 have byte-granular segments (odd widths
     put runs at every 16-byte phase), 203 convert between fp32 and bf16, 133 zero-fill pad rows, 177
-    replicate KV heads and 141 have uneven pipeline stages."""
+    replicate KV heads and 141 have uneven pipeline stages. Run once with row-wrapping tiles for 2D
+    segments (the default) and once with whole-row tiles and row slices."""
     import random
 
-    rng = random.Random(41)
+    old = emu.get_option(emu.OPT_ROW_WRAP)
+    emu.set_option(emu.OPT_ROW_WRAP, row_wrap)
+    try:
+        _random_pairs(random.Random(41))
+    finally:
+        emu.set_option(emu.OPT_ROW_WRAP, old)
+
+
+def _random_pairs(rng):
     n = 0
     while n < 400:
         nH = rng.choice([2, 4, 8])
@@ -209,9 +219,10 @@ def test_tiny_transition_in_a_hip_graph(gpu_lib):
     {emu.OPT_WG_PER_CU: 1, emu.OPT_LDS_STAGING: 1}, {emu.OPT_WG_PER_CU: 8, emu.OPT_BUCKET_TILES: 0},
     {emu.OPT_WG_PER_CU: 12}, {emu.OPT_WG_PER_CU: 24, emu.OPT_TILE_VECS: 2},
     {emu.OPT_WG_PER_CU: 32, emu.OPT_TILE_VECS: 1}, {emu.OPT_TILE_VECS: 4, emu.OPT_LDS_STAGING: 1},
+    {emu.OPT_ROW_WRAP: 0}, {emu.OPT_ROW_WRAP: 0, emu.OPT_TILE_VECS: 1}, {emu.OPT_ROW_WRAP: 0, emu.OPT_TILE_VECS: 16},
 ])
 def test_launch_options(gpu_lib, opts):
-    defaults = {k: emu.get_option(k) for k in range(7)}
+    defaults = {k: emu.get_option(k) for k in range(8)}
     try:
         m = emu.Model(*TINY)
         run_pair(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate"), options=opts)

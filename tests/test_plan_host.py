@@ -216,7 +216,7 @@ def test_error_codes():
     assert lib.emu_set_option(0, 5) == -11
     assert lib.emu_set_option(99, 1) == -10
     assert lib.emu_set_option(emu.OPT_WG_PER_CU, 33) == -11 and lib.emu_set_option(emu.OPT_WG_PER_CU, -2) == -11
-    assert lib.emu_set_option(7, 0) == -10
+    assert lib.emu_set_option(8, 0) == -10 and lib.emu_set_option(emu.OPT_ROW_WRAP, 2) == -11
     for s in range(-11, 1):
         assert lib.emu_status_str(s).startswith(b"EMU_")
 
