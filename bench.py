@@ -389,6 +389,7 @@ def main():
     ap.add_argument("--lds", type=int, default=None)
     ap.add_argument("--bucket-wg-per-cu", type=int, default=None)
     ap.add_argument("--wg-per-cu", type=int, default=None)
+    ap.add_argument("--row-wrap", type=int, default=None)
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -404,7 +405,8 @@ def main():
     emu.load()
     for opt, v in ((emu.OPT_TILE_VECS, args.tile_vecs), (emu.OPT_XCD_REMAP, args.xcd_remap),
                    (emu.OPT_NONTEMPORAL, args.nontemporal), (emu.OPT_LDS_STAGING, args.lds),
-                   (emu.OPT_BUCKET_WG_PER_CU, args.bucket_wg_per_cu), (emu.OPT_WG_PER_CU, args.wg_per_cu)):
+                   (emu.OPT_BUCKET_WG_PER_CU, args.bucket_wg_per_cu), (emu.OPT_WG_PER_CU, args.wg_per_cu),
+                   (emu.OPT_ROW_WRAP, args.row_wrap)):
         if v is not None:
             emu.set_option(opt, v)
 
@@ -582,6 +584,7 @@ def main():
                                                       ("lds_staging", emu.OPT_LDS_STAGING),
                                                       ("bucket_wg_per_cu", emu.OPT_BUCKET_WG_PER_CU),
                                                       ("bucket_tiles", emu.OPT_BUCKET_TILES),
+                                                      ("row_wrap", emu.OPT_ROW_WRAP),
                                                       ("wg_per_cu", emu.OPT_WG_PER_CU))},
         "device": {"name": props.name, "cus": props.multi_processor_count,
                    "hbm_GB": round(props.total_memory / 1e9, 1)},
