@@ -62,33 +62,36 @@ def ids_of(lay):
     return _IDS[lay]
 
 
-REPLICA = np.uint32(0x8000_0000)
-SENTINEL = np.uint32(0xFFFF_FFFF)
+# tag type, replica mark and pad sentinel per element type (bf16 tags need fewer than 2^15 elements)
+TAGS = {"fp32": (np.uint32, 0x8000_0000, 0xFFFF_FFFF), "bf16": (np.uint16, 0x8000, 0xFFFF)}
 
 
 def tagged_source(lay):
     """Source shards whose elements carry (logical id + 1); pad rows hold a sentinel that must never be
     read; every replica of a logical element held by an earlier rank (norms on TP ranks > 0, replicated
     KV heads past their first rank) carries a marked tag that must never be copied."""
+    dt, replica, sentinel = TAGS[lay.dtype]
     out = []
     seen = set()
     for r, (specs, ids) in enumerate(zip(oracle.rank_inventory(lay), ids_of(lay))):
         per = []
         for s, i in zip(specs, ids):
             a = np.array(i, dtype=np.int64)
-            tag = np.where(a < 0, SENTINEL, (a + 1).astype(np.uint32)).astype(np.uint32)
+            assert a.max() + 1 < replica
+            tag = np.where(a < 0, sentinel, a + 1)
             rep = np.array([x >= 0 and x in seen for x in i], dtype=bool)
-            tag = np.where(rep, tag | REPLICA, tag)
+            tag = np.where(rep, tag | replica, tag)
             seen.update(x for x in i if x >= 0)
-            per.append(tag.reshape(s.shape))
+            per.append(tag.astype(dt).reshape(s.shape))
         out.append(per)
     return out
 
 
 def expected_tags(lay):
+    dt = TAGS[lay.dtype][0]
     out = []
     for specs, ids in zip(oracle.rank_inventory(lay), ids_of(lay)):
-        out.append([np.where(np.array(i) < 0, 0, np.array(i) + 1).astype(np.uint32).reshape(s.shape)
+        out.append([np.where(np.array(i) < 0, 0, np.array(i) + 1).astype(dt).reshape(s.shape)
                     for s, i in zip(specs, ids)])
     return out
 
@@ -103,6 +106,18 @@ KV_LAYOUTS = micro_layouts(MICRO_KV, tps=(1, 2, 4, 8), pps=(1, 2, 3), pads=(0, 2
 def test_brute_force_all_pairs(src):
     s = tagged_source(src)
     for dst in MICRO_LAYOUTS:
+        got = oracle.reshard(s, src, dst)
+        assert_sets_equal(got, expected_tags(dst))
+
+
+MICRO_LAYOUTS_BF16 = micro_layouts(dtype="bf16")
+
+
+@pytest.mark.parametrize("src", MICRO_LAYOUTS_BF16[::4], ids=lambda l: f"tp{l.tp}pp{l.pp}m{l.pad}{l.qkv[0]}{l.mlp[0]}")
+def test_brute_force_bf16_tags(src):
+    """The same with 16-bit tags on bf16 layouts: the oracle moves 2-byte elements as they are."""
+    s = tagged_source(src)
+    for dst in MICRO_LAYOUTS_BF16[1::3]:
         got = oracle.reshard(s, src, dst)
         assert_sets_equal(got, expected_tags(dst))
 
