@@ -341,17 +341,26 @@ __device__ __forceinline__ v2u to_bf16x4(v4u a) {
   return v2u{bf16_rne(a.x) | (bf16_rne(a.y) << 16), bf16_rne(a.z) | (bf16_rne(a.w) << 16)};
 }
 
+// At most 8 destination vectors per lane per pass (16 source vectors, 64 VGPRs): larger tiles are moved in
+// passes, so that the conversion never spills registers.
+template <int U>
+constexpr int kCvtPass = U > 8 ? 8 : U;
+
 template <int U, bool NT>
 __device__ __forceinline__ void tile_run_f32_bf16(const uint8_t* s, uint8_t* d, uint32_t cnt) {
+  constexpr int P = kCvtPass<U>;
   const uint32_t tid = threadIdx.x;
   const uint32_t last = 2 * cnt - 1;
-  v4u a[2 * U];
 #pragma unroll
-  for (int k = 0; k < 2 * U; ++k) a[k] = ld16<NT>(s, umin(k * kReshardThreads + tid, last) * 16u);
+  for (int h = 0; h < U / P; ++h) {
+    v4u a[2 * P];
 #pragma unroll
-  for (int k = 0; k < 2 * U; ++k) {
-    const uint32_t i = k * kReshardThreads + tid;
-    if (i <= last) st8<NT>(d, i * 8u, to_bf16x4(a[k]));
+    for (int k = 0; k < 2 * P; ++k) a[k] = ld16<NT>(s, umin((h * 2 * P + k) * kReshardThreads + tid, last) * 16u);
+#pragma unroll
+    for (int k = 0; k < 2 * P; ++k) {
+      const uint32_t i = (h * 2 * P + k) * kReshardThreads + tid;
+      if (i <= last) st8<NT>(d, i * 8u, to_bf16x4(a[k]));
+    }
   }
 }
 
@@ -361,21 +370,25 @@ __device__ __forceinline__ void tile_run_f32_bf16(const uint8_t* s, uint8_t* d, 
 template <int U, bool NT>
 __device__ __forceinline__ void tile_rows_f32_bf16(const uint8_t* s, uint8_t* d, uint32_t r0, uint32_t last,
                                                    uint32_t rv, uint32_t mg, uint32_t ss, uint32_t ds) {
+  constexpr int P = kCvtPass<U>;
   const uint32_t tid = threadIdx.x;
   const uint32_t lasth = 2 * last + 1, h = 2 * rv;
-  v4u a[2 * U];
 #pragma unroll
-  for (int k = 0; k < 2 * U; ++k) {
-    const uint32_t n = 2 * r0 + umin(k * kReshardThreads + tid, lasth);
-    const uint32_t q = rv > 1 ? __umulhi(n >> 1, mg) : (n >> 1);
-    a[k] = ld16<NT>(s, q * ss + (n - q * h) * 16u);
-  }
+  for (int p = 0; p < U / P; ++p) {
+    v4u a[2 * P];
 #pragma unroll
-  for (int k = 0; k < 2 * U; ++k) {
-    const uint32_t i = k * kReshardThreads + tid;
-    const uint32_t n = 2 * r0 + i;
-    const uint32_t q = rv > 1 ? __umulhi(n >> 1, mg) : (n >> 1);
-    if (i <= lasth) st8<NT>(d, q * ds + (n - q * h) * 8u, to_bf16x4(a[k]));
+    for (int k = 0; k < 2 * P; ++k) {
+      const uint32_t n = 2 * r0 + umin((p * 2 * P + k) * kReshardThreads + tid, lasth);
+      const uint32_t q = rv > 1 ? __umulhi(n >> 1, mg) : (n >> 1);
+      a[k] = ld16<NT>(s, q * ss + (n - q * h) * 16u);
+    }
+#pragma unroll
+    for (int k = 0; k < 2 * P; ++k) {
+      const uint32_t i = (p * 2 * P + k) * kReshardThreads + tid;
+      const uint32_t n = 2 * r0 + i;
+      const uint32_t q = rv > 1 ? __umulhi(n >> 1, mg) : (n >> 1);
+      if (i <= lasth) st8<NT>(d, q * ds + (n - q * h) * 8u, to_bf16x4(a[k]));
+    }
   }
 }
 

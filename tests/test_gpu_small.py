@@ -417,6 +417,25 @@ def test_converting_reshard_small(gpu_lib, pair):
     run_pair(emu.Layout(m, 2, 2, 128, a), emu.Layout(m, 1, 1, 0, b), bucket_sizes=(65536, 4096 + 4))
 
 
+@pytest.mark.parametrize("tile_vecs", [1, 2, 8, 16])
+@pytest.mark.parametrize("pair", [("fp32", "bf16"), ("bf16", "fp32")])
+def test_converting_tile_sizes(gpu_lib, pair, tile_vecs):
+    """Converting plans at every tile size, row-wrapping tiles and whole-row tiles: fp32 -> bf16 tiles of
+    more than 8 vectors per lane are moved in passes of 8."""
+    a, b = pair
+    old = {k: emu.get_option(k) for k in (emu.OPT_TILE_VECS, emu.OPT_ROW_WRAP)}
+    m = emu.Model(*TINY)
+    try:
+        for wrap in (1, 0):
+            run_pair(emu.Layout(m, 2, 2, 128, a), emu.Layout(m, 1, 1, 0, b, "separate", "separate"),
+                     options={emu.OPT_TILE_VECS: tile_vecs, emu.OPT_ROW_WRAP: wrap})
+            run_pair(emu.Layout(m, 1, 1, 0, a), emu.Layout(m, 2, 2, 0, b), options={emu.OPT_TILE_VECS: tile_vecs,
+                                                                                  emu.OPT_ROW_WRAP: wrap})
+    finally:
+        for k, v in old.items():
+            emu.set_option(k, v)
+
+
 def test_fp32_to_bf16_special_values(gpu_lib):
     """Every fp32 bit pattern class through the kernel: NaNs with payloads in either half, infinities,
     denormals, ties, overflow to infinity -- against the oracle's round-to-nearest-even."""
