@@ -122,6 +122,12 @@ def load(path: str = LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is missing: build it with `python -m paper_2609_34645_amd.build`")
+    # torch ships its own HIP runtime, with the same soname as the system one libemu.so links against, but
+    # its libraries ask for it by the unversioned name. Loaded first, torch's copy satisfies libemu.so's
+    # dependency; loaded after libemu.so, torch would bring in a second HIP runtime in the same process,
+    # and the first one to lose the device reports none. The binding's buffers and streams are torch's, so
+    # torch's runtime is the one to share.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(path)
     P, V, I32, I64, U64 = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64
     sig = {
