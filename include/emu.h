@@ -46,6 +46,9 @@
  *     and the plan must stay alive until that work has completed.
  *   - Every function returns an emu_status (0 = EMU_OK); none aborts or throws. On error,
  *     emu_last_error() returns a thread-local message.
+ *   - Launch failures are read from the HIP runtime's per-thread last error (hipGetLastError), which
+ *     emu_reshard, emu_pack_buckets and emu_unpack_buckets clear just before launching: an error an
+ *     earlier HIP call on the thread left pending is not reported as theirs, and is gone afterwards.
  *   - A plan is immutable after emu_plan and may be used from several threads; an uploaded workspace
  *     is only read by the kernels and may serve concurrent launches on several streams.
  */

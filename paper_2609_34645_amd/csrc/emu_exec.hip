@@ -706,6 +706,11 @@ static size_t occupancy_lds(size_t need, uint64_t tile_bytes, uint64_t flight) {
   return r > need ? r : need;
 }
 
+// Kernel launches report through the runtime's per-thread last-error state. An error some earlier
+// runtime call left there belongs to that call, which has already returned it: it is dropped before the
+// library launches, so that hip_check afterwards sees only the library's own launches.
+static void drop_pending_error() { (void)hipGetLastError(); }
+
 static int hip_check(const char* what) {
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(EMU_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -818,6 +823,7 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
     const int32_t b_shift = (B & (B - 1)) == 0 ? __builtin_ctzll(B) : -1;
     const dim3 g(uint32_t(t.n_tiles));  // padded to a multiple of kXcds
     const size_t lds = occupancy_lds(0, kTileChunkBytes, kBucketFlightBytes);
+    drop_pending_error();
     if (unpack) {
       if (ntm) hipLaunchKernelGGL((k_buckets_tile<true, true, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
       else hipLaunchKernelGGL((k_buckets_tile<true, false, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
@@ -827,6 +833,7 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
     }
     return hip_check(unpack ? "emu_unpack_buckets launch" : "emu_pack_buckets launch");
   }
+  drop_pending_error();
   if (unpack) {
     if (ntm) hipLaunchKernelGGL((k_buckets<true, true, kBucketUnroll>), dim3(uint32_t(grid)), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);
     else hipLaunchKernelGGL((k_buckets<true, false, kBucketUnroll>), dim3(uint32_t(grid)), dim3(kThreads), 0, st, sizes, rf, rb, cf, s.nranks, B, tptr, bptr);
@@ -877,6 +884,7 @@ int emu_reshard(emu_plan_t plan, const void* d_workspace, const uint64_t* d_src_
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
   const bool ntm = option(EMU_OPT_NONTEMPORAL) != 0, lds = option(EMU_OPT_LDS_STAGING) != 0;
   const bool xcd = option(EMU_OPT_XCD_REMAP) != 0;
+  drop_pending_error();
   switch (P->tile_vecs) {
     case 1: dispatch_reshard<1>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;
     case 2: dispatch_reshard<2>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;

@@ -369,6 +369,46 @@ def test_execute_errors(gpu_lib):
     torch.cuda.synchronize()
 
 
+def test_pending_hip_error_is_not_reported(gpu_lib):
+    """An error that an earlier HIP call left pending on the thread (hipSetDevice of a device that does
+    not exist) is not reported by reshard, pack or unpack, which run, return EMU_OK and match the oracle."""
+    import ctypes
+
+    import torch
+
+    hip = ctypes.CDLL("libamdhip64.so.7")  # the runtime that torch and the library already share
+    bad = torch.cuda.device_count() + 1000
+
+    def leave_error():
+        assert hip.hipSetDevice(ctypes.c_int(bad)) != 0
+        assert hip.hipPeekAtLastError() != 0
+
+    m = emu.Model(*TINY)
+    src, dst = emu.Layout(m, 1, 1), emu.Layout(m, 2, 1)
+    plan = emu.Plan(src, dst)
+    ws = plan.workspace()
+    S, D = plan.alloc(0, fill=0x5A), plan.alloc(1, fill=0xA5)
+    os_ = o_layout(src)
+    upload_shards(oracle.shard(full_model(os_.model, 9, "bf16"), os_), S, tp=1)
+    torch.cuda.synchronize()
+    leave_error()
+    plan.reshard(ws, S.ptrs, D.ptrs)
+    assert hip.hipPeekAtLastError() == 0
+    torch.cuda.synchronize()
+    check_reshard(plan, S, D, label="after a pending error")
+    B = 12288
+    bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77)
+    R = plan.alloc(1, fill=0x11)
+    leave_error()
+    plan.pack(ws, 1, B, D.ptrs, bptrs)
+    leave_error()
+    plan.unpack(ws, 1, B, bptrs, R.ptrs)
+    assert hip.hipPeekAtLastError() == 0
+    torch.cuda.synchronize()
+    for a, b in zip(D.tensors, R.tensors):
+        assert torch.equal(a, b)
+
+
 @pytest.mark.parametrize("B", [64, 1000, 4094, 65536, 65538])
 def test_fused_reshard_to_buckets(gpu_lib, B):
     """emu_plan_to_buckets: source shards straight into the destination ranks' buckets; the receiver
