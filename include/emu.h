@@ -38,7 +38,10 @@
  * Ownership and execution:
  *   - The caller allocates and owns every device buffer (tensors, buckets, pointer tables, workspace)
  *     and every stream. The library allocates host memory for plans only: it never calls hipMalloc or
- *     hipFree and never synchronizes a device or stream.
+ *     hipFree and never synchronizes a device or stream itself. The one host-to-device copy,
+ *     emu_plan_upload, reads the plan's pageable host memory, and the HIP runtime may hold the calling
+ *     thread until the stream has reached that copy (it does for workspaces of megabytes): upload once
+ *     per plan, before the work it should not wait for.
  *   - Pointer tables are DEVICE arrays of 64-bit device addresses. Every tensor and bucket base must be
  *     16-byte aligned. Source and destination buffers must not overlap (undefined behaviour).
  *   - Execute calls only enqueue work on the given stream (a hipStream_t; NULL = default stream) on the
@@ -217,7 +220,8 @@ int emu_tensor_info(emu_plan_t plan, int32_t side, int32_t index, emu_tensor_des
 int emu_plan_segments(emu_plan_t plan, int64_t first, int64_t count, emu_segment_t* out);
 
 /* Enqueue the host-to-device copy of the plan's tables into the caller's workspace (at least
- * info.workspace_bytes, 256-byte aligned). The plan must outlive the copy. The library records that
+ * info.workspace_bytes, 256-byte aligned). The plan must outlive the copy. The source is pageable host
+ * memory, so the HIP runtime may return only once the stream has reached the copy. The library records that
  * this address now holds this plan's tables: execute calls of the plan accept only a workspace so
  * recorded (EMU_ERR_WORKSPACE otherwise, before anything is launched), and an upload of another plan to
  * the same address replaces the record. */
