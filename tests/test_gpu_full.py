@@ -2,7 +2,9 @@
 
 * 1B-class decoder, TP4 PP1 -> TP2 PP1 (bf16): every byte against the oracle.
 * 8B decoder, TP2 PP2 -> TP4 PP1 (bf16, 16 GB each side): every byte against the oracle, streamed per
-  tensor group; then the reverse transition checked as a round trip on the device.
+  tensor group; the benchmark's 2^28-byte buckets, from emu_pack_buckets and from the fused plan, every
+  byte against the oracle, and unpacked; then the reverse transition checked as a round trip on the
+  device.
 * 8B, padded vocabulary, TP8 PP4 -> TP2 PP2, packed into 2^28-byte buckets (mid-row bucket boundaries)
   and unpacked on the receiver side: reshard, bucket bytes and unpacked tensors against the oracle;
   again with 2^28 - 2 byte buckets, which put tensor and bucket bytes at different 16-byte phases.
@@ -89,7 +91,7 @@ def test_8b_tp2pp2_to_tp4pp1(gpu_lib):
     torch.cuda.synchronize()
     say(f"  8B reshard done in {time.time() - t:.3f} s (incl. launch)")
     check_reshard(p, S, D, label="8B TP2PP2->TP4PP1")
-    _pack_check(p, ws, D, 1 << 28, "fused reshard->buckets 2^28 (benchmark workload)", S=S)
+    _pack_check(p, ws, D, 1 << 28, "pack and fused reshard->buckets 2^28 (benchmark workload)", S=S, pack_too=True)
     # Merge back: the round trip reproduces the source; norm replicas of TP rank 1 come back as rank 0's
     A2 = back.alloc(1, fill=0x5A)
     back.reshard(wb, D.ptrs, A2.ptrs)
@@ -101,19 +103,24 @@ def test_8b_tp2pp2_to_tp4pp1(gpu_lib):
     cleanup()
 
 
-def _pack_check(p, ws, D, B, label, S=None):
+def _pack_check(p, ws, D, B, label, S=None, pack_too=False):
     """Fill buckets of size B -- with emu_pack_buckets from D, or, when the source set S is given, with
-    the fused source -> bucket plan -- and compare every bucket with oracle.pack of the (oracle-verified)
-    destination tensors rank by rank; then unpack into a receiver set and compare it with D."""
+    the fused source -> bucket plan (and with emu_pack_buckets as well when pack_too) -- and compare every
+    bucket with oracle.pack of the (oracle-verified) destination tensors rank by rank; then unpack the
+    first set into a receiver set and compare it with D."""
     import torch
 
-    bufs, bptrs = p.alloc_buckets(1, B, fill=0x77)
-    if S is None:
+    sets = []
+    if S is None or pack_too:
+        bufs, bptrs = p.alloc_buckets(1, B, fill=0x77)
         p.pack(ws, 1, B, D.ptrs, bptrs)
-    else:
+        sets.append(("pack", bufs, bptrs))
+    if S is not None:
+        bufs, bptrs = p.alloc_buckets(1, B, fill=0x33)
         fused = emu.Plan(p.src, p.dst, bucket_bytes=B)
         wf = fused.workspace()
         fused.reshard(wf, S.ptrs, bptrs)
+        sets.append(("fused", bufs, bptrs))
     torch.cuda.synchronize()
     dd = p.tensors(1)
     k = 0
@@ -121,18 +128,21 @@ def _pack_check(p, ws, D, B, label, S=None):
     for r in range(p.info["n_dst_ranks"]):
         tensors = [host_view(D.tensors[i], d, p.dst.dtype) for i, d in enumerate(dd) if d["rank"] == r]
         for w in oracle.pack(tensors, B):
-            got = bufs[k].cpu().numpy()
-            assert got.size == w.size and np.array_equal(got, w), f"{label}: bucket {k} of rank {r} differs"
+            for name, bufs, _ in sets:
+                got = bufs[k].cpu().numpy()
+                assert got.size == w.size and np.array_equal(got, w), f"{label}: {name} bucket {k} of rank {r} differs"
             k += 1
         del tensors
-    assert k == len(bufs)
-    say(f"  {label}: {k} buckets checked against the oracle in {time.time() - t:.1f} s")
+    for _, bufs, _ in sets:
+        assert k == len(bufs)
+    say(f"  {label}: {k} buckets x {len(sets)} checked against the oracle in {time.time() - t:.1f} s")
+    bptrs = sets[0][2]
     R = p.alloc(1, fill=0x11)
     p.unpack(ws, 1, B, bptrs, R.ptrs)
     torch.cuda.synchronize()
     for i, (x, y) in enumerate(zip(D.tensors, R.tensors)):
         assert torch.equal(x, y), f"{label}: unpacked tensor {i} differs"
-    del R, bufs, bptrs
+    del R, sets, bufs, bptrs
     cleanup()
 
 
