@@ -18,8 +18,9 @@ What it computes (paper section 5 and section 6.2):
 
 The paper fixes neither the per-tensor sharding rules nor the fused-weight formats. The readings taken
 here (column/row/vocab-parallel Megatron-style sharding, head-interleaved fused QKV per KV group, block
-fused gate/up, norms replicated on every TP rank and read from TP rank 0, even contiguous PP layer
-ranges, rank = p * tp + t, vocab padding to a multiple of tp * m) are stated where they are used.
+fused gate/up, norms replicated on every TP rank and read from TP rank 0, KV heads replicated when tp
+exceeds their count, contiguous PP layer ranges with the first L mod pp stages holding one more layer,
+rank = p * tp + t, vocab padding to a multiple of tp * m) are stated where they are used.
 
 Modules:
   model    -- model shapes, layout validity, padded vocabulary, per-rank tensor inventory
