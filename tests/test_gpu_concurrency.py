@@ -79,6 +79,8 @@ def test_threads_share_plan_and_workspace(gpu_lib):
         for k, (a, b) in enumerate(zip(bufs0, bufs)):
             assert torch.equal(a, b), f"thread {i}: bucket {k}"
     say(f"  {THREADS} threads x {ROUNDS} rounds of reshard + pack + unpack on one plan and workspace: exact")
+    del sets, S, D0, bufs0, bptrs0, ws
+    torch.cuda.empty_cache()
 
 
 def test_execute_calls_do_not_wait_for_the_stream(gpu_lib):
