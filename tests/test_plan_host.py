@@ -192,6 +192,10 @@ def test_error_codes():
         emu.Plan(emu.Layout(deep, 1, 2), emu.Layout(deep, 1, 1))
     assert e.value.code == -4
     assert emu.Plan(emu.Layout(deep, 1, 2), emu.Layout(deep, 2, 2)).info["n_dst_tensors"] == 2 * (2 * 6 * 200 + 3)
+    huge = emu.Model(1, 8192, 64, 128, 8, 2048, 1 << 30)         # 16 TiB embedding: 2^32 tiles of 4 KB
+    with pytest.raises(emu.EmuError) as e:
+        emu.Plan(emu.Layout(huge, 1, 1), emu.Layout(huge, 2, 1))
+    assert e.value.code == -4 and "too many tiles" in str(e.value)
     plan = emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1))
     with pytest.raises(emu.EmuError) as e:
         plan.bucket_layout(1, 0)
