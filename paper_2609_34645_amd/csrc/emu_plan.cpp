@@ -555,8 +555,9 @@ static int finalize(Plan& P) {
   uint8_t* h = P.host_ws.data();
   if (!P.dsegs.empty()) std::memcpy(h + w.off_segs, P.dsegs.data(), P.dsegs.size() * sizeof(DevSeg));
   uint32_t* tm = reinterpret_cast<uint32_t*>(h + w.off_tilemap);
-  std::fill_n(tm, nmap, kNoSeg);
   for (size_t i = 0; i < P.dsegs.size(); ++i) std::fill_n(tm + P.dsegs[i].tile0, segtiles[i], uint32_t(i));
+  std::fill(tm + P.ntiles_copy, tm + P.zero_tile0, kNoSeg);  // the two sections' padding
+  std::fill(tm + P.zero_tile0 + P.ntiles_zero, tm + nmap, kNoSeg);
   for (int sd = 0; sd < 2; ++sd) {
     const SideInfo& s = P.side[sd];
     uint64_t* sz = reinterpret_cast<uint64_t*>(h + w.side[sd].off_sizes);
@@ -576,11 +577,12 @@ static int finalize(Plan& P) {
       ri[4 * r + 0] = first;
       ri[4 * r + 1] = s.rank_bytes[r];
       ri[4 * r + 2] = t1;
-      uint32_t g = t0;
-      for (uint64_t j = 0; j < nch; ++j) {
-        const uint64_t pos = j * kTileChunkBytes;
-        while (g + 1 < t1 && s.tensors[g + 1].stream_offset <= pos) ++g;
-        cm[first + j] = (uint32_t(r) << kMapTensorBits) | g;
+      // chunk j starts in the last tensor g whose stream offset is <= j * kTileChunkBytes: tensor g
+      // takes chunks [ceil(offset_g / C), ceil(offset_{g+1} / C)), the rank's first tensor from chunk 0
+      for (uint32_t g = t0; g < t1; ++g) {
+        const uint64_t j0 = g == t0 ? 0 : (s.tensors[g].stream_offset + kTileChunkBytes - 1) / kTileChunkBytes;
+        const uint64_t j1 = g + 1 < t1 ? (s.tensors[g + 1].stream_offset + kTileChunkBytes - 1) / kTileChunkBytes : nch;
+        if (j1 > j0) std::fill(cm + first + j0, cm + first + j1, (uint32_t(r) << kMapTensorBits) | g);
       }
       first += nch;
     }
