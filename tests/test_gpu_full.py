@@ -11,6 +11,8 @@
 * Tensors over 4 GiB: a one-layer decoder with a 266,240-row vocabulary at hidden size 8192 in fp32
   (8.7 GB embedding and LM head), TP1 PP1 -> TP2 PP1, packed into 2^30-byte buckets and unpacked, then
   converted back to bf16 TP1 PP1: every byte against the oracle.
+* 8B conversions at full size: fp32 TP4 PP1 -> bf16 TP2 PP2 (the weight sync) and bf16 TP2 PP2 -> fp32
+  TP4 PP1, each also fused into 2^28-byte buckets; every byte against the oracle.
 * 8B training state, fp32 master + Adam m + v (96 GB in): TP4 PP1 -> TP1 PP1, one launch per tensor
   group, then split back into the source buffers; master checked in full against the oracle, m and v on
   sampled tensor groups, the back transition against a seeded regeneration of the original state.
@@ -163,6 +165,28 @@ def test_8b_weight_sync_fp32_tp4_to_bf16_tp2pp2(gpu_lib):
     torch.cuda.synchronize()
     check_reshard(p, S, D, label="8B fp32 TP4PP1 -> bf16 TP2PP2")
     _pack_check(p, ws, D, 1 << 28, "fused fp32 -> bf16 buckets 2^28", S=S)
+    del S, D, ws
+    cleanup()
+
+
+def test_8b_bf16_tp2pp2_to_fp32_tp4pp1(gpu_lib):
+    """Generation weights -> fp32 state: bf16 TP2 PP2 to fp32 TP4 PP1, the exact widening and the layout
+    change in one pass (each destination vector reads 8 bytes), then fused into 2^28-byte buckets;
+    every byte against the oracle."""
+    import torch
+
+    m = emu.Model(*EIGHT_B)
+    src, dst = emu.Layout(m, 2, 2, 0, "bf16"), emu.Layout(m, 4, 1, 0, "fp32")
+    p = emu.Plan(src, dst)
+    assert p.info["converts"] == 2 and 2 * p.info["bytes_read"] == p.info["bytes_written"]
+    ws = p.workspace()
+    S = p.alloc(0)
+    fill_device(p, 0, S, seed=405, dtype="bf16")
+    D = p.alloc(1, fill=0xA5)
+    p.reshard(ws, S.ptrs, D.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(p, S, D, label="8B bf16 TP2PP2 -> fp32 TP4PP1")
+    _pack_check(p, ws, D, 1 << 28, "fused bf16 -> fp32 buckets 2^28", S=S)
     del S, D, ws
     cleanup()
 
