@@ -11,6 +11,7 @@
 * Tensors over 4 GiB: a one-layer decoder with a 266,240-row vocabulary at hidden size 8192 in fp32
   (8.7 GB embedding and LM head), TP1 PP1 -> TP2 PP1, packed into 2^30-byte buckets and unpacked, then
   converted back to bf16 TP1 PP1: every byte against the oracle.
+* 8B TP2 PP2 -> TP4 PP1 with non-default tiling and launch options, on sampled tensor groups.
 * 8B conversions at full size: fp32 TP4 PP1 -> bf16 TP2 PP2 (the weight sync) and bf16 TP2 PP2 -> fp32
   TP4 PP1, each also fused into 2^28-byte buckets; every byte against the oracle.
 * 8B training state, fp32 master + Adam m + v (96 GB in): TP4 PP1 -> TP1 PP1, one launch per tensor
@@ -189,6 +190,36 @@ def test_8b_bf16_tp2pp2_to_fp32_tp4pp1(gpu_lib):
     _pack_check(p, ws, D, 1 << 28, "fused bf16 -> fp32 buckets 2^28", S=S)
     del S, D, ws
     cleanup()
+
+
+@pytest.mark.parametrize("opts", [
+    {emu.OPT_ROW_WRAP: 0},
+    {emu.OPT_LDS_STAGING: 1, emu.OPT_XCD_REMAP: 0, emu.OPT_NONTEMPORAL: 0, emu.OPT_WG_PER_CU: 0},
+    {emu.OPT_TILE_VECS: 16, emu.OPT_WG_PER_CU: 2},
+], ids=["whole_rows", "lds_plain_order_cached_uncapped", "16k_tiles_cap2"])
+def test_8b_non_default_launch_options(gpu_lib, opts):
+    """The benchmark transition at full size with non-default tiling and launch options, checked against
+    the oracle on the embedding, layers 0, 1 and 31 and the final norm + LM head."""
+    import torch
+
+    defaults = {k: emu.get_option(k) for k in range(8)}
+    try:
+        for k, v in opts.items():
+            emu.set_option(k, v)
+        m = emu.Model(*EIGHT_B)
+        p = emu.Plan(emu.Layout(m, 2, 2), emu.Layout(m, 4, 1))
+        ws = p.workspace()
+        S = p.alloc(0)
+        fill_device(p, 0, S, seed=77)
+        D = p.alloc(1, fill=0xA5)
+        p.reshard(ws, S.ptrs, D.ptrs)
+        torch.cuda.synchronize()
+        check_reshard(p, S, D, groups=["embed", 0, 1, 31, "final"], label=f"8B with {opts}")
+        del S, D, ws
+        cleanup()
+    finally:
+        for k, v in defaults.items():
+            emu.set_option(k, v)
 
 
 def test_8b_kv_replication_uneven_pp(gpu_lib):
