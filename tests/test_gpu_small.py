@@ -507,3 +507,82 @@ def test_kv_replication_and_uneven_pp_small(gpu_lib):
     for i, src in enumerate(lays):
         for dst in lays[i % 6::6]:
             run_pair(src, dst, seed=i)
+
+
+def _scattered(plan, side, rng, fill):
+    """One side's tensors at shuffled positions of one buffer, each at a random 16-byte (not 256-byte)
+    aligned offset: the ABI promises only 16-byte alignment."""
+    import torch
+
+    descs = plan.tensors(side)
+    order = list(range(len(descs)))
+    rng.shuffle(order)
+    offs, pos = [0] * len(descs), 0
+    for i in order:
+        pos += 16 * rng.randint(1, 15)
+        offs[i] = pos
+        pos = (pos + descs[i]["bytes"] + 15) // 16 * 16
+    buf = torch.full((pos + 256,), fill, dtype=torch.uint8, device="cuda")
+    tensors = [buf[o:o + d["bytes"]] for o, d in zip(offs, descs)]
+    return emu.ShardSet([buf], tensors, emu.ptr_table(tensors))
+
+
+def _scattered_buckets(plan, side, B, rng, fill):
+    import torch
+
+    nranks = plan.info["n_src_ranks" if side == 0 else "n_dst_ranks"]
+    sizes = []
+    for r in range(nranks):
+        nb, sb = plan.bucket_layout(side, B, r)
+        sizes += [min(B, sb - k * B) for k in range(nb)]
+    offs, pos = [], 0
+    for n in sizes:
+        pos += 16 * rng.randint(1, 15)
+        offs.append(pos)
+        pos = (pos + n + 15) // 16 * 16
+    buf = torch.full((pos + 256,), fill, dtype=torch.uint8, device="cuda")
+    bufs = [buf[o:o + n] for o, n in zip(offs, sizes)]
+    return bufs, emu.ptr_table(bufs)
+
+
+@pytest.mark.parametrize("pair", [("bf16", "bf16"), ("fp32", "bf16"), ("bf16", "fp32")])
+def test_tensors_at_16_byte_offsets(gpu_lib, pair):
+    """Source, destination and bucket buffers placed at shuffled, merely 16-byte aligned addresses: the
+    reshard (plain and converting), pack, unpack and the fused plan against the oracle."""
+    import random
+
+    import torch
+
+    rng = random.Random(17)
+    m = emu.Model(*TINY)
+    src = emu.Layout(m, 2, 2, 128, pair[0])
+    dst = emu.Layout(m, 1, 1, 0, pair[1], "separate", "block")
+    plan = emu.Plan(src, dst)
+    ws = plan.workspace()
+    S, D = _scattered(plan, 0, rng, 0x5A), _scattered(plan, 1, rng, 0xA5)
+    plan.check_tables(S.ptrs, D.ptrs)
+    os_ = o_layout(src)
+    upload_shards(oracle.shard(full_model(os_.model, 23, src.dtype), os_), S, tp=src.tp)
+    plan.reshard(ws, S.ptrs, D.ptrs)
+    torch.cuda.synchronize()
+    check_reshard(plan, S, D, label=f"16-byte offsets {pair}")
+    B = 6000 if pair[1] == "bf16" else 6004
+    bufs, bptrs = _scattered_buckets(plan, 1, B, rng, 0x77)
+    plan.check_bucket_tables(1, B, D.ptrs, bptrs)
+    plan.pack(ws, 1, B, D.ptrs, bptrs)
+    R = _scattered(plan, 1, rng, 0x11)
+    plan.unpack(ws, 1, B, bptrs, R.ptrs)
+    fused = emu.Plan(src, dst, bucket_bytes=B)
+    fws = fused.workspace()
+    fbufs, fbptrs = _scattered_buckets(plan, 1, B, rng, 0x33)
+    fused.reshard(fws, S.ptrs, fbptrs)
+    torch.cuda.synchronize()
+    dd = plan.tensors(1)
+    ranks = {}
+    for i, d in enumerate(dd):
+        ranks.setdefault(d["rank"], []).append(host_view(D.tensors[i], d, dst.dtype))
+    check_buckets(plan, 1, B, [ranks[r] for r in sorted(ranks)], bufs, label=f"16-byte offsets B={B}")
+    for k, (a, b) in enumerate(zip(bufs, fbufs)):
+        assert torch.equal(a, b), f"fused bucket {k}"
+    for i, (a, b) in enumerate(zip(D.tensors, R.tensors)):
+        assert torch.equal(a, b), f"unpacked tensor {i}"
