@@ -2,7 +2,9 @@
 
 Launch order: one plain elementwise copy of the destination bytes (torch uint8 add of 0, a kernel of
 known traffic: N bytes read + N written, used to calibrate FETCH_SIZE / WRITE_SIZE), one emu_reshard,
-one emu_pack_buckets (2^28-byte buckets) and one emu_unpack_buckets. Example:
+one emu_pack_buckets (2^28-byte buckets) and one emu_unpack_buckets; then the two converting
+reshards of the same model: fp32 TP4 PP1 -> bf16 TP2 PP2 (the weight sync) and bf16 TP2 PP2 -> fp32
+TP4 PP1. Example:
 
     rocprofv3 --pmc FETCH_SIZE -d out -o pmc_fetch -- python -m paper_2609_34645_amd.profile_once
 """
@@ -43,6 +45,21 @@ def main():
     print(f"profile_once: reshard {plan.info['bytes_read']} B read + {plan.info['bytes_written']} B written; "
           f"calibration copies {sum(min(a.numel(), b.numel()) for a, b in zip(S.bufs, R.bufs))} B; "
           f"destination {n} B", flush=True)
+    del D, R, bufs, bptrs
+    torch.cuda.empty_cache()
+    for s_lay, d_lay in ((emu.Layout(m, 4, 1, 0, "fp32"), emu.Layout(m, 2, 2, 0, "bf16")),
+                         (emu.Layout(m, 2, 2, 0, "bf16"), emu.Layout(m, 4, 1, 0, "fp32"))):
+        cp = emu.Plan(s_lay, d_lay)
+        cws = cp.workspace()
+        CS, CD = cp.alloc(0), cp.alloc(1)
+        device_fill(CS.tensors, 2, ["weight"] * len(CS.tensors), s_lay.dtype)
+        torch.cuda.synchronize()
+        cp.reshard(cws, CS.ptrs, CD.ptrs)
+        torch.cuda.synchronize()
+        print(f"profile_once: {s_lay.dtype} -> {d_lay.dtype} reshard {cp.info['bytes_read']} B read + "
+              f"{cp.info['bytes_written']} B written", flush=True)
+        del CS, CD, cws
+        torch.cuda.empty_cache()
 
 
 if __name__ == "__main__":
