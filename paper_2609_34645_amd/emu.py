@@ -209,6 +209,14 @@ class Layout:
     qkv: str = "interleaved"
     mlp: str = "block"
 
+    def __post_init__(self):
+        if self.dtype not in DTYPES:
+            raise ValueError(f"dtype must be one of {sorted(DTYPES)}, not {self.dtype!r}")
+        if self.qkv not in ("interleaved", "separate"):
+            raise ValueError(f"qkv must be 'interleaved' or 'separate', not {self.qkv!r}")
+        if self.mlp not in ("block", "separate"):
+            raise ValueError(f"mlp must be 'block' or 'separate', not {self.mlp!r}")
+
     def c(self) -> c_layout:
         m = self.model
         return c_layout(c_model(m.num_layers, m.hidden, m.num_heads, m.num_kv_heads, m.head_dim, m.ffn_hidden,
@@ -231,10 +239,11 @@ def _stream_handle(stream):
 
 
 class ShardSet:
-    """One side's tensors on the device: one uint8 buffer per rank, tensors as 256-byte aligned views.
+    """One side's tensors on the device: the backing buffers, the tensors and their pointer table.
 
-    ``ptrs`` is the device pointer table (int64) in global tensor order; ``tensors[i]`` is a uint8 view
-    of tensor i's bytes.
+    ``tensors[i]`` is a uint8 view of tensor i's bytes, ``ptrs`` the device pointer table (int64) in
+    global tensor order. ``Plan.alloc`` makes one buffer per rank with 256-byte aligned views; the
+    library itself needs only 16-byte aligned tensors.
     """
 
     def __init__(self, bufs, tensors, ptrs):

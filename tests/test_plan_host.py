@@ -528,3 +528,12 @@ def test_layout_validation_and_inventory_match_oracle_random():
                 for r, specs in enumerate(oracle.rank_inventory(ol)) for s in specs]
         assert got == want, (shape, args)
     assert min(seen.values()) > 100, seen
+
+
+def test_binding_rejects_unknown_format_names():
+    """A misspelt format or dtype must not silently select another format."""
+    m = emu.Model(*TINY)
+    for kw in ({"qkv": "interleave"}, {"mlp": "interleaved"}, {"dtype": "fp16"}):
+        with pytest.raises(ValueError):
+            emu.Layout(m, 1, 1, **kw)
+    assert emu.Layout(m, 1, 1, 0, "fp32", "separate", "separate").c().mlp_format == 1
