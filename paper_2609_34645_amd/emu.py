@@ -355,15 +355,48 @@ class Plan:
 
     # -- execution -----------------------------------------------------------------------------
     def reshard(self, ws, src_ptrs, dst_ptrs, stream=None):
+        self._tables(ws, (src_ptrs, self.info["n_src_tensors"], "src_ptrs"),
+                     (dst_ptrs, self.info["n_dst_tensors"], "dst_ptrs"))
         check(load().emu_reshard(self._h, ctypes.c_void_p(ws.data_ptr()), ctypes.c_void_p(src_ptrs.data_ptr()),
                                  ctypes.c_void_p(dst_ptrs.data_ptr()), _stream_handle(stream)))
 
+    def _tables(self, ws, *tables):
+        """Refuse, before any library call, pointer tables the kernels would read past the end of:
+        each must be an int64 device tensor with exactly the entries the plan indexes."""
+        for t, n, what in tables:
+            if getattr(t, "dtype", None) is None or str(t.dtype) != "torch.int64":
+                raise ValueError(f"{what} must be an int64 tensor (emu.ptr_table), not {type(t).__name__}")
+            if t.numel() != n or (n and not t.is_contiguous()):
+                raise ValueError(f"{what} has {t.numel()} entries, the plan needs {n} (contiguous)")
+        for t, _, what in tables:
+            if not t.is_cuda:
+                raise ValueError(f"{what} must be a device tensor")
+        if not getattr(ws, "is_cuda", False):
+            raise ValueError("the workspace must be a device tensor")
+
+    def _n_buckets(self, side, bucket_bytes):
+        if bucket_bytes <= 0:
+            return 0  # the library reports the invalid size
+        return self.bucket_layout(side, bucket_bytes, -1)[0]
+
     def pack(self, ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs, stream=None):
+        if side not in (0, 1):
+            raise ValueError("side must be 0 or 1")
+        n_t = self.info["n_src_tensors" if side == 0 else "n_dst_tensors"]
+        if bucket_bytes % ESIZE[DTYPES[(self.src if side == 0 else self.dst).dtype]] == 0:
+            self._tables(ws, (tensor_ptrs, n_t, "tensor_ptrs"),
+                         (bucket_ptrs, self._n_buckets(side, bucket_bytes), "bucket_ptrs"))
         check(load().emu_pack_buckets(self._h, ctypes.c_void_p(ws.data_ptr()), side, bucket_bytes,
                                       ctypes.c_void_p(tensor_ptrs.data_ptr()), ctypes.c_void_p(bucket_ptrs.data_ptr()),
                                       _stream_handle(stream)))
 
     def unpack(self, ws, side, bucket_bytes, bucket_ptrs, tensor_ptrs, stream=None):
+        if side not in (0, 1):
+            raise ValueError("side must be 0 or 1")
+        n_t = self.info["n_src_tensors" if side == 0 else "n_dst_tensors"]
+        if bucket_bytes % ESIZE[DTYPES[(self.src if side == 0 else self.dst).dtype]] == 0:
+            self._tables(ws, (tensor_ptrs, n_t, "tensor_ptrs"),
+                         (bucket_ptrs, self._n_buckets(side, bucket_bytes), "bucket_ptrs"))
         check(load().emu_unpack_buckets(self._h, ctypes.c_void_p(ws.data_ptr()), side, bucket_bytes,
                                         ctypes.c_void_p(bucket_ptrs.data_ptr()), ctypes.c_void_p(tensor_ptrs.data_ptr()),
                                         _stream_handle(stream)))

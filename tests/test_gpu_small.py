@@ -355,9 +355,14 @@ def test_execute_errors(gpu_lib):
     with pytest.raises(emu.EmuError) as e:
         p.reshard(fresh, S.ptrs, D.ptrs)                  # never uploaded
     assert e.value.code == -5 and "emu_plan_upload" in str(e.value)
+    _, fresh_bptrs = p.alloc_buckets(1, 1 << 16)
     with pytest.raises(emu.EmuError) as e:
-        p.pack(fresh, 1, 1 << 16, D.ptrs, D.ptrs)
+        p.pack(fresh, 1, 1 << 16, D.ptrs, fresh_bptrs)
     assert e.value.code == -5
+    with pytest.raises(ValueError):
+        p.pack(ws, 1, 1 << 16, D.ptrs, D.ptrs)            # a table of the wrong length, refused on the host
+    with pytest.raises(ValueError):
+        p.reshard(ws, S.ptrs[:-1], D.ptrs)
     q = emu.Plan(emu.Layout(m, 2, 1), emu.Layout(m, 1, 1))
     assert q.info["workspace_bytes"] <= ws.numel()
     q.upload(ws)                                          # another plan's tables now fill p's workspace

@@ -537,3 +537,30 @@ def test_binding_rejects_unknown_format_names():
         with pytest.raises(ValueError):
             emu.Layout(m, 1, 1, **kw)
     assert emu.Layout(m, 1, 1, 0, "fp32", "separate", "separate").c().mlp_format == 1
+
+
+def test_binding_refuses_tables_the_kernels_would_overrun():
+    """The binding checks pointer tables on the host before any library call: int64, exactly the
+    entries the plan indexes, contiguous, on the device."""
+    import torch
+
+    m = emu.Model(*TINY)
+    plan = emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1))
+    ns, nd = plan.info["n_src_tensors"], plan.info["n_dst_tensors"]
+    ws = torch.zeros(plan.info["workspace_bytes"], dtype=torch.uint8)
+    ok_s, ok_d = torch.zeros(ns, dtype=torch.int64), torch.zeros(nd, dtype=torch.int64)
+    cases = [
+        (lambda: plan.reshard(ws, ok_s[:-1], ok_d), "entries"),
+        (lambda: plan.reshard(ws, ok_s, torch.zeros(nd + 1, dtype=torch.int64)), "entries"),
+        (lambda: plan.reshard(ws, ok_s.to(torch.int32), ok_d), "int64"),
+        (lambda: plan.reshard(ws, [0] * ns, ok_d), "int64"),
+        (lambda: plan.reshard(ws, torch.zeros(2 * ns, dtype=torch.int64)[::2], ok_d), "contiguous"),
+        (lambda: plan.reshard(ws, ok_s, ok_d), "device"),
+        (lambda: plan.pack(ws, 1, 1 << 16, ok_d, ok_d), "entries"),
+        (lambda: plan.unpack(ws, 1, 1 << 16, ok_d, ok_d), "entries"),
+        (lambda: plan.pack(ws, 2, 1 << 16, ok_d, ok_d), "side"),
+    ]
+    for call, word in cases:
+        with pytest.raises(ValueError) as e:
+            call()
+        assert word in str(e.value), (word, str(e.value))
