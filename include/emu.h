@@ -44,6 +44,10 @@
  *     per plan, before the work it should not wait for.
  *   - Pointer tables are DEVICE arrays of 64-bit device addresses. Every tensor and bucket base must be
  *     16-byte aligned. Source and destination buffers must not overlap (undefined behaviour).
+ *   - A pointer table holds exactly the entries the plan indexes: n_src_tensors, n_dst_tensors, or the
+ *     side's bucket count from emu_bucket_layout. The kernels read the tables on the device, so the
+ *     library cannot check their length: a shorter table is undefined behaviour. emu_check_tables and
+ *     emu_check_bucket_tables check host copies of full tables.
  *   - Execute calls only enqueue work on the given stream (a hipStream_t; NULL = default stream) on the
  *     current device, and return. Device faults surface at the caller's next synchronization. Buffers
  *     and the plan must stay alive until that work has completed.
