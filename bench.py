@@ -334,7 +334,7 @@ def bench_other_config(args, emu, torch, cfg):
         "dtype": "u8",
         "data": "synthetic (seeded device draws: N(0,0.02) weights, 1+N(0,0.02) norms, Adam m N(0,1e-3), "
                 "v |N(0,1e-6)|)",
-        "config": {"workload": workload, "model": model_s, "bytes_per_step": step_bytes,
+        "config": {"workload": workload, "decoder_shape": model_s, "bytes_per_step": step_bytes,
                    "parallelism": "none (1 GPU holds all ranks' shards)", "config_id": cfg},
         "launches": [{"name": n, "mean_ms": round(sum(t) / len(t), 4), "median_ms": round(t[len(t) // 2], 4),
                       "GBps": round(nbytes(n, p) / (sum(t) / len(t) * 1e-3) / 1e9, 1)}
@@ -545,7 +545,7 @@ def main():
         "data": "synthetic (seeded N(0,0.02) bf16 weights, 1+N(0,0.02) norms; Llama-3.1-8B shapes)",
         "config": {
             "workload": "8B decoder bf16: reshard TP2PP2->TP4PP1 + pack into 2^28-byte buckets + unpack",
-            "model": "L32 H4096 32x128 heads 8 KV MLP14336 V128256",
+            "decoder_shape": "L32 H4096 32x128 heads 8 KV MLP14336 V128256",
             "src_layout": "TP2PP2", "dst_layout": "TP4PP1", "bucket_bytes": B,
             "bytes_per_step": step_bytes, "parallelism": "none (1 GPU holds all ranks' shards)",
         },
