@@ -374,29 +374,26 @@ class Plan:
         if not getattr(ws, "is_cuda", False):
             raise ValueError("the workspace must be a device tensor")
 
-    def _n_buckets(self, side, bucket_bytes):
-        if bucket_bytes <= 0:
-            return 0  # the library reports the invalid size
-        return self.bucket_layout(side, bucket_bytes, -1)[0]
-
-    def pack(self, ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs, stream=None):
+    def _bucket_tables(self, ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs):
         if side not in (0, 1):
             raise ValueError("side must be 0 or 1")
+        if bucket_bytes < 0:
+            raise ValueError("bucket_bytes must be positive")
+        es = ESIZE[DTYPES[(self.src if side == 0 else self.dst).dtype]]
+        if bucket_bytes == 0 or bucket_bytes % es:
+            return  # the library refuses the size (EMU_ERR_BUCKET) before launching anything
         n_t = self.info["n_src_tensors" if side == 0 else "n_dst_tensors"]
-        if bucket_bytes % ESIZE[DTYPES[(self.src if side == 0 else self.dst).dtype]] == 0:
-            self._tables(ws, (tensor_ptrs, n_t, "tensor_ptrs"),
-                         (bucket_ptrs, self._n_buckets(side, bucket_bytes), "bucket_ptrs"))
+        self._tables(ws, (tensor_ptrs, n_t, "tensor_ptrs"),
+                     (bucket_ptrs, self.bucket_layout(side, bucket_bytes, -1)[0], "bucket_ptrs"))
+
+    def pack(self, ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs, stream=None):
+        self._bucket_tables(ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs)
         check(load().emu_pack_buckets(self._h, ctypes.c_void_p(ws.data_ptr()), side, bucket_bytes,
                                       ctypes.c_void_p(tensor_ptrs.data_ptr()), ctypes.c_void_p(bucket_ptrs.data_ptr()),
                                       _stream_handle(stream)))
 
     def unpack(self, ws, side, bucket_bytes, bucket_ptrs, tensor_ptrs, stream=None):
-        if side not in (0, 1):
-            raise ValueError("side must be 0 or 1")
-        n_t = self.info["n_src_tensors" if side == 0 else "n_dst_tensors"]
-        if bucket_bytes % ESIZE[DTYPES[(self.src if side == 0 else self.dst).dtype]] == 0:
-            self._tables(ws, (tensor_ptrs, n_t, "tensor_ptrs"),
-                         (bucket_ptrs, self._n_buckets(side, bucket_bytes), "bucket_ptrs"))
+        self._bucket_tables(ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs)
         check(load().emu_unpack_buckets(self._h, ctypes.c_void_p(ws.data_ptr()), side, bucket_bytes,
                                         ctypes.c_void_p(bucket_ptrs.data_ptr()), ctypes.c_void_p(tensor_ptrs.data_ptr()),
                                         _stream_handle(stream)))

@@ -559,6 +559,7 @@ def test_binding_refuses_tables_the_kernels_would_overrun():
         (lambda: plan.pack(ws, 1, 1 << 16, ok_d, ok_d), "entries"),
         (lambda: plan.unpack(ws, 1, 1 << 16, ok_d, ok_d), "entries"),
         (lambda: plan.pack(ws, 2, 1 << 16, ok_d, ok_d), "side"),
+        (lambda: plan.unpack(ws, 1, -2, ok_d, ok_d), "positive"),
     ]
     for call, word in cases:
         with pytest.raises(ValueError) as e:
