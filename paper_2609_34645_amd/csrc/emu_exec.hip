@@ -15,6 +15,7 @@
 
 #include "emu_internal.h"
 
+
 namespace emu {
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
@@ -165,12 +166,53 @@ __device__ __forceinline__ void wg_vec_copy(const uint8_t* __restrict__ s, uint8
   }
 }
 
-// Workgroup-cooperative copy of nv destination-aligned vectors whose source starts `sh` bytes past
-// the 16-byte aligned address sa (0 < sh < 16): each output vector is cut from two consecutive aligned
-// source vectors. Each lane loads one; the next one comes from the neighbouring lane through a
-// cross-lane shuffle, and only lane 63 and the lanes from the last output on load it themselves. The
-// last output's second vector lies in the granule of the last source byte, so no read leaves the
-// granules the copy's own bytes occupy.
+// Workgroup-cooperative copies of nv destination-aligned vectors whose source starts `sh` bytes past the
+// 16-byte aligned address sa (0 < sh < 16): output vector i is cut from aligned source vectors i and
+// i + 1 (funnel). Each lane loads vector i; vector i + 1 comes from the next lane through DPP
+// (wave_shl:1, a VALU operand modifier rather than an LDS permute). The last output's second vector is
+// the granule holding the copy's last source byte, so no read leaves the granules the copy's own bytes
+// occupy.
+//
+// One wave per workgroup: lane 63 of a block of 64 vectors takes lane 0 of the next block through
+// wave_rol:1, and only lane 63 of a pass's last block loads a vector of its own (one masked load per
+// pass). Lanes past the end load vector last + 1, so lane `last` finds its second vector in the next lane.
+template <int U, bool NT, int Q>
+__device__ __forceinline__ void wave_shift_copy(const uint8_t* __restrict__ sa, uint8_t* __restrict__ d, uint32_t nv,
+                                                uint32_t b) {
+  const uint32_t lane = threadIdx.x;
+  constexpr uint32_t TV = 64u * U;
+#pragma nounroll
+  for (uint32_t base = 0; base < nv; base += TV) {
+    const uint32_t last = umin(nv - base, TV) - 1;
+    v4u lo[U + 1];
+#pragma unroll
+    for (int u = 0; u < U; ++u) lo[u] = ld16<NT>(sa, (base + umin(u * 64u + lane, last + 1)) * 16u);
+    lo[U] = v4u{0, 0, 0, 0};
+    if (lane == 63u) lo[U] = ld16<NT>(sa, (base + umin(TV - 1, last) + 1u) * 16u);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t i = u * 64u + lane;
+      v4u nx, hi;
+      if (u + 1 < U) {
+        nx.x = __builtin_amdgcn_update_dpp(0u, lo[u + 1].x, 0x134, 0xf, 0xf, false);  // wave_rol:1
+        nx.y = __builtin_amdgcn_update_dpp(0u, lo[u + 1].y, 0x134, 0xf, 0xf, false);
+        nx.z = __builtin_amdgcn_update_dpp(0u, lo[u + 1].z, 0x134, 0xf, 0xf, false);
+        nx.w = __builtin_amdgcn_update_dpp(0u, lo[u + 1].w, 0x134, 0xf, 0xf, false);
+      } else {
+        nx = lo[U];
+      }
+      // wave_shl:1; lane 63 has no source lane and keeps nx
+      hi.x = __builtin_amdgcn_update_dpp(nx.x, lo[u].x, 0x130, 0xf, 0xf, false);
+      hi.y = __builtin_amdgcn_update_dpp(nx.y, lo[u].y, 0x130, 0xf, 0xf, false);
+      hi.z = __builtin_amdgcn_update_dpp(nx.z, lo[u].z, 0x130, 0xf, 0xf, false);
+      hi.w = __builtin_amdgcn_update_dpp(nx.w, lo[u].w, 0x130, 0xf, 0xf, false);
+      if (i <= last) st16<NT>(d, (base + i) * 16u, funnel<Q>(lo[u], hi, b));
+    }
+  }
+}
+
+// Several waves per workgroup: lane 63 of every wave, and the lanes from the last output on, load their
+// second vector themselves.
 template <int NTH, int U, bool NT, int Q>
 __device__ __forceinline__ void wg_shift_copy(const uint8_t* __restrict__ sa, uint8_t* __restrict__ d, uint32_t nv,
                                               uint32_t b) {
@@ -192,10 +234,10 @@ __device__ __forceinline__ void wg_shift_copy(const uint8_t* __restrict__ sa, ui
     for (int u = 0; u < U; ++u) {
       const uint32_t i = u * NTH + tid;
       v4u hi;
-      hi.x = __shfl_down(lo[u].x, 1u, 64);
-      hi.y = __shfl_down(lo[u].y, 1u, 64);
-      hi.z = __shfl_down(lo[u].z, 1u, 64);
-      hi.w = __shfl_down(lo[u].w, 1u, 64);
+      hi.x = __builtin_amdgcn_update_dpp(0u, lo[u].x, 0x130, 0xf, 0xf, false);  // wave_shl:1
+      hi.y = __builtin_amdgcn_update_dpp(0u, lo[u].y, 0x130, 0xf, 0xf, false);
+      hi.z = __builtin_amdgcn_update_dpp(0u, lo[u].z, 0x130, 0xf, 0xf, false);
+      hi.w = __builtin_amdgcn_update_dpp(0u, lo[u].w, 0x130, 0xf, 0xf, false);
       if (lane == 63u || i >= last) hi = own[u];
       if (i <= last) st16<NT>(d, (base + i) * 16u, funnel<Q>(lo[u], hi, b));
     }
@@ -224,11 +266,20 @@ __device__ __forceinline__ void wg_copy_bytes(const uint8_t* s, uint8_t* d, uint
       wg_vec_copy<NTH, UA, NT, false>(s + head, d + head, nv);
     } else {
       const uint8_t* sa = s + head - sh;
-      switch (sh >> 2) {
-        case 0: wg_shift_copy<NTH, US, NT, 0>(sa, d + head, nv, sh & 3); break;
-        case 1: wg_shift_copy<NTH, US, NT, 1>(sa, d + head, nv, sh & 3); break;
-        case 2: wg_shift_copy<NTH, US, NT, 2>(sa, d + head, nv, sh & 3); break;
-        default: wg_shift_copy<NTH, US, NT, 3>(sa, d + head, nv, sh & 3); break;
+      if constexpr (NTH == 64) {
+        switch (sh >> 2) {
+          case 0: wave_shift_copy<US, NT, 0>(sa, d + head, nv, sh & 3); break;
+          case 1: wave_shift_copy<US, NT, 1>(sa, d + head, nv, sh & 3); break;
+          case 2: wave_shift_copy<US, NT, 2>(sa, d + head, nv, sh & 3); break;
+          default: wave_shift_copy<US, NT, 3>(sa, d + head, nv, sh & 3); break;
+        }
+      } else {
+        switch (sh >> 2) {
+          case 0: wg_shift_copy<NTH, US, NT, 0>(sa, d + head, nv, sh & 3); break;
+          case 1: wg_shift_copy<NTH, US, NT, 1>(sa, d + head, nv, sh & 3); break;
+          case 2: wg_shift_copy<NTH, US, NT, 2>(sa, d + head, nv, sh & 3); break;
+          default: wg_shift_copy<NTH, US, NT, 3>(sa, d + head, nv, sh & 3); break;
+        }
       }
     }
   }
@@ -598,6 +649,13 @@ __global__ __launch_bounds__(kThreads, EMU_BUCKET_WAVES_PER_EU) void k_buckets(c
 // record; the map is padded to the grid, so no bounds check precedes it. The rank's first bucket, the
 // sum over earlier ranks of ceil(bytes / B), comes from the host in a kernel argument for the first
 // kArgRanks ranks, else from a wave64 reduction. The chunk is then cut at tensor and bucket boundaries.
+//
+// Chunk ends sit on the destination's 4 KB grid. For aligned buckets and tensors that is the stream's
+// grid. When it is not (pack into buckets whose size is not a multiple of 4 KB, unpack into tensors whose
+// stream offsets are not), both ends of every chunk move down to the destination's grid, by the same
+// rule on either side of each cut, so consecutive chunks still tile the stream. Every destination cache
+// line is then written by one workgroup; cut on the stream's grid, every chunk end would split a line
+// between two workgroups, which costs partial-line writes to HBM.
 constexpr int kArgRanks = 128;
 struct BucketBases {
   uint64_t first[kArgRanks];  // first bucket of each rank, for ranks below kArgRanks
@@ -607,7 +665,8 @@ template <bool UNPACK, bool NT, int U>
 __global__ __launch_bounds__(kBucketTileThreads, EMU_RESHARD_WAVES_PER_EU) void k_buckets_tile(
     const uint64_t* __restrict__ stream_off, const uint64_t* __restrict__ rank_info,
     const uint64_t* __restrict__ rank_bytes, const uint32_t* __restrict__ tile_map, uint64_t B, int32_t b_shift,
-    const uint64_t* __restrict__ tensor_ptrs, const uint64_t* __restrict__ bucket_ptrs, BucketBases bases) {
+    uint32_t realign, const uint64_t* __restrict__ tensor_ptrs, const uint64_t* __restrict__ bucket_ptrs,
+    BucketBases bases) {
   const uint32_t per = gridDim.x / kXcds;  // the host launches the padded map's length, a multiple of kXcds
   const uint32_t c = (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
   const uint32_t m = tile_map[c];
@@ -625,9 +684,25 @@ __global__ __launch_bounds__(kBucketTileThreads, EMU_RESHARD_WAVES_PER_EU) void 
     for (uint32_t q = lane; q < r; q += 64) acc += (rank_bytes[q] + B - 1) / B;
     bucket0 = uniform64(wave_sum(acc));
   }
-  const uint64_t start = (c - c0) * kTileChunkBytes;
-  const uint64_t end = start + kTileChunkBytes < S ? start + kTileChunkBytes : S;
+  uint64_t start = (c - c0) * kTileChunkBytes;
+  uint64_t end = start + kTileChunkBytes < S ? start + kTileChunkBytes : S;
   uint64_t k = b_shift >= 0 ? start >> b_shift : start / B;
+  if (realign) {
+    // pack: bucket k's grid starts at stream byte k*B; unpack: a tensor's grid starts at its stream
+    // offset (the tensor holding `end` is the next chunk's map entry). A start never leaves its bucket
+    // (pack) or tensor (unpack); it may move back into earlier tensors (pack) or an earlier bucket
+    // (unpack). Chunks stay non-empty and below 2 * kTileChunkBytes.
+    constexpr uint64_t kGrid = kTileChunkBytes - 1;
+    if constexpr (UNPACK) {
+      start -= (start - stream_off[g]) & kGrid;
+      if (end < S) end -= (end - stream_off[tile_map[c + 1] & ((1u << kMapTensorBits) - 1)]) & kGrid;
+      k = b_shift >= 0 ? start >> b_shift : start / B;
+    } else {
+      start -= (start - k * B) & kGrid;
+      if (end < S) end -= (end - end / B * B) & kGrid;
+      while (stream_off[g] > start) --g;
+    }
+  }
   uint64_t kend = (k + 1) * B;
   uint64_t pos = start;
   while (pos < end) {
@@ -821,15 +896,18 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
       acc += (s.rank_bytes[r] + B - 1) / B;
     }
     const int32_t b_shift = (B & (B - 1)) == 0 ? __builtin_ctzll(B) : -1;
+    // chunks are cut on the stream's 16-byte grid unless the destination's grid differs: buckets whose
+    // size is not a multiple of 16 (pack), tensors at stream offsets that are not (unpack)
+    const uint32_t realign = unpack ? uint32_t(!s.offsets_grid) : uint32_t(B % kTileChunkBytes != 0);
     const dim3 g(uint32_t(t.n_tiles));  // padded to a multiple of kXcds
     const size_t lds = occupancy_lds(0, kTileChunkBytes, kBucketFlightBytes);
     drop_pending_error();
     if (unpack) {
-      if (ntm) hipLaunchKernelGGL((k_buckets_tile<true, true, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
-      else hipLaunchKernelGGL((k_buckets_tile<true, false, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
+      if (ntm) hipLaunchKernelGGL((k_buckets_tile<true, true, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, realign, tptr, bptr, bases);
+      else hipLaunchKernelGGL((k_buckets_tile<true, false, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, realign, tptr, bptr, bases);
     } else {
-      if (ntm) hipLaunchKernelGGL((k_buckets_tile<false, true, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
-      else hipLaunchKernelGGL((k_buckets_tile<false, false, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, tptr, bptr, bases);
+      if (ntm) hipLaunchKernelGGL((k_buckets_tile<false, true, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, realign, tptr, bptr, bases);
+      else hipLaunchKernelGGL((k_buckets_tile<false, false, kBucketTileVecs>), g, dim3(kBucketTileThreads), lds, st, so, ri, rb, tm, B, b_shift, realign, tptr, bptr, bases);
     }
     return hip_check(unpack ? "emu_unpack_buckets launch" : "emu_pack_buckets launch");
   }

@@ -86,6 +86,7 @@ struct SideInfo {
   int64_t vp = 0;
   int32_t nranks = 0;
   uint64_t total_bytes = 0;
+  bool offsets_grid = true;           // every tensor's stream offset is a multiple of kTileChunkBytes
   std::vector<emu_tensor_desc_t> tensors;
   std::vector<uint32_t> rank_first;   // nranks + 1
   std::vector<uint64_t> rank_bytes;   // nranks

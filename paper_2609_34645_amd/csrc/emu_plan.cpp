@@ -225,10 +225,12 @@ static int build_side(const emu_layout_t& lay, SideInfo& s, std::vector<std::vec
   s.rank_bytes.assign(s.nranks, 0);
   s.chunk_first.assign(s.nranks + 1, 0);
   s.total_bytes = 0;
+  s.offsets_grid = true;
   for (int r = 0; r < s.nranks; ++r) {
     uint64_t off = 0;
     for (uint32_t i = s.rank_first[r]; i < s.rank_first[r + 1]; ++i) {
       s.tensors[i].stream_offset = off;
+      s.offsets_grid = s.offsets_grid && off % kTileChunkBytes == 0;
       off += s.tensors[i].bytes;
     }
     s.rank_bytes[r] = off;
@@ -395,6 +397,7 @@ static int to_buckets(Plan& P, uint64_t B) {
   bk.vp = D.vp;
   bk.nranks = D.nranks;
   bk.total_bytes = D.total_bytes;
+  bk.offsets_grid = B % kTileChunkBytes == 0 || D.nranks == 0;
   bk.rank_first.assign(D.nranks + 1, 0);
   bk.rank_bytes = D.rank_bytes;
   bk.chunk_first.assign(D.nranks + 1, 0);
