@@ -315,27 +315,30 @@ class Plan:
     def upload(self, ws, stream=None):
         check(load().emu_plan_upload(self._h, ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream_handle(stream)))
 
-    def alloc(self, side: int, device=None, fill=None) -> ShardSet:
-        """Allocate one side's shard set (one buffer per rank, 256-byte aligned tensor views)."""
+    def alloc(self, side: int, device=None, fill=None, guard: int = 0) -> ShardSet:
+        """Allocate one side's shard set (one buffer per rank, 256-byte aligned tensor views). With
+        guard > 0, at least that many bytes separate consecutive views and precede the first and follow
+        the last, so that bytes a call must not touch surround every tensor (tests prefill them)."""
         import torch
 
         descs = self.tensors(side)
         nranks = self.info["n_src_ranks" if side == 0 else "n_dst_ranks"]
         offs, sizes = [], [0] * nranks
         for d in descs:
-            o = (sizes[d["rank"]] + 255) // 256 * 256
+            o = (sizes[d["rank"]] + guard + 255) // 256 * 256
             offs.append(o)
             sizes[d["rank"]] = o + d["bytes"]
-        bufs = [torch.empty(max(s, 16), dtype=torch.uint8, device=device or "cuda") for s in sizes]
+        bufs = [torch.empty(max(s + guard, 16), dtype=torch.uint8, device=device or "cuda") for s in sizes]
         if fill is not None:
             for b in bufs:
                 b.fill_(fill)
         tensors = [bufs[d["rank"]][o:o + d["bytes"]] for d, o in zip(descs, offs)]
         return ShardSet(bufs, tensors, ptr_table(tensors, device))
 
-    def alloc_buckets(self, side: int, bucket_bytes: int, device=None, fill=None):
+    def alloc_buckets(self, side: int, bucket_bytes: int, device=None, fill=None, guard: int = 0):
         """Bucket buffers for one side (rank 0's first) and their pointer table. The buckets are
-        256-byte aligned views of one backing allocation."""
+        256-byte aligned views of one backing allocation, separated by at least `guard` bytes (as in
+        ``alloc``)."""
         import torch
 
         nranks = self.info["n_src_ranks" if side == 0 else "n_dst_ranks"]
@@ -345,9 +348,10 @@ class Plan:
             sizes += [min(bucket_bytes, sb - k * bucket_bytes) for k in range(nb)]
         offs, total = [], 0
         for n in sizes:
-            offs.append(total)
-            total = (total + n + 255) // 256 * 256
-        backing = torch.empty(max(total, 256), dtype=torch.uint8, device=device or "cuda")
+            o = (total + guard + 255) // 256 * 256
+            offs.append(o)
+            total = o + n
+        backing = torch.empty(max(total + guard, 256), dtype=torch.uint8, device=device or "cuda")
         if fill is not None:
             backing.fill_(fill)
         bufs = [backing[o:o + n] for o, n in zip(offs, sizes)]

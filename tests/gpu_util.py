@@ -18,6 +18,109 @@ def say(*a):
     sys.stdout.flush()
 
 
+def _backings(views):
+    """Group tensor views by the allocation they live in: {storage ptr: (whole-allocation uint8 tensor,
+    [(byte offset, bytes) of each view])}."""
+    import torch
+
+    out = {}
+    for v in views:
+        st = v.untyped_storage()
+        key = st.data_ptr()
+        if key not in out:
+            whole = torch.empty(0, dtype=torch.uint8, device=v.device).set_(st)
+            out[key] = (whole, [])
+        out[key][1].append((v.data_ptr() - key, v.numel() * v.element_size()))
+    return out
+
+
+def fingerprint(whole):
+    """(sum of the 8-byte words, sum of word * (index + 1), tail bytes) of a uint8 device tensor, the
+    sums modulo 2^64, computed on the device in slices."""
+    import torch
+
+    n8 = whole.numel() // 8 * 8
+    words = whole[:n8].view(torch.int64)
+    acc = torch.zeros(2, dtype=torch.int64, device=whole.device)
+    step = 1 << 25
+    for a in range(0, words.numel(), step):
+        w = words[a:a + step]
+        ramp = torch.arange(a + 1, a + 1 + w.numel(), dtype=torch.int64, device=whole.device)
+        acc[0] += w.sum()
+        acc[1] += (w * ramp).sum()
+    return tuple(acc.cpu().tolist()) + (bytes(whole[n8:].cpu().numpy()),)
+
+
+def _outside(nbytes, spans):
+    """Byte ranges of [0, nbytes) that no span covers."""
+    gaps, pos = [], 0
+    for o, n in sorted(spans):
+        if o > pos:
+            gaps.append((pos, o))
+        pos = max(pos, o + n)
+    if pos < nbytes:
+        gaps.append((pos, nbytes))
+    return gaps
+
+
+class Guard:
+    """The write footprint of one library call, checked around it.
+
+    ``keep``: views the call only reads (its source tensors or buckets). Their whole allocations --
+    views, alignment gaps, guard bands, source pad rows -- must be byte-identical afterwards. The
+    snapshot is a host copy (``snapshot="host"``), a device copy ("device", full-size tests), or for
+    allocations too large to copy twice a device fingerprint ("hash": two 64-bit sums over the 8-byte
+    words, one weighted by position, plus the tail bytes), which any changed word alters.
+    ``fills``: (views, fill byte) pairs of what the call writes, in allocations prefilled with that byte.
+    Every byte of those allocations outside the views must still hold the fill afterwards. Construction
+    checks that the fill is there and that there are such bytes (a check on nothing proves nothing).
+
+    Paper section 5.2 (a)/(b): Split and Merge leave the model state unchanged; section 6.2: each shard
+    travels as one contiguous buffer, so nothing outside a destination shard or bucket is written."""
+
+    def __init__(self, keep=(), fills=(), snapshot="host", label=""):
+        import torch
+
+        assert snapshot in ("host", "device", "hash")
+        self.label = label
+        self.mode = snapshot
+        self.snaps = []
+        for whole, _ in _backings(keep).values():
+            snap = whole.cpu() if snapshot == "host" else whole.clone() if snapshot == "device" else fingerprint(whole)
+            self.snaps.append((whole, snap))
+        self.gaps = []
+        for views, fill in fills:
+            for whole, spans in _backings(views).values():
+                ranges = _outside(whole.numel(), spans)
+                assert ranges, f"{label}: an allocation of written views has no byte outside them"
+                idx = torch.cat([torch.arange(a, b, device=whole.device) for a, b in ranges])
+                got = whole[idx]
+                assert bool((got == fill).all()), f"{label}: prefill {fill:#x} missing before the call"
+                self.gaps.append((whole, idx, fill))
+
+    def check(self):
+        import torch
+
+        for whole, snap in self.snaps:
+            if self.mode == "hash":
+                assert fingerprint(whole) == snap, f"{self.label}: a read-only allocation changed (fingerprint)"
+                continue
+            now = whole if snap.is_cuda else whole.cpu()
+            if not torch.equal(now, snap):
+                bad = torch.nonzero(now != snap).flatten()
+                raise AssertionError(f"{self.label}: {bad.numel()} bytes of a read-only allocation changed, "
+                                     f"first at byte {int(bad[0])}")
+        for whole, idx, fill in self.gaps:
+            got = whole[idx]
+            if not bool((got == fill).all()):
+                bad = idx[got != fill]
+                raise AssertionError(f"{self.label}: {bad.numel()} bytes outside the written views changed, "
+                                     f"first at byte {int(bad[0])} of its allocation")
+        n = sum(idx.numel() for _, idx, _ in self.gaps)
+        self.snaps = []
+        return n
+
+
 def o_layout(lay: emu.Layout) -> oracle.Layout:
     m = lay.model
     om = oracle.Model(m.num_layers, m.hidden, m.num_heads, m.head_dim, m.num_kv_heads, m.ffn_hidden, m.vocab)

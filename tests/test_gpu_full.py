@@ -15,8 +15,13 @@
 * 8B conversions at full size: fp32 TP4 PP1 -> bf16 TP2 PP2 (the weight sync) and bf16 TP2 PP2 -> fp32
   TP4 PP1, each also fused into 2^28-byte buckets; every byte against the oracle.
 * 8B training state, fp32 master + Adam m + v (96 GB in): TP4 PP1 -> TP1 PP1, one launch per tensor
-  group, then split back into the source buffers; master checked in full against the oracle, m and v on
-  sampled tensor groups, the back transition against a seeded regeneration of the original state.
+  group, then split back into the source buffers; master, m and v checked in full against the oracle,
+  the back transition against a seeded regeneration of the original state.
+
+Every call's write footprint is checked as well (tests.gpu_util.Guard): each tensor and bucket view sits
+in a 4 KB guard band of a prefill byte, the call's input allocations must come out byte-identical (device
+snapshots; regeneration from the seed or a device fingerprint for the 96 GB training state), and every
+byte of its output allocations outside the views must still hold the prefill.
 
 Inputs are seeded device draws (synthetic.device_fill); the oracle reads them back as its input.
 """
@@ -28,10 +33,22 @@ import pytest
 
 import oracle
 from paper_2609_34645_amd import emu
-from tests.gpu_util import check_reshard, fill_device, host_view, o_layout, say
+from tests.gpu_util import Guard, check_reshard, fill_device, host_view, o_layout, say
 from tests.shapes import EIGHT_B, HUGE_VOCAB, ONE_B
 
 pytestmark = pytest.mark.gpu
+GUARD = 4096  # bytes of prefilled guard band around every view: one reshard tile
+
+
+def guarded(call, keep, fills, label, snapshot="device"):
+    """Run one library call between a Guard's snapshot and its check."""
+    import torch
+
+    g = Guard(keep=keep, fills=fills, snapshot=snapshot, label=label)
+    call()
+    torch.cuda.synchronize()
+    n = g.check()
+    say(f"  {label}: inputs unchanged, {n} bytes around the outputs untouched")
 
 
 def free_gb():
@@ -68,11 +85,10 @@ def test_1b_tp4_to_tp2(gpu_lib):
     p = emu.Plan(emu.Layout(m, 4, 1), emu.Layout(m, 2, 1))
     assert p.info["bytes_read"] == 2_997_100_544
     ws = p.workspace()
-    S = p.alloc(0)
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
     fill_device(p, 0, S, seed=21)
-    D = p.alloc(1, fill=0xA5)
-    p.reshard(ws, S.ptrs, D.ptrs)
-    torch.cuda.synchronize()
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], "1B reshard")
     check_reshard(p, S, D, label="1B TP4PP1->TP2PP1")
     del S, D, ws
     cleanup()
@@ -86,19 +102,15 @@ def test_8b_tp2pp2_to_tp4pp1(gpu_lib):
     p, back = emu.Plan(src, dst), emu.Plan(dst, src)
     assert p.info["bytes_read"] == 16_062_119_936
     ws, wb = p.workspace(), back.workspace()
-    S = p.alloc(0)
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
     fill_device(p, 0, S, seed=1234)
-    D = p.alloc(1, fill=0xA5)
-    t = time.time()
-    p.reshard(ws, S.ptrs, D.ptrs)
-    torch.cuda.synchronize()
-    say(f"  8B reshard done in {time.time() - t:.3f} s (incl. launch)")
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], "8B reshard")
     check_reshard(p, S, D, label="8B TP2PP2->TP4PP1")
     _pack_check(p, ws, D, 1 << 28, "pack and fused reshard->buckets 2^28 (benchmark workload)", S=S, pack_too=True)
     # Merge back: the round trip reproduces the source; norm replicas of TP rank 1 come back as rank 0's
-    A2 = back.alloc(1, fill=0x5A)
-    back.reshard(wb, D.ptrs, A2.ptrs)
-    torch.cuda.synchronize()
+    A2 = back.alloc(1, fill=0x5A, guard=GUARD)
+    guarded(lambda: back.reshard(wb, D.ptrs, A2.ptrs), D.tensors, [(A2.tensors, 0x5A)], "8B merge back")
     make_consistent_replicas(p, 0, S)
     for i, (x, y) in enumerate(zip(S.tensors, A2.tensors)):
         assert torch.equal(x, y), f"round trip differs in source tensor {i}"
@@ -115,16 +127,15 @@ def _pack_check(p, ws, D, B, label, S=None, pack_too=False):
 
     sets = []
     if S is None or pack_too:
-        bufs, bptrs = p.alloc_buckets(1, B, fill=0x77)
-        p.pack(ws, 1, B, D.ptrs, bptrs)
+        bufs, bptrs = p.alloc_buckets(1, B, fill=0x77, guard=GUARD)
+        guarded(lambda: p.pack(ws, 1, B, D.ptrs, bptrs), D.tensors, [(bufs, 0x77)], f"{label}: pack")
         sets.append(("pack", bufs, bptrs))
     if S is not None:
-        bufs, bptrs = p.alloc_buckets(1, B, fill=0x33)
+        bufs, bptrs = p.alloc_buckets(1, B, fill=0x33, guard=GUARD)
         fused = emu.Plan(p.src, p.dst, bucket_bytes=B)
         wf = fused.workspace()
-        fused.reshard(wf, S.ptrs, bptrs)
+        guarded(lambda: fused.reshard(wf, S.ptrs, bptrs), S.tensors, [(bufs, 0x33)], f"{label}: fused")
         sets.append(("fused", bufs, bptrs))
-    torch.cuda.synchronize()
     dd = p.tensors(1)
     k = 0
     t = time.time()
@@ -139,10 +150,9 @@ def _pack_check(p, ws, D, B, label, S=None, pack_too=False):
     for _, bufs, _ in sets:
         assert k == len(bufs)
     say(f"  {label}: {k} buckets x {len(sets)} checked against the oracle in {time.time() - t:.1f} s")
-    bptrs = sets[0][2]
-    R = p.alloc(1, fill=0x11)
-    p.unpack(ws, 1, B, bptrs, R.ptrs)
-    torch.cuda.synchronize()
+    bufs, bptrs = sets[0][1], sets[0][2]
+    R = p.alloc(1, fill=0x11, guard=GUARD)
+    guarded(lambda: p.unpack(ws, 1, B, bptrs, R.ptrs), bufs, [(R.tensors, 0x11)], f"{label}: unpack")
     for i, (x, y) in enumerate(zip(D.tensors, R.tensors)):
         assert torch.equal(x, y), f"{label}: unpacked tensor {i} differs"
     del R, sets, bufs, bptrs
@@ -159,11 +169,10 @@ def test_8b_weight_sync_fp32_tp4_to_bf16_tp2pp2(gpu_lib):
     p = emu.Plan(src, dst)
     assert p.info["converts"] == 1 and p.info["bytes_read"] == 2 * p.info["bytes_written"]
     ws = p.workspace()
-    S = p.alloc(0)
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
     fill_device(p, 0, S, seed=404, dtype="fp32")
-    D = p.alloc(1, fill=0xA5)
-    p.reshard(ws, S.ptrs, D.ptrs)
-    torch.cuda.synchronize()
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], "8B fp32 -> bf16 reshard")
     check_reshard(p, S, D, label="8B fp32 TP4PP1 -> bf16 TP2PP2")
     _pack_check(p, ws, D, 1 << 28, "fused fp32 -> bf16 buckets 2^28", S=S)
     del S, D, ws
@@ -181,11 +190,10 @@ def test_8b_bf16_tp2pp2_to_fp32_tp4pp1(gpu_lib):
     p = emu.Plan(src, dst)
     assert p.info["converts"] == 2 and 2 * p.info["bytes_read"] == p.info["bytes_written"]
     ws = p.workspace()
-    S = p.alloc(0)
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
     fill_device(p, 0, S, seed=405, dtype="bf16")
-    D = p.alloc(1, fill=0xA5)
-    p.reshard(ws, S.ptrs, D.ptrs)
-    torch.cuda.synchronize()
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], "8B bf16 -> fp32 reshard")
     check_reshard(p, S, D, label="8B bf16 TP2PP2 -> fp32 TP4PP1")
     _pack_check(p, ws, D, 1 << 28, "fused bf16 -> fp32 buckets 2^28", S=S)
     del S, D, ws
@@ -209,11 +217,10 @@ def test_8b_non_default_launch_options(gpu_lib, opts):
         m = emu.Model(*EIGHT_B)
         p = emu.Plan(emu.Layout(m, 2, 2), emu.Layout(m, 4, 1))
         ws = p.workspace()
-        S = p.alloc(0)
+        S = p.alloc(0, fill=0x5A, guard=GUARD)
         fill_device(p, 0, S, seed=77)
-        D = p.alloc(1, fill=0xA5)
-        p.reshard(ws, S.ptrs, D.ptrs)
-        torch.cuda.synchronize()
+        D = p.alloc(1, fill=0xA5, guard=GUARD)
+        guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], f"8B reshard with {opts}")
         check_reshard(p, S, D, groups=["embed", 0, 1, 31, "final"], label=f"8B with {opts}")
         del S, D, ws
         cleanup()
@@ -229,11 +236,10 @@ def test_8b_kv_replication_uneven_pp(gpu_lib):
     m = emu.Model(*EIGHT_B)
     p = emu.Plan(emu.Layout(m, 2, 2), emu.Layout(m, 16, 3))
     ws = p.workspace()
-    S = p.alloc(0)
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
     fill_device(p, 0, S, seed=616)
-    D = p.alloc(1, fill=0xA5)
-    p.reshard(ws, S.ptrs, D.ptrs)
-    torch.cuda.synchronize()
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], "8B TP2PP2 -> TP16PP3 reshard")
     check_reshard(p, S, D, label="8B TP2PP2 -> TP16PP3")
     del S, D, ws
     cleanup()
@@ -247,11 +253,10 @@ def test_8b_padded_tp8pp4_to_tp2pp2_buckets(gpu_lib):
     assert p.info["src_vocab_padded"] == 129024 and p.info["dst_vocab_padded"] == 128256
     assert p.bucket_layout(1, 1 << 28, -1) == (60, 16_061_054_976)
     ws = p.workspace()
-    S = p.alloc(0)
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
     fill_device(p, 0, S, seed=55)    # source pad rows hold random values: they must never be read
-    D = p.alloc(1, fill=0xA5)
-    p.reshard(ws, S.ptrs, D.ptrs)
-    torch.cuda.synchronize()
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], "8B padded reshard")
     check_reshard(p, S, D, label="8B TP8PP4(pad)->TP2PP2")
     _pack_check(p, ws, D, 1 << 28, "buckets 2^28")
     _pack_check(p, ws, D, (1 << 28) - 2, "buckets 2^28-2 (phase-shifted)")
@@ -277,30 +282,36 @@ def test_tensors_over_4gib(gpu_lib):
     p = emu.Plan(a, b)
     assert max(d["bytes"] for d in p.tensors(1)) > 1 << 32
     ws = p.workspace()
-    S = p.alloc(0)
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
     fill_device(p, 0, S, seed=606, dtype="fp32")
-    D = p.alloc(1, fill=0xA5)
-    say("  huge vocab: fp32 TP1 -> TP2")
-    p.reshard(ws, S.ptrs, D.ptrs)
-    torch.cuda.synchronize()
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], "huge vocab fp32 TP1 -> TP2")
     check_reshard(p, S, D, label="huge vocab fp32 TP1 PP1 -> TP2 PP1")
     del S
     cleanup()
     _pack_check(p, ws, D, 1 << 30, "huge vocab buckets 2^30")
     q = emu.Plan(b, c)
     wq = q.workspace()
-    E = q.alloc(1, fill=0x5A)
-    say("  huge vocab: fp32 TP2 -> bf16 TP1")
-    q.reshard(wq, D.ptrs, E.ptrs)
-    torch.cuda.synchronize()
+    E = q.alloc(1, fill=0x5A, guard=GUARD)
+    guarded(lambda: q.reshard(wq, D.ptrs, E.ptrs), D.tensors, [(E.tensors, 0x5A)], "huge vocab fp32 TP2 -> bf16 TP1")
     check_reshard(q, D, E, label="huge vocab fp32 TP2 PP1 -> bf16 TP1 PP1")
     del D, E, ws, wq
     cleanup()
 
 
+def regenerate(fwd, name, dist, seed):
+    """The training-state group `name` as the fixture made it, in a fresh, identically laid out set."""
+    ref = fwd.alloc(0, fill=0x5A, guard=GUARD)
+    fill_device(fwd, 0, ref, seed=seed, dtype="fp32", dist_override=None if name == "master" else dist)
+    make_consistent_replicas(fwd, 0, ref)
+    return ref
+
+
 @pytest.fixture(scope="module")
 def train_state(gpu_lib):
-    """fp32 master, Adam m and v in the TP4 PP1 layout, resharded to TP1 PP1 with one launch per group."""
+    """fp32 master, Adam m and v in the TP4 PP1 layout, resharded to TP1 PP1 with one launch per group.
+    The sources must come out of the three launches unchanged (whole allocations, against a seeded
+    regeneration) and the destination allocations untouched outside their views."""
     import torch
 
     need = 2 * 96.4 + 33
@@ -314,16 +325,22 @@ def train_state(gpu_lib):
     S, D = {}, {}
     t = time.time()
     for name, (dist, seed) in groups.items():
-        S[name] = fwd.alloc(0)
-        fill_device(fwd, 0, S[name], seed=seed, dtype="fp32",
-                    dist_override=None if name == "master" else dist)
-        make_consistent_replicas(fwd, 0, S[name])
-        D[name] = fwd.alloc(1, fill=0xA5)
+        S[name] = regenerate(fwd, name, dist, seed)
+        D[name] = fwd.alloc(1, fill=0xA5, guard=GUARD)
     torch.cuda.synchronize()
     say(f"  fp32 state filled ({3 * fwd.info['src_bytes'] / 1e9:.1f} GB) in {time.time() - t:.1f} s")
+    guards = [Guard(fills=[(D[name].tensors, 0xA5)], label=f"fp32 {name} TP4->TP1") for name in groups]
     for name in groups:
         fwd.reshard(wf, S[name].ptrs, D[name].ptrs)     # one launch per tensor group
     torch.cuda.synchronize()
+    n = sum(g.check() for g in guards)
+    for name, (dist, seed) in groups.items():
+        ref = regenerate(fwd, name, dist, seed)
+        for r, (x, y) in enumerate(zip(ref.bufs, S[name].bufs)):
+            assert torch.equal(x, y), f"{name}: source buffer of rank {r} changed by the forward reshard"
+        del ref
+        cleanup()
+    say(f"  fp32 state TP4->TP1: sources unchanged, {n} bytes around the destinations untouched")
     yield dict(fwd=fwd, back=back, wf=wf, wb=wb, S=S, D=D, groups=groups)
     S.clear()
     D.clear()
@@ -336,28 +353,32 @@ def test_8b_fp32_master_full(train_state):
     check_reshard(st["fwd"], st["S"]["master"], st["D"]["master"], label="fp32 master TP4->TP1")
 
 
-def test_8b_fp32_adam_sampled_groups(train_state):
+@pytest.mark.parametrize("name", ["adam_m", "adam_v"])
+def test_8b_fp32_adam_full(train_state, name):
     st = train_state
-    for name in ("adam_m", "adam_v"):
-        check_reshard(st["fwd"], st["S"][name], st["D"][name], groups=["embed", 0, 17, 31, "final"],
-                      label=f"fp32 {name} TP4->TP1 (sampled groups)")
+    check_reshard(st["fwd"], st["S"][name], st["D"][name], label=f"fp32 {name} TP4->TP1")
 
 
 def test_8b_fp32_split_back_in_place(train_state):
+    """Split back into the original source buffers, one launch per group: the destination sets (read
+    only) keep their device fingerprint, the bytes around the rewritten source views keep their
+    prefill, and every source allocation equals a seeded regeneration of the original state."""
     import torch
 
     st = train_state
     fwd, back = st["fwd"], st["back"]
     assert back.info["bytes_read"] * 3 == 96_372_719_616
+    guards = [Guard(keep=st["D"][name].tensors, fills=[(st["S"][name].tensors, 0x5A)], snapshot="hash",
+                    label=f"fp32 {name} TP1->TP4") for name in st["groups"]]
     for name in st["groups"]:
         back.reshard(st["wb"], st["D"][name].ptrs, st["S"][name].ptrs)   # into the original source buffers
     torch.cuda.synchronize()
+    for g in guards:
+        g.check()
     for name, (dist, seed) in st["groups"].items():
-        ref = fwd.alloc(0)
-        fill_device(fwd, 0, ref, seed=seed, dtype="fp32", dist_override=None if name == "master" else dist)
-        make_consistent_replicas(fwd, 0, ref)
-        for i, (x, y) in enumerate(zip(ref.tensors, st["S"][name].tensors)):
-            assert torch.equal(x, y), f"{name}: tensor {i} differs after the round trip"
+        ref = regenerate(fwd, name, dist, seed)
+        for r, (x, y) in enumerate(zip(ref.bufs, st["S"][name].bufs)):
+            assert torch.equal(x, y), f"{name}: buffer of rank {r} differs after the round trip"
         del ref
         cleanup()
     say("  fp32 training state round trip TP4->TP1->TP4 bit-exact")

@@ -13,7 +13,8 @@ import pytest
 
 import oracle
 from paper_2609_34645_amd import emu
-from tests.gpu_util import (check_buckets, check_reshard, full_model, host_view, o_layout, say, upload_shards)
+from tests.gpu_util import (Guard, check_buckets, check_reshard, full_model, host_view, o_layout, say,
+                             upload_shards)
 from tests.shapes import MICRO, MICRO8, TINY
 
 pytestmark = pytest.mark.gpu
@@ -21,7 +22,12 @@ pytestmark = pytest.mark.gpu
 FORMATS = [("interleaved", "block"), ("separate", "separate"), ("interleaved", "separate")]
 
 
+GUARD = 48  # bytes of prefilled guard band around every tensor and bucket view
+
+
 def run_pair(src, dst, seed=5, options=None, bucket_sizes=(), fused=False):
+    """Reshard (and pack / unpack / fused plan) one layout pair on seeded oracle shards; every output
+    byte against the oracle, and every call's write footprint checked (Guard)."""
     import torch
 
     for k, v in (options or {}).items():
@@ -29,20 +35,28 @@ def run_pair(src, dst, seed=5, options=None, bucket_sizes=(), fused=False):
     plan = emu.Plan(src, dst)
     os_ = o_layout(src)
     ws = plan.workspace()
-    S = plan.alloc(0, fill=0x5A)
-    D = plan.alloc(1, fill=0xA5)
+    S = plan.alloc(0, fill=0x5A, guard=GUARD)
+    D = plan.alloc(1, fill=0xA5, guard=GUARD)
     plan.check_tables(S.ptrs, D.ptrs)
     upload_shards(oracle.shard(full_model(os_.model, seed, src.dtype), os_), S, tp=src.tp)
+    label = f"{src.tp}x{src.pp}->{dst.tp}x{dst.pp}"
+    g = Guard(keep=S.tensors, fills=[(D.tensors, 0xA5)], label=f"reshard {label}")
     plan.reshard(ws, S.ptrs, D.ptrs)
     torch.cuda.synchronize()
-    check_reshard(plan, S, D, label=f"{src.tp}x{src.pp}->{dst.tp}x{dst.pp}")
+    g.check()
+    check_reshard(plan, S, D, label=label)
     for B in bucket_sizes:
-        bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77)
+        bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77, guard=GUARD)
         plan.check_bucket_tables(1, B, D.ptrs, bptrs)
+        g = Guard(keep=D.tensors, fills=[(bufs, 0x77)], label=f"pack B={B} {label}")
         plan.pack(ws, 1, B, D.ptrs, bptrs)
-        R = plan.alloc(1, fill=0x11)
+        torch.cuda.synchronize()
+        g.check()
+        R = plan.alloc(1, fill=0x11, guard=GUARD)
+        g = Guard(keep=bufs, fills=[(R.tensors, 0x11)], label=f"unpack B={B} {label}")
         plan.unpack(ws, 1, B, bptrs, R.ptrs)
         torch.cuda.synchronize()
+        g.check()
         dd = plan.tensors(1)
         ranks = {}
         for i, d in enumerate(dd):
@@ -53,10 +67,12 @@ def run_pair(src, dst, seed=5, options=None, bucket_sizes=(), fused=False):
         if fused:  # source shards straight into buckets: the same buckets as reshard + pack
             fp = emu.Plan(src, dst, bucket_bytes=B)
             fws = fp.workspace()
-            fbufs, fbptrs = plan.alloc_buckets(1, B, fill=0x33)
+            fbufs, fbptrs = plan.alloc_buckets(1, B, fill=0x33, guard=GUARD)
             fp.check_tables(S.ptrs, fbptrs)
+            g = Guard(keep=S.tensors, fills=[(fbufs, 0x33)], label=f"fused B={B} {label}")
             fp.reshard(fws, S.ptrs, fbptrs)
             torch.cuda.synchronize()
+            g.check()
             for k, (a, b) in enumerate(zip(bufs, fbufs)):
                 assert torch.equal(a, b), f"fused bucket {k} differs (B={B})"
     return plan
@@ -137,13 +153,15 @@ def test_t_sub_paper_example_micro8(gpu_lib):
     a, b, c = emu.Layout(m, 4, 8), emu.Layout(m, 4, 2), emu.Layout(m, 8, 2)
     pab, pbc, pac = emu.Plan(a, b), emu.Plan(b, c), emu.Plan(a, c)
     wab, wbc, wac = pab.workspace(), pbc.workspace(), pac.workspace()
-    A = pab.alloc(0)
+    A = pab.alloc(0, fill=0x5A, guard=GUARD)
     upload_shards(oracle.shard(full_model(o_layout(a).model, 3), o_layout(a)), A, tp=4)
-    B, C1, C2 = pab.alloc(1), pbc.alloc(1), pac.alloc(1)
-    pab.reshard(wab, A.ptrs, B.ptrs)
-    pbc.reshard(wbc, B.ptrs, C1.ptrs)
-    pac.reshard(wac, A.ptrs, C2.ptrs)
-    torch.cuda.synchronize()
+    B, C1, C2 = (pab.alloc(1, fill=0xA5, guard=GUARD), pbc.alloc(1, fill=0xA5, guard=GUARD),
+                 pac.alloc(1, fill=0xA5, guard=GUARD))
+    for p, w, x, y in ((pab, wab, A, B), (pbc, wbc, B, C1), (pac, wac, A, C2)):
+        g = Guard(keep=x.tensors, fills=[(y.tensors, 0xA5)], label="T_sub route")
+        p.reshard(w, x.ptrs, y.ptrs)
+        torch.cuda.synchronize()
+        g.check()
     for x, y in zip(C1.tensors, C2.tensors):
         assert torch.equal(x, y)
     check_reshard(pac, A, C2, label="TP4PP8->TP8PP2")
@@ -158,12 +176,14 @@ def test_tiny_split_and_merge_back(gpu_lib):
     fwd, back = emu.Plan(a, b), emu.Plan(b, a)
     assert fwd.info["bytes_read"] == 3_953_664 and back.info["bytes_read"] == 3_951_104
     wf, wb = fwd.workspace(), back.workspace()
-    A = fwd.alloc(0)
+    A = fwd.alloc(0, fill=0x5A, guard=GUARD)
     upload_shards(oracle.shard(full_model(o_layout(a).model, 1), o_layout(a)), A)
-    B, A2 = fwd.alloc(1, fill=0xA5), back.alloc(1, fill=0xA5)
-    fwd.reshard(wf, A.ptrs, B.ptrs)
-    back.reshard(wb, B.ptrs, A2.ptrs)
-    torch.cuda.synchronize()
+    B, A2 = fwd.alloc(1, fill=0xA5, guard=GUARD), back.alloc(1, fill=0xA5, guard=GUARD)
+    for p, w, x, y in ((fwd, wf, A, B), (back, wb, B, A2)):
+        g = Guard(keep=x.tensors, fills=[(y.tensors, 0xA5)], label="tiny split / merge")
+        p.reshard(w, x.ptrs, y.ptrs)
+        torch.cuda.synchronize()
+        g.check()
     check_reshard(fwd, A, B, label="tiny TP1->TP2")
     check_reshard(back, B, A2, label="tiny TP2->TP1")
     for x, y in zip(A.tensors, A2.tensors):
@@ -182,9 +202,9 @@ def test_tiny_transition_in_a_hip_graph(gpu_lib):
     plan = emu.Plan(a, b)
     ws = plan.workspace()
     B = 1 << 16
-    S = plan.alloc(0)
-    D, R = plan.alloc(1, fill=0xA5), plan.alloc(1, fill=0x5A)
-    bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77)
+    S = plan.alloc(0, fill=0x3C, guard=GUARD)
+    D, R = plan.alloc(1, fill=0xA5, guard=GUARD), plan.alloc(1, fill=0x5A, guard=GUARD)
+    bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77, guard=GUARD)
     torch.cuda.synchronize()
     stream = torch.cuda.Stream()
     graph = torch.cuda.CUDAGraph()
@@ -198,8 +218,11 @@ def test_tiny_transition_in_a_hip_graph(gpu_lib):
         for t in D.bufs + R.bufs:
             t.fill_(replay + 1)
         torch.cuda.synchronize()
+        g = Guard(keep=S.tensors, fills=[(D.tensors, replay + 1), (bufs, 0x77), (R.tensors, replay + 1)],
+                  label=f"graph replay {replay}")
         graph.replay()
         torch.cuda.synchronize()
+        g.check()
         check_reshard(plan, S, D, label=f"graph replay {replay}")
         dd = plan.tensors(1)
         ranks = {}
@@ -243,20 +266,24 @@ def test_padded_vocab_zero_fill_and_source_pad_not_read(gpu_lib):
     p = emu.Plan(a, b)
     assert p.info["zero_fill_bytes"] == 2 * 24 * 256 * 2
     ws = p.workspace()
-    S = p.alloc(0)
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
     upload_shards(oracle.shard(full_model(o_layout(a).model, 9), o_layout(a)), S, tp=2)
-    D = p.alloc(1, fill=0xA5)
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    g = Guard(keep=S.tensors, fills=[(D.tensors, 0xA5)], label="pad 0 -> pad 128")
     p.reshard(ws, S.ptrs, D.ptrs)
     torch.cuda.synchronize()
+    g.check()
     check_reshard(p, S, D, label="pad 0 -> pad 128")
     back = emu.Plan(b, a)
     wb = back.workspace()
     for t, d in zip(D.tensors, back.tensors(0)):
         if d["kind"] in ("embed", "lm_head") and d["rank"] % 2 == 1:
             t.view(-1)[-24 * 256 * 2:] = 0xEE      # garbage in the source pad rows
-    A2 = back.alloc(1, fill=0xA5)
+    A2 = back.alloc(1, fill=0xA5, guard=GUARD)
+    g = Guard(keep=D.tensors, fills=[(A2.tensors, 0xA5)], label="pad 128 -> pad 0")
     back.reshard(wb, D.ptrs, A2.ptrs)
     torch.cuda.synchronize()
+    g.check()
     check_reshard(back, D, A2, label="pad 128 -> pad 0")
     for x, y, d in zip(S.tensors, A2.tensors, p.tensors(0)):
         if not (d["kind"].endswith("norm") and d["rank"] % 2):   # TP-rank-1 replicas were altered on upload
@@ -312,14 +339,19 @@ def test_buckets_source_side_and_fp32(gpu_lib):
     a, b = emu.Layout(m, 2, 2, 0, "fp32"), emu.Layout(m, 1, 1, 0, "fp32")
     p = emu.Plan(a, b)
     ws = p.workspace()
-    S = p.alloc(0)
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
     upload_shards(oracle.shard(full_model(o_layout(a).model, 4, "fp32"), o_layout(a)), S, tp=2)
     for B in (4, 1 << 16, 12345 * 4):
-        bufs, bptrs = p.alloc_buckets(0, B)
+        bufs, bptrs = p.alloc_buckets(0, B, fill=0x77, guard=GUARD)
+        g = Guard(keep=S.tensors, fills=[(bufs, 0x77)], label=f"source-side pack B={B}")
         p.pack(ws, 0, B, S.ptrs, bptrs)
-        R = p.alloc(0, fill=0)
+        torch.cuda.synchronize()
+        g.check()
+        R = p.alloc(0, fill=0, guard=GUARD)
+        g = Guard(keep=bufs, fills=[(R.tensors, 0)], label=f"source-side unpack B={B}")
         p.unpack(ws, 0, B, bptrs, R.ptrs)
         torch.cuda.synchronize()
+        g.check()
         sd = p.tensors(0)
         ranks = {}
         for i, d in enumerate(sd):
@@ -392,24 +424,31 @@ def test_pending_hip_error_is_not_reported(gpu_lib):
     src, dst = emu.Layout(m, 1, 1), emu.Layout(m, 2, 1)
     plan = emu.Plan(src, dst)
     ws = plan.workspace()
-    S, D = plan.alloc(0, fill=0x5A), plan.alloc(1, fill=0xA5)
+    S, D = plan.alloc(0, fill=0x5A, guard=GUARD), plan.alloc(1, fill=0xA5, guard=GUARD)
     os_ = o_layout(src)
     upload_shards(oracle.shard(full_model(os_.model, 9, "bf16"), os_), S, tp=1)
     torch.cuda.synchronize()
+    g = Guard(keep=S.tensors, fills=[(D.tensors, 0xA5)], label="reshard after a pending error")
     leave_error()
     plan.reshard(ws, S.ptrs, D.ptrs)
     assert hip.hipPeekAtLastError() == 0
     torch.cuda.synchronize()
+    g.check()
     check_reshard(plan, S, D, label="after a pending error")
     B = 12288
-    bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77)
-    R = plan.alloc(1, fill=0x11)
+    bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77, guard=GUARD)
+    R = plan.alloc(1, fill=0x11, guard=GUARD)
+    g = Guard(keep=D.tensors, fills=[(bufs, 0x77)], label="pack after a pending error")
     leave_error()
     plan.pack(ws, 1, B, D.ptrs, bptrs)
+    torch.cuda.synchronize()
+    g.check()
+    g = Guard(keep=bufs, fills=[(R.tensors, 0x11)], label="unpack after a pending error")
     leave_error()
     plan.unpack(ws, 1, B, bptrs, R.ptrs)
     assert hip.hipPeekAtLastError() == 0
     torch.cuda.synchronize()
+    g.check()
     for a, b in zip(D.tensors, R.tensors):
         assert torch.equal(a, b)
 
@@ -430,13 +469,18 @@ def test_fused_reshard_to_buckets(gpu_lib, B):
         fused, base = emu.Plan(src, dst, bucket_bytes=B), emu.Plan(src, dst)
         wf, wb = fused.workspace(), base.workspace()
         os_, od = o_layout(src), o_layout(dst)
-        S = base.alloc(0)
+        S = base.alloc(0, fill=0x5A, guard=GUARD)
         upload_shards(oracle.shard(full_model(os_.model, 8, src.dtype), os_), S, tp=src.tp)
-        K = fused.alloc(1, fill=0x77)          # side 1 of the fused plan = the buckets
+        K = fused.alloc(1, fill=0x77, guard=GUARD)          # side 1 of the fused plan = the buckets
+        g = Guard(keep=S.tensors, fills=[(K.tensors, 0x77)], label=f"fused B={B}")
         fused.reshard(wf, S.ptrs, K.ptrs)
-        R = base.alloc(1, fill=0x11)
+        torch.cuda.synchronize()
+        g.check()
+        R = base.alloc(1, fill=0x11, guard=GUARD)
+        g = Guard(keep=K.tensors, fills=[(R.tensors, 0x11)], label=f"unpack of fused buckets B={B}")
         base.unpack(wb, 1, B, K.ptrs, R.ptrs)
         torch.cuda.synchronize()
+        g.check()
         sd = base.tensors(0)
         ranks_src = {}
         for i, d in enumerate(sd):
@@ -490,7 +534,7 @@ def test_fp32_to_bf16_special_values(gpu_lib):
     src, dst = emu.Layout(m, 1, 1, 0, "fp32"), emu.Layout(m, 2, 1, 0, "bf16")
     p = emu.Plan(src, dst)
     ws = p.workspace()
-    S = p.alloc(0)
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
     rng = np.random.default_rng(77)
     specials = np.array([0x3F808000, 0x3F818000, 0x7F7F8000, 0x7F7FFFFF, 0x7F800000, 0xFF800000, 0x7FC00000,
                          0x7F800001, 0xFFA00000, 0x80000000, 0x00000001, 0x00008000, 0x00018000, 0x007FFFFF],
@@ -499,9 +543,11 @@ def test_fp32_to_bf16_special_values(gpu_lib):
         u = rng.integers(0, 1 << 32, size=t.numel() // 4, dtype=np.uint64).astype(np.uint32)
         u[:specials.size] = specials[:u.size]
         t.copy_(torch.from_numpy(u.view(np.uint8)))
-    D = p.alloc(1, fill=0xA5)
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    g = Guard(keep=S.tensors, fills=[(D.tensors, 0xA5)], label="fp32 bit patterns -> bf16")
     p.reshard(ws, S.ptrs, D.ptrs)
     torch.cuda.synchronize()
+    g.check()
     check_reshard(p, S, D, label="fp32 bit patterns -> bf16")
 
 
@@ -568,20 +614,25 @@ def test_tensors_at_16_byte_offsets(gpu_lib, pair):
     plan.check_tables(S.ptrs, D.ptrs)
     os_ = o_layout(src)
     upload_shards(oracle.shard(full_model(os_.model, 23, src.dtype), os_), S, tp=src.tp)
-    plan.reshard(ws, S.ptrs, D.ptrs)
-    torch.cuda.synchronize()
+
+    def guarded(call, keep, fills, label):
+        g = Guard(keep=keep, fills=fills, label=f"16-byte offsets {pair}: {label}")
+        call()
+        torch.cuda.synchronize()
+        g.check()
+
+    guarded(lambda: plan.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], "reshard")
     check_reshard(plan, S, D, label=f"16-byte offsets {pair}")
     B = 6000 if pair[1] == "bf16" else 6004
     bufs, bptrs = _scattered_buckets(plan, 1, B, rng, 0x77)
     plan.check_bucket_tables(1, B, D.ptrs, bptrs)
-    plan.pack(ws, 1, B, D.ptrs, bptrs)
+    guarded(lambda: plan.pack(ws, 1, B, D.ptrs, bptrs), D.tensors, [(bufs, 0x77)], "pack")
     R = _scattered(plan, 1, rng, 0x11)
-    plan.unpack(ws, 1, B, bptrs, R.ptrs)
+    guarded(lambda: plan.unpack(ws, 1, B, bptrs, R.ptrs), bufs, [(R.tensors, 0x11)], "unpack")
     fused = emu.Plan(src, dst, bucket_bytes=B)
     fws = fused.workspace()
     fbufs, fbptrs = _scattered_buckets(plan, 1, B, rng, 0x33)
-    fused.reshard(fws, S.ptrs, fbptrs)
-    torch.cuda.synchronize()
+    guarded(lambda: fused.reshard(fws, S.ptrs, fbptrs), S.tensors, [(fbufs, 0x33)], "fused")
     dd = plan.tensors(1)
     ranks = {}
     for i, d in enumerate(dd):

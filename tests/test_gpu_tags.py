@@ -7,7 +7,9 @@ values are common in bf16) could hide.
   top bit set, and source pad rows carry an all-ones sentinel: neither may ever reach the output;
 * expected destination: id + 1 everywhere, zero in destination pad rows;
 * buckets: each destination rank's tags concatenated and cut every B bytes, from pack and from the fused
-  source -> bucket plan; unpack restores the destination tensors.
+  source -> bucket plan; unpack restores the destination tensors;
+* every call leaves its inputs' allocations byte-identical and the bytes around its outputs' views
+  (alignment gaps, guard bands, short buckets' tails) at their prefill.
 
 Micro-model layouts, in bf16 (16-bit tags; the models have fewer than 2^15 elements) and fp32 (32-bit tags).
 """
@@ -20,11 +22,12 @@ import pytest
 import oracle
 from oracle import coords
 from paper_2609_34645_amd import emu
-from tests.gpu_util import o_layout, say, upload_shards
+from tests.gpu_util import Guard, o_layout, say, upload_shards
 from tests.shapes import MICRO
 
 pytestmark = pytest.mark.gpu
 
+GUARD = 48  # bytes of prefilled guard band around every tensor and bucket view
 MICRO_KV = (3, 16, 8, 2, 2, 16, 16)  # KV replication up to TP8 over 2 KV heads, uneven stages at PP2
 FORMATS = [("interleaved", "block"), ("separate", "separate"), ("interleaved", "separate"), ("separate", "block")]
 TAG = {"bf16": (np.uint16, 0x8000, 0xFFFF), "fp32": (np.uint32, 0x8000_0000, 0xFFFF_FFFF)}
@@ -66,27 +69,32 @@ def run_tagged(src, dst, B):
 
     plan = emu.Plan(src, dst)
     ws = plan.workspace()
-    S, D = plan.alloc(0, fill=0x5A), plan.alloc(1, fill=0xA5)
+    S, D = plan.alloc(0, fill=0x5A, guard=GUARD), plan.alloc(1, fill=0xA5, guard=GUARD)
     upload_shards(tags(src, True), S, tweak_replicas=False)
-    plan.reshard(ws, S.ptrs, D.ptrs)
-    torch.cuda.synchronize()
+    label = f"{src} -> {dst}"
+
+    def guarded(call, keep, fills, what):
+        g = Guard(keep=keep, fills=fills, label=f"{label}: {what}")
+        call()
+        torch.cuda.synchronize()
+        g.check()
+
+    guarded(lambda: plan.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], "reshard")
     want = tags(dst, False)
     flat = [a for rank in want for a in rank]
-    label = f"{src} -> {dst}"
     for i, (t, w) in enumerate(zip(D.tensors, flat)):
         assert np.array_equal(host_bytes(t), w.reshape(-1).view(np.uint8)), f"{label}: destination tensor {i}"
     # buckets: each rank's stream cut every B bytes, from pack and from the fused plan
     streams = [np.concatenate([a.reshape(-1).view(np.uint8) for a in rank]) for rank in want]
     expect = [s[k:k + B] for s in streams for k in range(0, len(s), B)]
-    bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77)
-    plan.pack(ws, 1, B, D.ptrs, bptrs)
-    R = plan.alloc(1, fill=0x11)
-    plan.unpack(ws, 1, B, bptrs, R.ptrs)
+    bufs, bptrs = plan.alloc_buckets(1, B, fill=0x77, guard=GUARD)
+    guarded(lambda: plan.pack(ws, 1, B, D.ptrs, bptrs), D.tensors, [(bufs, 0x77)], f"pack B={B}")
+    R = plan.alloc(1, fill=0x11, guard=GUARD)
+    guarded(lambda: plan.unpack(ws, 1, B, bptrs, R.ptrs), bufs, [(R.tensors, 0x11)], f"unpack B={B}")
     fused = emu.Plan(src, dst, bucket_bytes=B)
     fws = fused.workspace()
-    fbufs, fbptrs = plan.alloc_buckets(1, B, fill=0x33)
-    fused.reshard(fws, S.ptrs, fbptrs)
-    torch.cuda.synchronize()
+    fbufs, fbptrs = plan.alloc_buckets(1, B, fill=0x33, guard=GUARD)
+    guarded(lambda: fused.reshard(fws, S.ptrs, fbptrs), S.tensors, [(fbufs, 0x33)], f"fused B={B}")
     assert len(bufs) == len(expect) == len(fbufs)
     for k, (b, f, e) in enumerate(zip(bufs, fbufs, expect)):
         assert np.array_equal(host_bytes(b), e), f"{label}: bucket {k} (B={B})"
