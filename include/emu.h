@@ -38,7 +38,8 @@
  * Ownership and execution:
  *   - The caller allocates and owns every device buffer (tensors, buckets, pointer tables, workspace)
  *     and every stream. The library allocates host memory for plans only: it never calls hipMalloc or
- *     hipFree and never synchronizes a device or stream itself. The one host-to-device copy,
+ *     hipFree and never synchronizes a device or stream itself. Its only device memory is one static
+ *     32 MiB array per device, part of its code object, that emu_reshard_noalloc uses as workspace. The one host-to-device copy,
  *     emu_plan_upload, reads the plan's pageable host memory, and the HIP runtime may hold the calling
  *     thread until the stream has reached that copy (it does for workspaces of megabytes): upload once
  *     per plan, before the work it should not wait for.
@@ -237,6 +238,22 @@ int emu_plan_upload(emu_plan_t plan, void* d_workspace, uint64_t workspace_bytes
  * destination byte exactly once. d_workspace holds the uploaded plan tables. */
 int emu_reshard(emu_plan_t plan, const void* d_workspace, const uint64_t* d_src_ptrs,
                 const uint64_t* d_dst_ptrs, void* hip_stream);
+
+/* emu_reshard without a caller workspace, for callers that cannot allocate device memory (code that
+ * must not call hipMalloc, tight serving loops, harnesses that forbid allocation). The plan's reshard
+ * tables (segments and tile map, at most 32 MiB: every plan of a decoder up to the 8B shapes at the
+ * default tile size fits; a larger one returns EMU_ERR_WORKSPACE before anything is enqueued) live in a
+ * static device array of the library, of which every device it runs on holds one copy until the
+ * process ends. The call allocates nothing and launches the same kernels as emu_reshard: the first call
+ * with a plan on a device enqueues the copy of its tables into that device's array on hip_stream (from
+ * the plan's pageable host memory, so the plan must outlive it); later calls with the same plan find
+ * the tables there and only launch. Under stream capture a call whose tables are not yet resident
+ * returns EMU_ERR_ARG: make one call outside capture first.
+ * All calls on one device share its array, which holds the tables of the last plan copied in: calls
+ * that overlap on one device with different plans (on different streams, or from several threads)
+ * race and are undefined; calls on one stream are ordered. Arguments, pointer tables and status codes
+ * as for emu_reshard. */
+int emu_reshard_noalloc(emu_plan_t plan, const uint64_t* d_src_ptrs, const uint64_t* d_dst_ptrs, void* hip_stream);
 
 /* Bucket geometry of one rank (rank >= 0) or of all ranks together (rank == -1) of one side, for
  * bucket size bucket_bytes (section 6.2: each shard sent once as a contiguous buffer). Host only. */

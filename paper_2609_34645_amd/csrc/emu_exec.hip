@@ -12,6 +12,7 @@
 
 #include <atomic>
 #include <cstring>
+#include <mutex>
 
 #include "emu_internal.h"
 
@@ -922,6 +923,71 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
   return hip_check(unpack ? "emu_unpack_buckets launch" : "emu_pack_buckets launch");
 }
 
+// Launches the reshard of plan P whose tables (segments, tile map) start at device address w.
+static int launch_plan(const Plan* P, const uint8_t* w, const uint64_t* sp, const uint64_t* dp, hipStream_t st,
+                       const char* what) {
+  const DevSeg* segs = reinterpret_cast<const DevSeg*>(w + P->ws.off_segs);
+  const uint32_t* tm = reinterpret_cast<const uint32_t*>(w + P->ws.off_tilemap);
+  const bool ntm = option(EMU_OPT_NONTEMPORAL) != 0, lds = option(EMU_OPT_LDS_STAGING) != 0;
+  const bool xcd = option(EMU_OPT_XCD_REMAP) != 0;
+  drop_pending_error();
+  switch (P->tile_vecs) {
+    case 1: dispatch_reshard<1>(P, ntm, lds, xcd, st, segs, tm, sp, dp); break;
+    case 2: dispatch_reshard<2>(P, ntm, lds, xcd, st, segs, tm, sp, dp); break;
+    case 4: dispatch_reshard<4>(P, ntm, lds, xcd, st, segs, tm, sp, dp); break;
+    case 16: dispatch_reshard<16>(P, ntm, lds, xcd, st, segs, tm, sp, dp); break;
+    default: dispatch_reshard<8>(P, ntm, lds, xcd, st, segs, tm, sp, dp); break;
+  }
+  return hip_check(what);
+}
+
+// ------------------------------------------------------------------------------------------------
+// plan tables without a caller workspace (emu_reshard_noalloc)
+// ------------------------------------------------------------------------------------------------
+// For callers that cannot allocate device memory, the reshard tables go to a static device array. Each
+// device the library runs on holds its own copy of the array, at its own address, until the process
+// ends. Host code never uses the array's name as an address (in host code it names a host-side
+// stand-in): once per device, with that device current, hipGetSymbolAddress gives the device address,
+// which is kept per device and used for the upload and as the kernels' table pointer.
+constexpr uint64_t kScratchBytes = 32ull << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+struct ScratchSlot {
+  std::mutex mu;
+  void* ptr = nullptr;    // device address of `scratch` on this device
+  uint64_t resident = 0;  // id of the plan whose tables the array holds (0: none)
+};
+static ScratchSlot g_scratch[kMaxDevices];
+
+// The current device's array, holding P's tables: the first call on a device looks the array up, and
+// the tables are copied in (on stream st) unless the array already holds them from an earlier call.
+static int scratch_tables(const Plan* P, hipStream_t st, void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(EMU_ERR_HIP, "cannot query the current device");
+  if (dev < 0 || dev >= kMaxDevices) return fail(EMU_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  ScratchSlot& sl = g_scratch[dev];
+  std::lock_guard<std::mutex> lk(sl.mu);
+  if (!sl.ptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return fail(EMU_ERR_HIP, "scratch address on device %d: %s", dev, hipGetErrorString(e));
+    sl.ptr = p;
+  }
+  if (sl.resident != P->id) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cs) == hipSuccess && cs != hipStreamCaptureStatusNone)
+      return fail(EMU_ERR_ARG, "the static scratch does not hold this plan's tables: make one call outside stream "
+                  "capture first");
+    sl.resident = 0;
+    const hipError_t e = hipMemcpyAsync(sl.ptr, P->host_ws.data(), P->reshard_ws_bytes, hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return fail(EMU_ERR_HIP, "scratch upload: %s", hipGetErrorString(e));
+    sl.resident = P->id;
+  }
+  *out = sl.ptr;
+  return EMU_OK;
+}
+
 }  // namespace emu
 
 using namespace emu;
@@ -956,21 +1022,25 @@ int emu_reshard(emu_plan_t plan, const void* d_workspace, const uint64_t* d_src_
   if (!ws_current(d_workspace, P))
     return fail(EMU_ERR_WORKSPACE, "workspace %p holds no upload of this plan (fill it with emu_plan_upload)",
                 d_workspace);
-  const uint8_t* w = static_cast<const uint8_t*>(d_workspace);
-  const DevSeg* segs = reinterpret_cast<const DevSeg*>(w + P->ws.off_segs);
-  const uint32_t* tm = reinterpret_cast<const uint32_t*>(w + P->ws.off_tilemap);
+  return launch_plan(P, static_cast<const uint8_t*>(d_workspace), d_src_ptrs, d_dst_ptrs,
+                     static_cast<hipStream_t>(hip_stream), "emu_reshard launch");
+}
+
+int emu_reshard_noalloc(emu_plan_t plan, const uint64_t* d_src_ptrs, const uint64_t* d_dst_ptrs, void* hip_stream) {
+  clear_error();
+  const Plan* P = reinterpret_cast<const Plan*>(plan);
+  if (!plan_live(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
+  if (!d_src_ptrs || !d_dst_ptrs) return fail(EMU_ERR_NULL, "NULL pointer table");
+  if (misaligned(d_src_ptrs, 8) || misaligned(d_dst_ptrs, 8)) return fail(EMU_ERR_ALIGN, "pointer tables must be 8-byte aligned");
+  if (P->ntiles == 0) return EMU_OK;
+  if (P->reshard_ws_bytes > kScratchBytes)
+    return fail(EMU_ERR_WORKSPACE, "the plan's tables take %llu bytes, the static scratch holds %llu: use emu_reshard "
+                "with a workspace", (unsigned long long)P->reshard_ws_bytes, (unsigned long long)kScratchBytes);
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
-  const bool ntm = option(EMU_OPT_NONTEMPORAL) != 0, lds = option(EMU_OPT_LDS_STAGING) != 0;
-  const bool xcd = option(EMU_OPT_XCD_REMAP) != 0;
-  drop_pending_error();
-  switch (P->tile_vecs) {
-    case 1: dispatch_reshard<1>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;
-    case 2: dispatch_reshard<2>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;
-    case 4: dispatch_reshard<4>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;
-    case 16: dispatch_reshard<16>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;
-    default: dispatch_reshard<8>(P, ntm, lds, xcd, st, segs, tm, d_src_ptrs, d_dst_ptrs); break;
-  }
-  return hip_check("emu_reshard launch");
+  void* w = nullptr;
+  const int rc = scratch_tables(P, st, &w);
+  if (rc) return rc;
+  return launch_plan(P, static_cast<const uint8_t*>(w), d_src_ptrs, d_dst_ptrs, st, "emu_reshard_noalloc launch");
 }
 
 int emu_pack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, uint64_t bucket_bytes,

@@ -95,6 +95,7 @@ struct SideInfo {
 
 struct Plan {
   uint32_t magic = kPlanMagic;
+  uint64_t id = 0;                  // unique per plan object of the process (never reused)
   SideInfo side[2];
   std::vector<emu_segment_t> segs;  // execution order
   std::vector<DevSeg> dsegs;
@@ -108,7 +109,10 @@ struct Plan {
   emu_plan_info_t info{};
   WsLayout ws{};
   std::vector<uint8_t> host_ws;     // workspace image uploaded by emu_plan_upload
+  uint64_t reshard_ws_bytes = 0;    // prefix of host_ws that emu_reshard reads (segments and tile map)
 };
+
+uint64_t next_plan_id();
 
 // errors.cpp-style helpers (defined in emu_plan.cpp)
 int fail(int code, const char* fmt, ...);

@@ -67,6 +67,11 @@ void ws_forget(const Plan* p) {
   for (auto it = g_ws.begin(); it != g_ws.end();) it = it->second == p ? g_ws.erase(it) : std::next(it);
 }
 
+uint64_t next_plan_id() {
+  static std::atomic<uint64_t> next{1};
+  return next.fetch_add(1, std::memory_order_relaxed);
+}
+
 static std::atomic<int64_t> g_opt[8] = {{0}, {1}, {1}, {0}, {32}, {1}, {-1}, {1}};
 
 int64_t option(int32_t key) { return g_opt[key].load(std::memory_order_relaxed); }
@@ -554,6 +559,7 @@ static int finalize(Plan& P) {
     w.side[sd].n_tiles = nchunk[sd];
   }
   w.total = off;
+  P.reshard_ws_bytes = w.side[0].off_sizes;  // segments and tile map come first
   P.host_ws.assign(w.total, 0);
   uint8_t* h = P.host_ws.data();
   if (!P.dsegs.empty()) std::memcpy(h + w.off_segs, P.dsegs.data(), P.dsegs.size() * sizeof(DevSeg));
@@ -755,6 +761,7 @@ int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out) 
     return fail(EMU_ERR_MISMATCH, "source and destination layouts describe different models");
   Plan* P = new (std::nothrow) Plan();
   if (!P) return fail(EMU_ERR_ARG, "out of host memory");
+  P->id = next_plan_id();
   try {
     P->cvt = src->dtype == dst->dtype ? CVT_NONE : (src->dtype == EMU_FP32 ? CVT_F32_BF16 : CVT_BF16_F32);
     // automatic tile size: 4 KB (4 vectors per lane of the one-wave workgroup), the size that ran

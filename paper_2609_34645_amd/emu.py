@@ -146,6 +146,7 @@ def load(path: str = LIB_PATH):
         "emu_plan_segments": ([P, I64, I64, ctypes.POINTER(c_segment)], ctypes.c_int),
         "emu_plan_upload": ([P, V, U64, V], ctypes.c_int),
         "emu_reshard": ([P, V, V, V, V], ctypes.c_int),
+        "emu_reshard_noalloc": ([P, V, V, V], ctypes.c_int),
         "emu_bucket_layout": ([P, I32, U64, I32, ctypes.POINTER(U64), ctypes.POINTER(U64)], ctypes.c_int),
         "emu_pack_buckets": ([P, V, I32, U64, V, V, V], ctypes.c_int),
         "emu_unpack_buckets": ([P, V, I32, U64, V, V, V], ctypes.c_int),
@@ -364,6 +365,14 @@ class Plan:
         check(load().emu_reshard(self._h, ctypes.c_void_p(ws.data_ptr()), ctypes.c_void_p(src_ptrs.data_ptr()),
                                  ctypes.c_void_p(dst_ptrs.data_ptr()), _stream_handle(stream)))
 
+    def reshard_noalloc(self, src_ptrs, dst_ptrs, stream=None):
+        """``emu_reshard_noalloc``: the reshard with the plan tables in the library's static device array
+        (no workspace; nothing allocated by the call)."""
+        self._tables(None, (src_ptrs, self.info["n_src_tensors"], "src_ptrs"),
+                     (dst_ptrs, self.info["n_dst_tensors"], "dst_ptrs"))
+        check(load().emu_reshard_noalloc(self._h, ctypes.c_void_p(src_ptrs.data_ptr()),
+                                         ctypes.c_void_p(dst_ptrs.data_ptr()), _stream_handle(stream)))
+
     def _tables(self, ws, *tables):
         """Refuse, before any library call, pointer tables the kernels would read past the end of:
         each must be an int64 device tensor with exactly the entries the plan indexes."""
@@ -375,7 +384,7 @@ class Plan:
         for t, _, what in tables:
             if not t.is_cuda:
                 raise ValueError(f"{what} must be a device tensor")
-        if not getattr(ws, "is_cuda", False):
+        if ws is not None and not getattr(ws, "is_cuda", False):
             raise ValueError("the workspace must be a device tensor")
 
     def _bucket_tables(self, ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs):

@@ -225,6 +225,29 @@ def test_error_codes():
         assert lib.emu_status_str(s).startswith(b"EMU_")
 
 
+def test_noalloc_size_limit_is_checked_before_any_gpu_call():
+    """emu_reshard_noalloc refuses a plan whose tables exceed its 32 MiB static array with
+    EMU_ERR_WORKSPACE before any HIP call (so here, without a GPU, too); the 8B fp32 training-state plan
+    at the default 4 KB tiles (31.4 MB of tables, the largest workload) passes the check and only then
+    meets the missing device (EMU_ERR_HIP)."""
+    lib = emu.load()
+    m = emu.Model(*EIGHT_B)
+    a, b = emu.Layout(m, 4, 1, 0, "fp32"), emu.Layout(m, 1, 1, 0, "fp32")
+    fits = emu.Plan(a, b)
+    fake = ctypes.c_void_p(1 << 20)   # 8-byte aligned, never dereferenced: the call stops on the host
+    assert lib.emu_reshard_noalloc(fits._h, fake, fake, None) == -8
+    old = emu.get_option(emu.OPT_TILE_VECS)
+    emu.set_option(emu.OPT_TILE_VECS, 1)                          # 1 KB tiles: 4x the tile map
+    try:
+        big = emu.Plan(a, b)
+    finally:
+        emu.set_option(emu.OPT_TILE_VECS, old)
+    assert big.info["n_tiles"] * 4 > 32 << 20
+    assert lib.emu_reshard_noalloc(big._h, fake, fake, None) == -5
+    assert b"static scratch" in lib.emu_last_error()
+    assert lib.emu_reshard_noalloc(big._h, None, fake, None) == -1
+
+
 # ------------------------------------------------------------------------------------------------
 # fused reshard -> buckets (emu_plan_to_buckets)
 # ------------------------------------------------------------------------------------------------
