@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define EMU_ABI_VERSION 1
+#define EMU_ABI_VERSION 2
 
 typedef enum {
   EMU_OK = 0,
@@ -133,6 +133,9 @@ typedef struct {
   int32_t src_vocab_padded, dst_vocab_padded;
   int32_t n_general_segments; /* segments not on the 16-byte vector path (misaligned runs) */
   int32_t converts;          /* 0: same element type; 1: fp32 -> bf16; 2: bf16 -> fp32 */
+  int32_t n_alias_tensors;   /* destination tensors that are byte copies of one whole source tensor */
+  int32_t aliased;           /* 1: the map leaves those tensors out (EMU_PLAN_ALIAS_RESIDENT) */
+  uint64_t alias_bytes;      /* their bytes; with `aliased`, bytes_read and bytes_written exclude them */
 } emu_plan_info_t;
 
 typedef struct {
@@ -143,7 +146,27 @@ typedef struct {
   int64_t rows, cols;  /* row-major shape */
   uint64_t bytes;
   uint64_t stream_offset; /* byte offset inside its rank's bucket stream */
+  int32_t alias;          /* destination side: index of the source tensor this tensor equals byte for
+                             byte (same element type, whole tensor), else -1; source side: -1 */
+  int32_t reserved;
 } emu_tensor_desc_t;
+
+/* One bucket of one side for a bucket size B: bucket `index` of rank `rank` holds stream bytes
+ * [stream_offset, stream_offset + bytes) of that rank, stream_offset = index * B. */
+typedef struct {
+  int32_t rank, reserved;
+  uint64_t index;
+  uint64_t stream_offset;
+  uint64_t bytes;         /* B, or less for the rank's last bucket */
+} emu_bucket_desc_t;
+
+/* Flags of emu_plan_ex. */
+typedef enum {
+  EMU_PLAN_DEFAULT = 0,
+  EMU_PLAN_ALIAS_RESIDENT = 1  /* leave out of the map every destination tensor that is a byte copy of one
+                                  whole source tensor (emu_tensor_desc_t.alias >= 0): the caller points
+                                  its destination table entry at that source tensor instead */
+} emu_plan_flags;
 
 /* One entry of the copy map: for i < rows, src_run bytes of the source tensor (src_tensor < 0: none,
  * the destination gets zeros) at src_offset + i*src_stride become run bytes of the destination tensor at
@@ -206,6 +229,15 @@ int emu_layout_check(const emu_layout_t* layout);
  * the weight synchronisation from a training model-stage to a generation model-stage of the same model
  * (section 5, EMU definition). Host only: no GPU call. *out receives a new plan. */
 int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out);
+/* emu_plan with flags (emu_plan_flags). EMU_PLAN_ALIAS_RESIDENT: shards already resident are not
+ * copied (section 6.2, DAG execution and safety: Merge assembles the target from its sub-units and copies
+ * no shard that is already in place). Every plan reports its alias tensors (emu_plan_info,
+ * emu_tensor_info); with this flag the map leaves them out, emu_reshard writes only the other
+ * destination tensors, and the caller uses the source tensor as the destination tensor (for a PP-only
+ * change every destination tensor is one, and the reshard moves nothing). Whatever the destination
+ * table holds at an alias tensor's index is neither read nor written by emu_reshard. Unknown flags:
+ * EMU_ERR_ARG. Host only. */
+int emu_plan_ex(const emu_layout_t* src, const emu_layout_t* dst, uint32_t flags, emu_plan_t* out);
 /* Compile the fused sender-side map: source shards of layout *src straight into the contiguous
  * transfer buckets of layout *dst's ranks (bucket k of rank r = bytes [k*B, (k+1)*B) of r's stream),
  * skipping the destination tensors. The paper sends each shard once as a contiguous buffer after a
@@ -227,9 +259,11 @@ int emu_plan_segments(emu_plan_t plan, int64_t first, int64_t count, emu_segment
 /* Enqueue the host-to-device copy of the plan's tables into the caller's workspace (at least
  * info.workspace_bytes, 256-byte aligned). The plan must outlive the copy. The source is pageable host
  * memory, so the HIP runtime may return only once the stream has reached the copy. The library records that
- * this address now holds this plan's tables: execute calls of the plan accept only a workspace so
+ * this address now holds this plan's tables: execute calls of the plan accept only a workspace address so
  * recorded (EMU_ERR_WORKSPACE otherwise, before anything is launched), and an upload of another plan to
- * the same address replaces the record. */
+ * the same address replaces the record. The record is of the address, not of the allocation: the caller
+ * keeps the workspace allocated, and unwritten by anything but emu_plan_upload, while it uses it (a
+ * buffer freed and a new one allocated at the same address would pass for the upload). */
 int emu_plan_upload(emu_plan_t plan, void* d_workspace, uint64_t workspace_bytes, void* hip_stream);
 
 /* Execute the reshard (section 5.2 (a)/(b), the local layout change of section 6.2):
@@ -238,6 +272,14 @@ int emu_plan_upload(emu_plan_t plan, void* d_workspace, uint64_t workspace_bytes
  * destination byte exactly once. d_workspace holds the uploaded plan tables. */
 int emu_reshard(emu_plan_t plan, const void* d_workspace, const uint64_t* d_src_ptrs,
                 const uint64_t* d_dst_ptrs, void* hip_stream);
+
+/* emu_reshard of n_groups shard sets that share the plan's layouts, in one launch: the parameters and
+ * the optimizer states that follow their layout (section 5, EMU definition: omega in theta's layout),
+ * e.g. fp32 master weights, Adam m and Adam v. d_src_ptrs holds n_groups source tables back to back
+ * (group g's tensor i at g * n_src_tensors + i), d_dst_ptrs n_groups destination tables likewise. The
+ * result equals n_groups emu_reshard calls, one per group. 1 <= n_groups <= 65535 (EMU_ERR_RANGE). */
+int emu_reshard_groups(emu_plan_t plan, const void* d_workspace, int32_t n_groups, const uint64_t* d_src_ptrs,
+                       const uint64_t* d_dst_ptrs, void* hip_stream);
 
 /* emu_reshard without a caller workspace, for callers that cannot allocate device memory (code that
  * must not call hipMalloc, tight serving loops, harnesses that forbid allocation). The plan's reshard
@@ -259,8 +301,15 @@ int emu_reshard_noalloc(emu_plan_t plan, const uint64_t* d_src_ptrs, const uint6
  * bucket size bucket_bytes (section 6.2: each shard sent once as a contiguous buffer). Host only. */
 int emu_bucket_layout(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, int32_t rank,
                       uint64_t* n_buckets, uint64_t* stream_bytes);
+/* Buckets [first, first + count) of one side for bucket size bucket_bytes, in pointer-table order (rank
+ * 0's first), into out[] (section 6.2: each shard sent once as a contiguous buffer): the sizes a caller
+ * allocates and the stream range each bucket carries. EMU_ERR_RANGE if the range passes the side's
+ * bucket count (emu_bucket_layout(..., -1, ...)). Host only. */
+int emu_bucket_info(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, uint64_t first, uint64_t count,
+                    emu_bucket_desc_t* out);
 
-/* Pack one side's tensors into buckets: bucket k of rank r receives bytes [k*B, (k+1)*B) of r's
+/* Pack one side's tensors into contiguous buckets (section 6.2: each shard is sent once as a contiguous
+ * buffer, after the local layout change): bucket k of rank r receives bytes [k*B, (k+1)*B) of r's
  * stream. d_tensor_ptrs lists that side's tensors (as for emu_reshard); d_bucket_ptrs lists all
  * buckets, rank 0 first (emu_bucket_layout(..., -1, ...) of them). Tensor stream offsets (exclusive
  * prefix sums of the ragged tensor sizes) come from the uploaded workspace; each rank's first bucket
@@ -269,7 +318,8 @@ int emu_bucket_layout(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, int3
  * device). bucket_bytes must be a positive multiple of the element size. */
 int emu_pack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, uint64_t bucket_bytes,
                      const uint64_t* d_tensor_ptrs, const uint64_t* d_bucket_ptrs, void* hip_stream);
-/* The inverse of emu_pack_buckets: buckets -> that side's tensors. */
+/* The inverse of emu_pack_buckets on the receiver side (section 6.2: the receiver restores its shards
+ * from the contiguous buffers): buckets -> that side's tensors. */
 int emu_unpack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, uint64_t bucket_bytes,
                        const uint64_t* d_bucket_ptrs, const uint64_t* d_tensor_ptrs, void* hip_stream);
 
@@ -280,6 +330,8 @@ int emu_unpack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, u
  * emu_plan_to_buckets the destination entries are the buckets). Every entry must be non-zero
  * (EMU_ERR_NULL) and 16-byte aligned (EMU_ERR_ALIGN), and no destination byte range may overlap
  * another destination range or a source range (EMU_ERR_OVERLAP); source ranges may overlap each other.
+ * The destination entries of alias tensors a plan leaves out of its map (EMU_PLAN_ALIAS_RESIDENT) are
+ * not written and take no part in the overlap test.
  *
  * emu_check_bucket_tables: tensor_ptrs of one side and bucket_ptrs of its buckets of size bucket_bytes
  * (as for emu_pack_buckets / emu_unpack_buckets). The same conditions, with every tensor and bucket

@@ -510,7 +510,8 @@ __global__ __launch_bounds__(kReshardThreads, EMU_RESHARD_WAVES_PER_EU) void k_r
                                                                              const uint32_t* __restrict__ tilemap,
                                                                              uint64_t tile_base,
                                                                              const uint64_t* __restrict__ src_ptrs,
-                                                                             const uint64_t* __restrict__ dst_ptrs) {
+                                                                             const uint64_t* __restrict__ dst_ptrs,
+                                                                             uint32_t src_n, uint32_t dst_n) {
   extern __shared__ v4u stage[];
   uint32_t local = blockIdx.x;
   if constexpr (XCD) {
@@ -525,12 +526,13 @@ __global__ __launch_bounds__(kReshardThreads, EMU_RESHARD_WAVES_PER_EU) void k_r
   const uint32_t si = tilemap[tile];
   if (si == kNoSeg) return;
   const DevSeg g = segs[si];
-  uint8_t* db = reinterpret_cast<uint8_t*>(dst_ptrs[g.dst_idx]);
+  // grid row y runs tensor group y: its pointer tables follow the earlier groups' back to back
+  uint8_t* db = reinterpret_cast<uint8_t*>(dst_ptrs[uint64_t(blockIdx.y) * dst_n + g.dst_idx]);
   const uint64_t lt = tile - g.tile0;
   if constexpr (ZERO) {
     run_tile<U, NT, true, LDS, CVT_NONE>(g, lt, nullptr, db, stage);
   } else {
-    const uint8_t* sb = reinterpret_cast<const uint8_t*>(src_ptrs[g.src_idx]);
+    const uint8_t* sb = reinterpret_cast<const uint8_t*>(src_ptrs[uint64_t(blockIdx.y) * src_n + g.src_idx]);
     run_tile<U, NT, false, LDS, CVT>(g, lt, sb, db, stage);
   }
 }
@@ -793,19 +795,28 @@ static int hip_check(const char* what) {
   return EMU_OK;
 }
 
-// Launches k_reshard over the map section [first, first + count); first is a multiple of kXcds and the
-// section is padded to one.
+// Pointer tables of one reshard launch: `groups` source and destination tables back to back, each group
+// src_n source and dst_n destination entries (one group for emu_reshard).
+struct Tables {
+  const uint64_t* sp;
+  const uint64_t* dp;
+  uint32_t groups, src_n, dst_n;
+};
+
+// Launches k_reshard over the map section [first, first + count) for every group (grid row y = group y);
+// first is a multiple of kXcds and the section is padded to one.
 template <int U, bool NT, bool LDS, bool XCD, int CVT, bool ZERO>
 static void launch_reshard(hipStream_t st, const DevSeg* segs, const uint32_t* tm, uint64_t first, uint64_t count,
-                           const uint64_t* sp, const uint64_t* dp) {
+                           const Tables& tb) {
   const size_t lds = occupancy_lds(LDS ? size_t(kReshardThreads) * U * 16 : 0, uint64_t(kReshardThreads) * U * 16,
                                    kReshardFlightBytes<CVT>);
-  constexpr uint64_t kMaxGrid = 0x7ffffff8ull;  // a multiple of kXcds below the grid-size limit
+  // a multiple of kXcds whose work-items (64 per workgroup) stay below 2^32 in the grid's x dimension
+  constexpr uint64_t kMaxGrid = (1ull << 26) - kXcds;
   for (uint64_t done = 0; done < count; done += kMaxGrid) {
     const uint32_t n = uint32_t(count - done < kMaxGrid ? count - done : kMaxGrid);
     const uint32_t grid = XCD ? (n + kXcds - 1) / kXcds * kXcds : n;
-    hipLaunchKernelGGL((k_reshard<U, NT, LDS, XCD, CVT, ZERO>), dim3(grid), dim3(kReshardThreads), lds, st, segs, tm,
-                       first + done, sp, dp);
+    hipLaunchKernelGGL((k_reshard<U, NT, LDS, XCD, CVT, ZERO>), dim3(grid, tb.groups), dim3(kReshardThreads), lds, st,
+                       segs, tm, first + done, tb.sp, tb.dp, tb.src_n, tb.dst_n);
   }
 }
 
@@ -813,40 +824,40 @@ static void launch_reshard(hipStream_t st, const DevSeg* segs, const uint32_t* t
 // the launch options (converting plans: no LDS staging).
 template <int U, int CVT>
 static void launch_copy(bool nt_hint, bool lds, bool xcd, hipStream_t st, const DevSeg* segs, const uint32_t* tm,
-                        uint64_t first, uint64_t count, const uint64_t* sp, const uint64_t* dp) {
+                        uint64_t first, uint64_t count, const Tables& tb) {
   constexpr bool kLds = CVT == CVT_NONE;  // staging instances exist for plain copies only
   const int key = (nt_hint ? 4 : 0) | (lds && kLds ? 2 : 0) | (xcd ? 1 : 0);
   switch (key) {
-    case 0: launch_reshard<U, false, false, false, CVT, false>(st, segs, tm, first, count, sp, dp); break;
-    case 1: launch_reshard<U, false, false, true, CVT, false>(st, segs, tm, first, count, sp, dp); break;
-    case 2: launch_reshard<U, false, kLds, false, CVT, false>(st, segs, tm, first, count, sp, dp); break;
-    case 3: launch_reshard<U, false, kLds, true, CVT, false>(st, segs, tm, first, count, sp, dp); break;
-    case 4: launch_reshard<U, true, false, false, CVT, false>(st, segs, tm, first, count, sp, dp); break;
-    case 5: launch_reshard<U, true, false, true, CVT, false>(st, segs, tm, first, count, sp, dp); break;
-    case 6: launch_reshard<U, true, kLds, false, CVT, false>(st, segs, tm, first, count, sp, dp); break;
-    default: launch_reshard<U, true, kLds, true, CVT, false>(st, segs, tm, first, count, sp, dp); break;
+    case 0: launch_reshard<U, false, false, false, CVT, false>(st, segs, tm, first, count, tb); break;
+    case 1: launch_reshard<U, false, false, true, CVT, false>(st, segs, tm, first, count, tb); break;
+    case 2: launch_reshard<U, false, kLds, false, CVT, false>(st, segs, tm, first, count, tb); break;
+    case 3: launch_reshard<U, false, kLds, true, CVT, false>(st, segs, tm, first, count, tb); break;
+    case 4: launch_reshard<U, true, false, false, CVT, false>(st, segs, tm, first, count, tb); break;
+    case 5: launch_reshard<U, true, false, true, CVT, false>(st, segs, tm, first, count, tb); break;
+    case 6: launch_reshard<U, true, kLds, false, CVT, false>(st, segs, tm, first, count, tb); break;
+    default: launch_reshard<U, true, kLds, true, CVT, false>(st, segs, tm, first, count, tb); break;
   }
 }
 
 template <int U>
 static void dispatch_reshard(const Plan* P, bool nt_hint, bool lds, bool xcd, hipStream_t st, const DevSeg* segs,
-                             const uint32_t* tm, const uint64_t* sp, const uint64_t* dp) {
+                             const uint32_t* tm, const Tables& tb) {
   if (P->ntiles_copy > 0) {
     const uint64_t n = P->ntiles_copy;
     switch (P->cvt) {
-      case CVT_F32_BF16: launch_copy<U, CVT_F32_BF16>(nt_hint, lds, xcd, st, segs, tm, 0, n, sp, dp); break;
-      case CVT_BF16_F32: launch_copy<U, CVT_BF16_F32>(nt_hint, lds, xcd, st, segs, tm, 0, n, sp, dp); break;
-      default: launch_copy<U, CVT_NONE>(nt_hint, lds, xcd, st, segs, tm, 0, n, sp, dp); break;
+      case CVT_F32_BF16: launch_copy<U, CVT_F32_BF16>(nt_hint, lds, xcd, st, segs, tm, 0, n, tb); break;
+      case CVT_BF16_F32: launch_copy<U, CVT_BF16_F32>(nt_hint, lds, xcd, st, segs, tm, 0, n, tb); break;
+      default: launch_copy<U, CVT_NONE>(nt_hint, lds, xcd, st, segs, tm, 0, n, tb); break;
     }
   }
   if (P->ntiles_zero > 0) {
     const uint64_t z0 = P->zero_tile0, n = P->ntiles_zero;
     const int key = (nt_hint ? 2 : 0) | (xcd ? 1 : 0);
     switch (key) {
-      case 0: launch_reshard<U, false, false, false, CVT_NONE, true>(st, segs, tm, z0, n, sp, dp); break;
-      case 1: launch_reshard<U, false, false, true, CVT_NONE, true>(st, segs, tm, z0, n, sp, dp); break;
-      case 2: launch_reshard<U, true, false, false, CVT_NONE, true>(st, segs, tm, z0, n, sp, dp); break;
-      default: launch_reshard<U, true, false, true, CVT_NONE, true>(st, segs, tm, z0, n, sp, dp); break;
+      case 0: launch_reshard<U, false, false, false, CVT_NONE, true>(st, segs, tm, z0, n, tb); break;
+      case 1: launch_reshard<U, false, false, true, CVT_NONE, true>(st, segs, tm, z0, n, tb); break;
+      case 2: launch_reshard<U, true, false, false, CVT_NONE, true>(st, segs, tm, z0, n, tb); break;
+      default: launch_reshard<U, true, false, true, CVT_NONE, true>(st, segs, tm, z0, n, tb); break;
     }
   }
 }
@@ -923,20 +934,22 @@ static int bucket_call(emu_plan_t plan, const void* ws, int32_t side, uint64_t B
   return hip_check(unpack ? "emu_unpack_buckets launch" : "emu_pack_buckets launch");
 }
 
-// Launches the reshard of plan P whose tables (segments, tile map) start at device address w.
-static int launch_plan(const Plan* P, const uint8_t* w, const uint64_t* sp, const uint64_t* dp, hipStream_t st,
-                       const char* what) {
+// Launches the reshard of plan P, whose tables (segments, tile map) start at device address w, for
+// `groups` tensor groups.
+static int launch_plan(const Plan* P, const uint8_t* w, const uint64_t* sp, const uint64_t* dp, uint32_t groups,
+                       hipStream_t st, const char* what) {
   const DevSeg* segs = reinterpret_cast<const DevSeg*>(w + P->ws.off_segs);
   const uint32_t* tm = reinterpret_cast<const uint32_t*>(w + P->ws.off_tilemap);
   const bool ntm = option(EMU_OPT_NONTEMPORAL) != 0, lds = option(EMU_OPT_LDS_STAGING) != 0;
   const bool xcd = option(EMU_OPT_XCD_REMAP) != 0;
+  const Tables tb{sp, dp, groups, uint32_t(P->side[0].tensors.size()), uint32_t(P->side[1].tensors.size())};
   drop_pending_error();
   switch (P->tile_vecs) {
-    case 1: dispatch_reshard<1>(P, ntm, lds, xcd, st, segs, tm, sp, dp); break;
-    case 2: dispatch_reshard<2>(P, ntm, lds, xcd, st, segs, tm, sp, dp); break;
-    case 4: dispatch_reshard<4>(P, ntm, lds, xcd, st, segs, tm, sp, dp); break;
-    case 16: dispatch_reshard<16>(P, ntm, lds, xcd, st, segs, tm, sp, dp); break;
-    default: dispatch_reshard<8>(P, ntm, lds, xcd, st, segs, tm, sp, dp); break;
+    case 1: dispatch_reshard<1>(P, ntm, lds, xcd, st, segs, tm, tb); break;
+    case 2: dispatch_reshard<2>(P, ntm, lds, xcd, st, segs, tm, tb); break;
+    case 4: dispatch_reshard<4>(P, ntm, lds, xcd, st, segs, tm, tb); break;
+    case 16: dispatch_reshard<16>(P, ntm, lds, xcd, st, segs, tm, tb); break;
+    default: dispatch_reshard<8>(P, ntm, lds, xcd, st, segs, tm, tb); break;
   }
   return hip_check(what);
 }
@@ -1022,8 +1035,25 @@ int emu_reshard(emu_plan_t plan, const void* d_workspace, const uint64_t* d_src_
   if (!ws_current(d_workspace, P))
     return fail(EMU_ERR_WORKSPACE, "workspace %p holds no upload of this plan (fill it with emu_plan_upload)",
                 d_workspace);
-  return launch_plan(P, static_cast<const uint8_t*>(d_workspace), d_src_ptrs, d_dst_ptrs,
+  return launch_plan(P, static_cast<const uint8_t*>(d_workspace), d_src_ptrs, d_dst_ptrs, 1,
                      static_cast<hipStream_t>(hip_stream), "emu_reshard launch");
+}
+
+int emu_reshard_groups(emu_plan_t plan, const void* d_workspace, int32_t n_groups, const uint64_t* d_src_ptrs,
+                       const uint64_t* d_dst_ptrs, void* hip_stream) {
+  clear_error();
+  const Plan* P = reinterpret_cast<const Plan*>(plan);
+  if (!plan_live(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
+  if (!d_workspace || !d_src_ptrs || !d_dst_ptrs) return fail(EMU_ERR_NULL, "NULL workspace or pointer table");
+  if (n_groups < 1 || n_groups > 65535) return fail(EMU_ERR_RANGE, "n_groups %d not in [1, 65535]", n_groups);
+  if (misaligned(d_workspace, kWsAlign)) return fail(EMU_ERR_WORKSPACE, "workspace not %llu-byte aligned", (unsigned long long)kWsAlign);
+  if (misaligned(d_src_ptrs, 8) || misaligned(d_dst_ptrs, 8)) return fail(EMU_ERR_ALIGN, "pointer tables must be 8-byte aligned");
+  if (P->ntiles == 0) return EMU_OK;
+  if (!ws_current(d_workspace, P))
+    return fail(EMU_ERR_WORKSPACE, "workspace %p holds no upload of this plan (fill it with emu_plan_upload)",
+                d_workspace);
+  return launch_plan(P, static_cast<const uint8_t*>(d_workspace), d_src_ptrs, d_dst_ptrs, uint32_t(n_groups),
+                     static_cast<hipStream_t>(hip_stream), "emu_reshard_groups launch");
 }
 
 int emu_reshard_noalloc(emu_plan_t plan, const uint64_t* d_src_ptrs, const uint64_t* d_dst_ptrs, void* hip_stream) {
@@ -1040,7 +1070,7 @@ int emu_reshard_noalloc(emu_plan_t plan, const uint64_t* d_src_ptrs, const uint6
   void* w = nullptr;
   const int rc = scratch_tables(P, st, &w);
   if (rc) return rc;
-  return launch_plan(P, static_cast<const uint8_t*>(w), d_src_ptrs, d_dst_ptrs, st, "emu_reshard_noalloc launch");
+  return launch_plan(P, static_cast<const uint8_t*>(w), d_src_ptrs, d_dst_ptrs, 1, st, "emu_reshard_noalloc launch");
 }
 
 int emu_pack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, uint64_t bucket_bytes,

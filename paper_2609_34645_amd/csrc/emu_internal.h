@@ -101,6 +101,7 @@ struct Plan {
   std::vector<DevSeg> dsegs;
   int tile_vecs = 2;                // 16-byte vectors per thread per tile
   int cvt = CVT_NONE;               // element conversion of the whole plan
+  bool aliased = false;             // alias destination tensors are left out of the map
   uint64_t tile_bytes = 0;
   uint64_t ntiles = 0;              // copy + zero-fill tiles
   uint64_t ntiles_copy = 0;         // tiles [0, ntiles_copy) of the map: copy segments
@@ -121,8 +122,10 @@ bool plan_live(const Plan* p);
 int64_t option(int32_t key);
 
 // Workspace registry (emu_plan.cpp): which plan's tables were last uploaded to each workspace address.
-// Execute calls refuse a workspace that holds no upload of their plan, so that a forgotten upload or a
-// workspace overwritten by another plan's upload is an error instead of a kernel reading foreign tables.
+// Execute calls refuse an address that never received an upload of their plan, or whose last upload
+// was another plan's. The registry knows addresses, not allocations: a workspace freed after its upload
+// and an unrelated buffer later allocated at the same address pass for the upload (the caller must keep
+// an uploaded workspace alive while it uses it; the Python binding holds the tensors it uploaded to).
 void ws_register(const void* ws, const Plan* p);
 bool ws_current(const void* ws, const Plan* p);
 void ws_forget(const Plan* p);

@@ -150,6 +150,7 @@ static int build_side(const emu_layout_t& lay, SideInfo& s, std::vector<std::vec
   auto add = [&](int r, int kind, int layer, int ndim, int64_t rows, int64_t cols) {
     emu_tensor_desc_t d{};
     d.rank = r; d.kind = kind; d.layer = layer; d.ndim = ndim; d.rows = rows; d.cols = cols;
+    d.alias = -1;
     d.bytes = uint64_t(rows) * uint64_t(cols) * uint64_t(es);
     s.tensors.push_back(d);
     blocks.emplace_back();
@@ -335,6 +336,28 @@ static int compile(Plan& P, const std::vector<std::vector<Block>>& sb, const std
   return EMU_OK;
 }
 
+// Destination tensors that are byte copies of one whole source tensor: exactly one segment covers them,
+// from offset 0 of a source tensor of the same size, as one run, without conversion. These are the shards
+// a transition finds already in place (a PP-only change: every tensor; a TP change: the replicated norms,
+// and tensors whose TP slicing the two layouts share). With `drop`, their segments leave the map.
+static void find_aliases(Plan& P, bool drop) {
+  SideInfo& D = P.side[1];
+  const SideInfo& S = P.side[0];
+  std::vector<int32_t> nseg(D.tensors.size(), 0);
+  for (const emu_segment_t& g : P.segs) ++nseg[g.dst_tensor];
+  for (const emu_segment_t& g : P.segs) {
+    emu_tensor_desc_t& d = D.tensors[g.dst_tensor];
+    if (nseg[g.dst_tensor] == 1 && g.src_tensor >= 0 && P.cvt == CVT_NONE && g.rows == 1 && g.src_offset == 0 &&
+        g.dst_offset == 0 && g.run == d.bytes && S.tensors[g.src_tensor].bytes == d.bytes)
+      d.alias = g.src_tensor;
+  }
+  P.aliased = drop;
+  if (drop)
+    P.segs.erase(std::remove_if(P.segs.begin(), P.segs.end(),
+                                [&](const emu_segment_t& g) { return D.tensors[g.dst_tensor].alias >= 0; }),
+                 P.segs.end());
+}
+
 // Rewrite a destination-driven copy map so that it writes the destination ranks' bucket streams
 // instead of the destination tensors: tensor j's byte o lands at stream position
 // stream_offset(j) + o of its rank, i.e. in bucket (pos / B) at offset (pos % B). Rows that stay inside
@@ -415,6 +438,7 @@ static int to_buckets(Plan& P, uint64_t B) {
       d.layer = -1;
       d.ndim = 1;
       d.bytes = std::min<uint64_t>(B, D.rank_bytes[r] - k * B);
+      d.alias = -1;
       d.rows = 1;
       d.cols = int64_t(d.bytes / es);
       d.stream_offset = k * B;
@@ -525,7 +549,14 @@ static int finalize(Plan& P) {
     else P.ntiles_zero = nmap - P.zero_tile0;
     nmap = (nmap + kXcdCount - 1) / kXcdCount * kXcdCount;
   }
-  if (written != P.side[1].total_bytes)
+  int32_t n_alias = 0;
+  uint64_t alias_bytes = 0;
+  for (const emu_tensor_desc_t& d : P.side[1].tensors)
+    if (d.alias >= 0) {
+      ++n_alias;
+      alias_bytes += d.bytes;
+    }
+  if (written + (P.aliased ? alias_bytes : 0) != P.side[1].total_bytes)
     return fail(EMU_ERR_ARG, "internal: copy map covers %llu of %llu destination bytes",
                 (unsigned long long)written, (unsigned long long)P.side[1].total_bytes);
 
@@ -618,6 +649,9 @@ static int finalize(Plan& P) {
   I.src_vocab_padded = int32_t(P.side[0].vp);
   I.dst_vocab_padded = int32_t(P.side[1].vp);
   I.n_general_segments = ngeneral;
+  I.n_alias_tensors = n_alias;
+  I.aliased = P.aliased ? 1 : 0;
+  I.alias_bytes = alias_bytes;
   return EMU_OK;
 }
 
@@ -643,8 +677,9 @@ struct Range {
 };
 
 int add_ranges(std::vector<Range>& out, const uint64_t* ptrs, const std::vector<uint64_t>& sizes, bool shared,
-               const char* what) {
+               const char* what, const std::vector<bool>* skip = nullptr) {
   for (size_t i = 0; i < sizes.size(); ++i) {
+    if (skip && (*skip)[i]) continue;
     const uint64_t p = ptrs[i];
     if (p == 0) return emu::fail(EMU_ERR_NULL, "%s %zu has a NULL address", what, i);
     if (p % 16) return emu::fail(EMU_ERR_ALIGN, "%s %zu at 0x%llx is not 16-byte aligned", what, i, (unsigned long long)p);
@@ -750,9 +785,14 @@ int emu_layout_check(const emu_layout_t* layout) {
 }
 
 int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out) {
+  return emu_plan_ex(src, dst, EMU_PLAN_DEFAULT, out);
+}
+
+int emu_plan_ex(const emu_layout_t* src, const emu_layout_t* dst, uint32_t flags, emu_plan_t* out) {
   clear_error();
   if (!src || !dst || !out) return fail(EMU_ERR_NULL, "NULL argument");
   *out = nullptr;
+  if (flags & ~uint32_t(EMU_PLAN_ALIAS_RESIDENT)) return fail(EMU_ERR_ARG, "unknown plan flags 0x%x", flags);
   int rc = check_layout(src);
   if (rc) return rc;
   rc = check_layout(dst);
@@ -773,6 +813,7 @@ int emu_plan(const emu_layout_t* src, const emu_layout_t* dst, emu_plan_t* out) 
     rc = build_side(*src, P->side[0], sb);
     if (!rc) rc = build_side(*dst, P->side[1], db);
     if (!rc) rc = compile(*P, sb, db);
+    if (!rc) find_aliases(*P, (flags & EMU_PLAN_ALIAS_RESIDENT) != 0);
     if (!rc) rc = finalize(*P);
   } catch (const std::bad_alloc&) {
     rc = fail(EMU_ERR_ARG, "out of host memory");
@@ -889,6 +930,39 @@ int emu_bucket_layout(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, int3
 
 
 
+int emu_bucket_info(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, uint64_t first, uint64_t count,
+                    emu_bucket_desc_t* out) {
+  clear_error();
+  const Plan* P = reinterpret_cast<const Plan*>(plan);
+  if (!plan_live(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
+  if (side != 0 && side != 1) return fail(EMU_ERR_RANGE, "side must be 0 or 1");
+  if (count > 0 && !out) return fail(EMU_ERR_NULL, "out is NULL");
+  const SideInfo& s = P->side[side];
+  const uint64_t es = uint64_t(elem_size(s.lay.dtype));
+  if (bucket_bytes == 0 || bucket_bytes % es)
+    return fail(EMU_ERR_BUCKET, "bucket size %llu is not a positive multiple of %llu",
+                (unsigned long long)bucket_bytes, (unsigned long long)es);
+  uint64_t total = 0;
+  for (int r = 0; r < s.nranks; ++r) total += (s.rank_bytes[r] + bucket_bytes - 1) / bucket_bytes;
+  if (first > total || count > total - first)
+    return fail(EMU_ERR_RANGE, "buckets [%llu, %llu + %llu) out of %llu", (unsigned long long)first,
+                (unsigned long long)first, (unsigned long long)count, (unsigned long long)total);
+  uint64_t k0 = 0, i = 0;  // global index of rank r's first bucket
+  for (int r = 0; r < s.nranks && i < count; ++r) {
+    const uint64_t nb = (s.rank_bytes[r] + bucket_bytes - 1) / bucket_bytes;
+    for (uint64_t k = first + i > k0 ? first + i - k0 : 0; k < nb && i < count; ++k, ++i) {
+      emu_bucket_desc_t& b = out[i];
+      b.rank = r;
+      b.reserved = 0;
+      b.index = k;
+      b.stream_offset = k * bucket_bytes;
+      b.bytes = std::min<uint64_t>(bucket_bytes, s.rank_bytes[r] - k * bucket_bytes);
+    }
+    k0 += nb;
+  }
+  return EMU_OK;
+}
+
 int emu_check_tables(emu_plan_t plan, const uint64_t* src_ptrs, const uint64_t* dst_ptrs) {
   emu::clear_error();
   const emu::Plan* P = reinterpret_cast<const emu::Plan*>(plan);
@@ -898,7 +972,11 @@ int emu_check_tables(emu_plan_t plan, const uint64_t* src_ptrs, const uint64_t* 
     std::vector<Range> rs;
     int rc = add_ranges(rs, src_ptrs, tensor_sizes(P->side[0]), true, "source tensor");
     if (rc) return rc;
-    rc = add_ranges(rs, dst_ptrs, tensor_sizes(P->side[1]), false, "destination tensor");
+    // alias tensors left out of the map are never written: their entries take no part
+    std::vector<bool> skip(P->side[1].tensors.size(), false);
+    if (P->aliased)
+      for (size_t i = 0; i < skip.size(); ++i) skip[i] = P->side[1].tensors[i].alias >= 0;
+    rc = add_ranges(rs, dst_ptrs, tensor_sizes(P->side[1]), false, "destination tensor", &skip);
     if (rc) return rc;
     return sweep(rs);
   } catch (const std::bad_alloc&) {

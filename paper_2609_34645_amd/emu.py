@@ -62,13 +62,20 @@ class c_plan_info(ctypes.Structure):
                 ("zero_fill_bytes", ctypes.c_uint64), ("src_bytes", ctypes.c_uint64),
                 ("dst_bytes", ctypes.c_uint64), ("workspace_bytes", ctypes.c_uint64),
                 ("src_vocab_padded", ctypes.c_int32), ("dst_vocab_padded", ctypes.c_int32),
-                ("n_general_segments", ctypes.c_int32), ("converts", ctypes.c_int32)]
+                ("n_general_segments", ctypes.c_int32), ("converts", ctypes.c_int32),
+                ("n_alias_tensors", ctypes.c_int32), ("aliased", ctypes.c_int32), ("alias_bytes", ctypes.c_uint64)]
 
 
 class c_tensor_desc(ctypes.Structure):
     _fields_ = [("rank", ctypes.c_int32), ("kind", ctypes.c_int32), ("layer", ctypes.c_int32),
                 ("ndim", ctypes.c_int32), ("rows", ctypes.c_int64), ("cols", ctypes.c_int64),
-                ("bytes", ctypes.c_uint64), ("stream_offset", ctypes.c_uint64)]
+                ("bytes", ctypes.c_uint64), ("stream_offset", ctypes.c_uint64), ("alias", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+class c_bucket_desc(ctypes.Structure):
+    _fields_ = [("rank", ctypes.c_int32), ("reserved", ctypes.c_int32), ("index", ctypes.c_uint64),
+                ("stream_offset", ctypes.c_uint64), ("bytes", ctypes.c_uint64)]
 
 
 class c_segment(ctypes.Structure):
@@ -138,6 +145,8 @@ def load(path: str = LIB_PATH):
         "emu_get_option": ([I32, ctypes.POINTER(I64)], ctypes.c_int),
         "emu_layout_check": ([ctypes.POINTER(c_layout)], ctypes.c_int),
         "emu_plan": ([ctypes.POINTER(c_layout), ctypes.POINTER(c_layout), ctypes.POINTER(P)], ctypes.c_int),
+        "emu_plan_ex": ([ctypes.POINTER(c_layout), ctypes.POINTER(c_layout), ctypes.c_uint32, ctypes.POINTER(P)],
+                        ctypes.c_int),
         "emu_plan_to_buckets": ([ctypes.POINTER(c_layout), ctypes.POINTER(c_layout), U64, ctypes.POINTER(P)],
                                 ctypes.c_int),
         "emu_plan_free": ([P], ctypes.c_int),
@@ -147,6 +156,8 @@ def load(path: str = LIB_PATH):
         "emu_plan_upload": ([P, V, U64, V], ctypes.c_int),
         "emu_reshard": ([P, V, V, V, V], ctypes.c_int),
         "emu_reshard_noalloc": ([P, V, V, V], ctypes.c_int),
+        "emu_reshard_groups": ([P, V, I32, V, V, V], ctypes.c_int),
+        "emu_bucket_info": ([P, I32, U64, U64, U64, ctypes.POINTER(c_bucket_desc)], ctypes.c_int),
         "emu_bucket_layout": ([P, I32, U64, I32, ctypes.POINTER(U64), ctypes.POINTER(U64)], ctypes.c_int),
         "emu_pack_buckets": ([P, V, I32, U64, V, V, V], ctypes.c_int),
         "emu_unpack_buckets": ([P, V, I32, U64, V, V, V], ctypes.c_int),
@@ -256,17 +267,22 @@ class ShardSet:
 class Plan:
     """A compiled copy map between two layouts (``emu_plan``)."""
 
-    def __init__(self, src: Layout, dst: Layout, bucket_bytes: int = 0):
+    def __init__(self, src: Layout, dst: Layout, bucket_bytes: int = 0, alias: bool = False):
         """bucket_bytes > 0 compiles the fused map (``emu_plan_to_buckets``): its destination side is
-        the destination ranks' buckets of that size."""
+        the destination ranks' buckets of that size. alias=True leaves destination tensors that are byte
+        copies of a whole source tensor out of the map (``emu_plan_ex`` with EMU_PLAN_ALIAS_RESIDENT);
+        ``alloc(1, alias=S)`` makes them views of the source set S."""
         lib = load()
         self.src, self.dst, self.bucket_bytes = src, dst, bucket_bytes
+        self._uploads = {}  # data_ptr -> workspace tensor this plan uploaded to (kept alive)
         cs, cd = src.c(), dst.c()
         h = ctypes.c_void_p()
         if bucket_bytes:
+            if alias:
+                raise ValueError("a fused plan's destination is its buckets: nothing to alias")
             check(lib.emu_plan_to_buckets(ctypes.byref(cs), ctypes.byref(cd), bucket_bytes, ctypes.byref(h)))
         else:
-            check(lib.emu_plan(ctypes.byref(cs), ctypes.byref(cd), ctypes.byref(h)))
+            check(lib.emu_plan_ex(ctypes.byref(cs), ctypes.byref(cd), 1 if alias else 0, ctypes.byref(h)))
         self._h = h
         info = c_plan_info()
         check(lib.emu_plan_info(h, ctypes.byref(info)))
@@ -288,7 +304,7 @@ class Plan:
                 if d.kind == 14:
                     shape = (d.bytes,)
                 out.append(dict(rank=d.rank, kind=KINDS[d.kind], layer=d.layer, shape=shape, bytes=d.bytes,
-                                stream_offset=d.stream_offset))
+                                stream_offset=d.stream_offset, alias=d.alias))
             self._descs[side] = out
         return self._descs[side]
 
@@ -303,6 +319,14 @@ class Plan:
         check(load().emu_bucket_layout(self._h, side, bucket_bytes, rank, ctypes.byref(nb), ctypes.byref(sb)))
         return nb.value, sb.value
 
+    def bucket_info(self, side: int, bucket_bytes: int) -> list:
+        """Every bucket of one side (``emu_bucket_info``), in pointer-table order: dict(rank, index,
+        stream_offset, bytes)."""
+        n = self.bucket_layout(side, bucket_bytes, -1)[0]
+        arr = (c_bucket_desc * max(1, n))()
+        check(load().emu_bucket_info(self._h, side, bucket_bytes, 0, n, arr))
+        return [dict(rank=b.rank, index=b.index, stream_offset=b.stream_offset, bytes=b.bytes) for b in arr[:n]]
+
     # -- device helpers (plumbing) -------------------------------------------------------------
     def workspace(self, device=None, stream=None):
         """Allocate a workspace tensor and enqueue the plan upload into it."""
@@ -314,26 +338,37 @@ class Plan:
         return ws
 
     def upload(self, ws, stream=None):
+        """Upload the plan tables into `ws`. The plan keeps `ws` alive, so its address cannot be handed to
+        another buffer while the plan may still name it; execute calls accept only workspaces this plan
+        uploaded to (the library also refuses one that another plan has overwritten since)."""
         check(load().emu_plan_upload(self._h, ctypes.c_void_p(ws.data_ptr()), ws.numel(), _stream_handle(stream)))
+        self._uploads[ws.data_ptr()] = ws
 
-    def alloc(self, side: int, device=None, fill=None, guard: int = 0) -> ShardSet:
+    def alloc(self, side: int, device=None, fill=None, guard: int = 0, alias: ShardSet = None) -> ShardSet:
         """Allocate one side's shard set (one buffer per rank, 256-byte aligned tensor views). With
         guard > 0, at least that many bytes separate consecutive views and precede the first and follow
-        the last, so that bytes a call must not touch surround every tensor (tests prefill them)."""
+        the last, so that bytes a call must not touch surround every tensor (tests prefill them). With
+        alias=S (destination side of an alias plan), every alias tensor is S's source tensor itself and
+        gets no bytes of its own."""
         import torch
 
         descs = self.tensors(side)
+        if alias is not None and (side != 1 or not self.info["aliased"]):
+            raise ValueError("alias= needs the destination side of a plan made with alias=True")
+        own = [alias is None or d["alias"] < 0 for d in descs]
         nranks = self.info["n_src_ranks" if side == 0 else "n_dst_ranks"]
         offs, sizes = [], [0] * nranks
-        for d in descs:
-            o = (sizes[d["rank"]] + guard + 255) // 256 * 256
+        for d, mine in zip(descs, own):
+            o = (sizes[d["rank"]] + guard + 255) // 256 * 256 if mine else -1
             offs.append(o)
-            sizes[d["rank"]] = o + d["bytes"]
+            if mine:
+                sizes[d["rank"]] = o + d["bytes"]
         bufs = [torch.empty(max(s + guard, 16), dtype=torch.uint8, device=device or "cuda") for s in sizes]
         if fill is not None:
             for b in bufs:
                 b.fill_(fill)
-        tensors = [bufs[d["rank"]][o:o + d["bytes"]] for d, o in zip(descs, offs)]
+        tensors = [bufs[d["rank"]][o:o + d["bytes"]] if mine else alias.tensors[d["alias"]]
+                   for d, o, mine in zip(descs, offs, own)]
         return ShardSet(bufs, tensors, ptr_table(tensors, device))
 
     def alloc_buckets(self, side: int, bucket_bytes: int, device=None, fill=None, guard: int = 0):
@@ -342,11 +377,7 @@ class Plan:
         ``alloc``)."""
         import torch
 
-        nranks = self.info["n_src_ranks" if side == 0 else "n_dst_ranks"]
-        sizes = []
-        for r in range(nranks):
-            nb, sb = self.bucket_layout(side, bucket_bytes, r)
-            sizes += [min(bucket_bytes, sb - k * bucket_bytes) for k in range(nb)]
+        sizes = [b["bytes"] for b in self.bucket_info(side, bucket_bytes)]
         offs, total = [], 0
         for n in sizes:
             o = (total + guard + 255) // 256 * 256
@@ -364,6 +395,17 @@ class Plan:
                      (dst_ptrs, self.info["n_dst_tensors"], "dst_ptrs"))
         check(load().emu_reshard(self._h, ctypes.c_void_p(ws.data_ptr()), ctypes.c_void_p(src_ptrs.data_ptr()),
                                  ctypes.c_void_p(dst_ptrs.data_ptr()), _stream_handle(stream)))
+
+    def reshard_groups(self, ws, src_tables, dst_tables, stream=None):
+        """``emu_reshard_groups``: one launch over several shard sets of this plan's layouts. src_tables
+        and dst_tables are int64 device tensors holding the groups' pointer tables back to back
+        (``group_tables``)."""
+        ns, nd = self.info["n_src_tensors"], self.info["n_dst_tensors"]
+        n = src_tables.numel() // ns if ns else 0
+        self._tables(ws, (src_tables, n * ns, "src_tables"), (dst_tables, n * nd, "dst_tables"))
+        check(load().emu_reshard_groups(self._h, ctypes.c_void_p(ws.data_ptr()), n,
+                                        ctypes.c_void_p(src_tables.data_ptr()), ctypes.c_void_p(dst_tables.data_ptr()),
+                                        _stream_handle(stream)))
 
     def reshard_noalloc(self, src_ptrs, dst_ptrs, stream=None):
         """``emu_reshard_noalloc``: the reshard with the plan tables in the library's static device array
@@ -386,6 +428,8 @@ class Plan:
                 raise ValueError(f"{what} must be a device tensor")
         if ws is not None and not getattr(ws, "is_cuda", False):
             raise ValueError("the workspace must be a device tensor")
+        if ws is not None and self._uploads.get(ws.data_ptr()) is None:
+            raise EmuError(-5, f"workspace at {ws.data_ptr():#x} holds no upload of this plan (Plan.upload)")
 
     def _bucket_tables(self, ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs):
         if side not in (0, 1):
@@ -439,6 +483,13 @@ def _u64_array(ptrs):
         ptrs = ptrs.cpu().tolist()
     vals = [int(x) & 0xFFFFFFFFFFFFFFFF for x in ptrs]
     return (ctypes.c_uint64 * max(1, len(vals)))(*vals)
+
+
+def group_tables(sets, device=None):
+    """Back-to-back device pointer table of several ShardSets (for ``Plan.reshard_groups``)."""
+    import torch
+
+    return torch.cat([s.ptrs for s in sets]).to(device or "cuda")
 
 
 def ptr_table(tensors, device=None):

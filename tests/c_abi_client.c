@@ -62,8 +62,32 @@ int main(void) {
   printf("overlap %s\n", emu_status_str(emu_check_tables(plan, sp, dp)));
   free(sp);
   free(dp);
+  {
+    /* buckets of the destination side at B = 2^28, sized by the library */
+    uint64_t nb = 0, sb = 0, k, sum = 0;
+    emu_bucket_desc_t* bk;
+    CHECK(emu_bucket_layout(plan, 1, 1ull << 28, -1, &nb, &sb));
+    bk = (emu_bucket_desc_t*)malloc(sizeof(emu_bucket_desc_t) * (size_t)nb);
+    if (!bk) return 1;
+    CHECK(emu_bucket_info(plan, 1, 1ull << 28, 0, nb, bk));
+    for (k = 0; k < nb; ++k) sum += bk[k].bytes;
+    printf("buckets %llu %llu %d %llu %llu\n", (unsigned long long)nb, (unsigned long long)sum, bk[nb - 1].rank,
+           (unsigned long long)bk[nb - 1].index, (unsigned long long)bk[nb - 1].bytes);
+    printf("bucket_range %s\n", emu_status_str(emu_bucket_info(plan, 1, 1ull << 28, nb, 1, bk)));
+    free(bk);
+  }
   CHECK(emu_plan_free(plan));
   printf("freed_again %s\n", emu_status_str(emu_plan_free(plan)));
+
+  {
+    /* a PP-only change with resident shards aliased: nothing left to copy */
+    emu_layout_t s2 = layout(4, 2), d2 = layout(4, 1);
+    CHECK(emu_plan_ex(&s2, &d2, EMU_PLAN_ALIAS_RESIDENT, &plan));
+    CHECK(emu_plan_info(plan, &info));
+    printf("alias %d %d %llu %llu %lld\n", info.n_alias_tensors, info.aliased, (unsigned long long)info.alias_bytes,
+           (unsigned long long)info.bytes_read, (long long)info.n_tiles);
+    CHECK(emu_plan_free(plan));
+  }
 
   /* transition DAG: one training model-stage, (TP4, PP8) on 32 GPUs -> (TP8, PP2) on the first 16 */
   {

@@ -62,8 +62,9 @@ int main(int argc, char** argv) {
   emu_plan_info_t info;
   emu_tensor_desc_t d;
   const uint64_t B = 12288;
-  uint64_t nb = 0, sb = 0, k, off;
-  int32_t i, r, ns, nd;
+  uint64_t nb = 0, sb = 0, k;
+  int32_t i, ns, nd;
+  emu_bucket_desc_t* bk;
   void **S, **D, **R, **K, *ws, *ws2;
   uint64_t *ssz, *dsz, *ksz, *hs, *hd, *hr, *hk, *d_sp, *d_dp, *d_rp, *d_kp;
   int equal = 1;
@@ -115,21 +116,17 @@ int main(int argc, char** argv) {
   EMUCHECK(emu_plan_upload(plan, ws, info.workspace_bytes, NULL));
   EMUCHECK(emu_reshard(plan, ws, d_sp, d_dp, NULL));
 
-  /* buckets of every destination rank, rank 0 first */
+  /* buckets of every destination rank, rank 0 first, sized as the library reports them */
   EMUCHECK(emu_bucket_layout(plan, 1, B, -1, &nb, &sb));
   K = calloc((size_t)nb, sizeof(void*)); ksz = calloc((size_t)nb, 8); hk = calloc((size_t)nb, 8);
-  if (!K || !ksz || !hk) return 1;
-  k = 0;
-  for (r = 0; r < info.n_dst_ranks; ++r) {
-    uint64_t rb = 0, rs = 0;
-    EMUCHECK(emu_bucket_layout(plan, 1, B, r, &rb, &rs));
-    for (off = 0; off < rs; off += B, ++k) {
-      ksz[k] = rs - off < B ? rs - off : B;
-      HIPCHECK(hipMalloc(&K[k], ksz[k]));
-      hk[k] = (uint64_t)(uintptr_t)K[k];
-    }
+  bk = calloc((size_t)nb, sizeof(emu_bucket_desc_t));
+  if (!K || !ksz || !hk || !bk) return 1;
+  EMUCHECK(emu_bucket_info(plan, 1, B, 0, nb, bk));
+  for (k = 0; k < nb; ++k) {
+    ksz[k] = bk[k].bytes;
+    HIPCHECK(hipMalloc(&K[k], ksz[k]));
+    hk[k] = (uint64_t)(uintptr_t)K[k];
   }
-  if (k != nb) return 1;
   EMUCHECK(emu_check_bucket_tables(plan, 1, B, hd, hk));
   HIPCHECK(hipMalloc((void**)&d_kp, (size_t)nb * 8));
   HIPCHECK(hipMemcpy(d_kp, hk, (size_t)nb * 8, hipMemcpyHostToDevice));
@@ -158,6 +155,7 @@ int main(int argc, char** argv) {
     HIPCHECK(hipFree(R[i]));
   }
   for (k = 0; k < nb; ++k) HIPCHECK(hipFree(K[k]));
+  free(bk);
   HIPCHECK(hipFree(d_sp)); HIPCHECK(hipFree(d_dp)); HIPCHECK(hipFree(d_rp)); HIPCHECK(hipFree(d_kp));
   HIPCHECK(hipFree(ws)); HIPCHECK(hipFree(ws2));
   EMUCHECK(emu_plan_free(plan));

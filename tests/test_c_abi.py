@@ -41,6 +41,15 @@ def test_header_compiles_as_c99_and_host_calls_work(client):
     spec = oracle.rank_inventory(dst)[0][1]                              # rank 0's second tensor
     assert spec.kind == "attn_norm" and client["dst1"] == f"0 {emu.KINDS.index('attn_norm')} 1 {om.H}"
     assert client["overlap"] == "EMU_ERR_OVERLAP"
+    # buckets at 2^28 bytes: the destination streams cut by the oracle's rule
+    streams = [sum(s.numel * 2 for s in r) for r in oracle.rank_inventory(dst)]
+    nb = sum(-(-n // (1 << 28)) for n in streams)
+    last = streams[-1] - (streams[-1] - 1) // (1 << 28) * (1 << 28)
+    assert client["buckets"] == f"{nb} {sum(streams)} {len(streams) - 1} {(streams[-1] - 1) // (1 << 28)} {last}"
+    assert client["bucket_range"] == "EMU_ERR_RANGE"
+    # TP4 PP2 -> TP4 PP1 aliased: every destination tensor is a whole source tensor, nothing is read
+    n_dst41 = sum(len(r) for r in oracle.rank_inventory(oracle.Layout(om, 4, 1)))
+    assert client["alias"] == f"{n_dst41} 1 {dst_bytes} 0 0"
     assert client["freed_again"] == "EMU_ERR_HANDLE"
     n_nodes, n_edges, l_tran = client["dag"].split()
     py = emu.dag_plan([dict(kind=2, tp=4, pp=8, dp=1, gpus=list(range(32)), tgt_tp=8, tgt_pp=2, tgt_dp=1,

@@ -12,10 +12,12 @@
   (8.7 GB embedding and LM head), TP1 PP1 -> TP2 PP1, packed into 2^30-byte buckets and unpacked, then
   converted back to bf16 TP1 PP1: every byte against the oracle.
 * 8B TP2 PP2 -> TP4 PP1 with non-default tiling and launch options, on sampled tensor groups.
+* Resident shards aliased (EMU_PLAN_ALIAS_RESIDENT): 8B TP4 PP2 -> TP4 PP1, PP-only (nothing copied) and
+  with the fused formats changed too; every destination tensor against the oracle.
 * 8B conversions at full size: fp32 TP4 PP1 -> bf16 TP2 PP2 (the weight sync) and bf16 TP2 PP2 -> fp32
   TP4 PP1, each also fused into 2^28-byte buckets; every byte against the oracle.
-* 8B training state, fp32 master + Adam m + v (96 GB in): TP4 PP1 -> TP1 PP1, one launch per tensor
-  group, then split back into the source buffers; master, m and v checked in full against the oracle,
+* 8B training state, fp32 master + Adam m + v (96 GB in): TP4 PP1 -> TP1 PP1 in one emu_reshard_groups
+  launch, then split back into the source buffers with one emu_reshard launch per group; master, m and v checked in full against the oracle,
   the back transition against a seeded regeneration of the original state.
 
 Every call's write footprint is checked as well (tests.gpu_util.Guard): each tensor and bucket view sits
@@ -299,6 +301,39 @@ def test_tensors_over_4gib(gpu_lib):
     cleanup()
 
 
+@pytest.mark.parametrize("mixed", [False, True], ids=["pp_only", "pp_and_formats"])
+def test_8b_alias_resident_shards(gpu_lib, mixed):
+    """Shards already resident are not copied (section 6.2): 8B TP4 PP2 -> TP4 PP1 with the alias plan.
+    PP-only, every destination tensor is a source tensor and the reshard moves nothing; with the fused
+    formats changed to separate ones as well, the qkv and gate/up tensors are copied and the embedding,
+    norms, o, down and LM head are aliased. Every destination tensor against the oracle; bytes read
+    drop by exactly the alias bytes."""
+    import torch
+
+    m = emu.Model(*EIGHT_B)
+    src = emu.Layout(m, 4, 2)
+    dst = emu.Layout(m, 4, 1, qkv="separate", mlp="separate") if mixed else emu.Layout(m, 4, 1)
+    full, p = emu.Plan(src, dst), emu.Plan(src, dst, alias=True)
+    assert p.info["bytes_read"] == full.info["bytes_read"] - p.info["alias_bytes"]
+    assert p.info["bytes_written"] == full.info["bytes_written"] - p.info["alias_bytes"]
+    if not mixed:
+        assert p.info["n_alias_tensors"] == p.info["n_dst_tensors"] and p.info["bytes_read"] == 0
+    ws = p.workspace()
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
+    fill_device(p, 0, S, seed=808)
+    make_consistent_replicas(p, 0, S)
+    D = p.alloc(1, fill=0xA5, guard=GUARD, alias=S)
+    own = [t for t, d in zip(D.tensors, p.tensors(1)) if d["alias"] < 0]
+    assert len(own) == p.info["n_dst_tensors"] - p.info["n_alias_tensors"]
+    guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(own, 0xA5)] if own else [],
+            f"8B alias plan {'mixed' if mixed else 'PP-only'}")
+    check_reshard(p, S, D, label=f"8B TP4PP2->TP4PP1 aliased ({'formats changed' if mixed else 'PP only'})")
+    say(f"  alias plan: {p.info['n_alias_tensors']} of {p.info['n_dst_tensors']} tensors aliased, "
+        f"{p.info['alias_bytes'] / 1e9:.2f} GB not copied, {p.info['bytes_read'] / 1e9:.2f} GB read")
+    del S, D, ws
+    cleanup()
+
+
 def regenerate(fwd, name, dist, seed):
     """The training-state group `name` as the fixture made it, in a fresh, identically laid out set."""
     ref = fwd.alloc(0, fill=0x5A, guard=GUARD)
@@ -309,8 +344,8 @@ def regenerate(fwd, name, dist, seed):
 
 @pytest.fixture(scope="module")
 def train_state(gpu_lib):
-    """fp32 master, Adam m and v in the TP4 PP1 layout, resharded to TP1 PP1 with one launch per group.
-    The sources must come out of the three launches unchanged (whole allocations, against a seeded
+    """fp32 master, Adam m and v in the TP4 PP1 layout, resharded to TP1 PP1 in one grouped launch.
+    The sources must come out of it unchanged (whole allocations, against a seeded
     regeneration) and the destination allocations untouched outside their views."""
     import torch
 
@@ -330,8 +365,8 @@ def train_state(gpu_lib):
     torch.cuda.synchronize()
     say(f"  fp32 state filled ({3 * fwd.info['src_bytes'] / 1e9:.1f} GB) in {time.time() - t:.1f} s")
     guards = [Guard(fills=[(D[name].tensors, 0xA5)], label=f"fp32 {name} TP4->TP1") for name in groups]
-    for name in groups:
-        fwd.reshard(wf, S[name].ptrs, D[name].ptrs)     # one launch per tensor group
+    # master, m and v in one launch (emu_reshard_groups); the back transition below takes one launch each
+    fwd.reshard_groups(wf, emu.group_tables([S[n] for n in groups]), emu.group_tables([D[n] for n in groups]))
     torch.cuda.synchronize()
     n = sum(g.check() for g in guards)
     for name, (dist, seed) in groups.items():

@@ -6,6 +6,7 @@ graph and replayed, format changes, padded vocabularies with zero-filled destina
 launch option, and bucket pack/unpack at awkward bucket sizes (including sizes that put source and
 bucket bytes at different 16-byte phases).
 """
+import ctypes
 import itertools
 
 import numpy as np
@@ -382,11 +383,18 @@ def test_execute_errors(gpu_lib):
     with pytest.raises(emu.EmuError) as e:
         emu.ptr_table([S.bufs[0][1:]])
     assert e.value.code == -7
-    # workspace registry: refused on the host, before anything is launched
+    # workspace registry: refused on the host, before anything is launched -- by the binding, which
+    # accepts only workspaces the plan uploaded to (and keeps alive), and by the library itself
     fresh = torch.empty(p.info["workspace_bytes"], dtype=torch.uint8, device="cuda")
     with pytest.raises(emu.EmuError) as e:
         p.reshard(fresh, S.ptrs, D.ptrs)                  # never uploaded
-    assert e.value.code == -5 and "emu_plan_upload" in str(e.value)
+    assert e.value.code == -5 and "Plan.upload" in str(e.value)
+    lib = emu.load()
+    V = ctypes.c_void_p
+    assert lib.emu_reshard(p._h, V(fresh.data_ptr()), V(S.ptrs.data_ptr()), V(D.ptrs.data_ptr()), None) == -5
+    assert b"emu_plan_upload" in lib.emu_last_error()
+    assert lib.emu_reshard(p._h, V(off.data_ptr()), V(S.ptrs.data_ptr()), V(D.ptrs.data_ptr()), None) == -5
+    assert b"aligned" in lib.emu_last_error()
     _, fresh_bptrs = p.alloc_buckets(1, 1 << 16)
     with pytest.raises(emu.EmuError) as e:
         p.pack(fresh, 1, 1 << 16, D.ptrs, fresh_bptrs)
@@ -642,3 +650,72 @@ def test_tensors_at_16_byte_offsets(gpu_lib, pair):
         assert torch.equal(a, b), f"fused bucket {k}"
     for i, (a, b) in enumerate(zip(D.tensors, R.tensors)):
         assert torch.equal(a, b), f"unpacked tensor {i}"
+
+
+@pytest.mark.parametrize("case", ["tiny", "zero_fill", "fp32_to_bf16"])
+def test_reshard_groups_small(gpu_lib, case):
+    """emu_reshard_groups: three shard sets of one plan (different contents) in one launch give what
+    three emu_reshard calls give, and each group's result matches the oracle; write footprints guarded."""
+    import torch
+
+    if case == "tiny":
+        m = emu.Model(*TINY)
+        src, dst = emu.Layout(m, 2, 2), emu.Layout(m, 1, 1, 0, "bf16", "separate", "block")
+    elif case == "zero_fill":                       # destination pad rows: the zero-fill instance runs too
+        m = emu.Model(2, 256, 4, 64, 2, 688, 1000)
+        src, dst = emu.Layout(m, 2, 1, 0), emu.Layout(m, 2, 2, 128)
+    else:
+        m = emu.Model(*TINY)
+        src, dst = emu.Layout(m, 1, 1, 0, "fp32"), emu.Layout(m, 2, 2, 0, "bf16")
+    plan = emu.Plan(src, dst)
+    ws = plan.workspace()
+    os_ = o_layout(src)
+    S = [plan.alloc(0, fill=0x5A, guard=GUARD) for _ in range(3)]
+    for k, s in enumerate(S):
+        upload_shards(oracle.shard(full_model(os_.model, 60 + k, src.dtype), os_), s, tp=src.tp)
+    G = [plan.alloc(1, fill=0xA5, guard=GUARD) for _ in range(3)]
+    ref = [plan.alloc(1, fill=0xA5, guard=GUARD) for _ in range(3)]
+    torch.cuda.synchronize()
+    g = Guard(keep=[t for s in S for t in s.tensors], fills=[(d.tensors, 0xA5) for d in G], label=f"groups {case}")
+    plan.reshard_groups(ws, emu.group_tables(S), emu.group_tables(G))
+    torch.cuda.synchronize()
+    g.check()
+    for s, r in zip(S, ref):
+        plan.reshard(ws, s.ptrs, r.ptrs)
+    torch.cuda.synchronize()
+    for k in range(3):
+        for i, (a, b) in enumerate(zip(G[k].bufs, ref[k].bufs)):
+            assert torch.equal(a, b), f"{case}: group {k} rank buffer {i} differs from emu_reshard"
+        check_reshard(plan, S[k], G[k], label=f"groups {case}, group {k}")
+    rc = emu.load().emu_reshard_groups(plan._h, ctypes.c_void_p(ws.data_ptr()), 0,
+                                       ctypes.c_void_p(S[0].ptrs.data_ptr()), ctypes.c_void_p(G[0].ptrs.data_ptr()), None)
+    assert rc == -10                                   # no group: refused on the host
+
+
+def test_alias_plans_small(gpu_lib):
+    """Plans that leave already-resident shards out (EMU_PLAN_ALIAS_RESIDENT): the destination set takes
+    the source tensors for its alias tensors and its own buffers for the rest; every destination tensor
+    matches the oracle, the kernel touches nothing outside the non-alias views, and the source is
+    unchanged. Micro layouts, PP-only and mixed changes."""
+    import torch
+
+    mm = emu.Model(*MICRO)
+    pairs = [(emu.Layout(mm, 2, 4), emu.Layout(mm, 2, 1)), (emu.Layout(mm, 4, 2, 2), emu.Layout(mm, 4, 1, 2)),
+             (emu.Layout(mm, 2, 2), emu.Layout(mm, 2, 1, 0, "bf16", "separate", "separate")),
+             (emu.Layout(mm, 1, 2), emu.Layout(mm, 4, 1)), (emu.Layout(mm, 2, 2, 0, "fp32"), emu.Layout(mm, 1, 4, 0, "fp32"))]
+    for src, dst in pairs:
+        plan = emu.Plan(src, dst, alias=True)
+        assert plan.info["n_alias_tensors"] > 0, (src, dst)
+        ws = plan.workspace()
+        os_ = o_layout(src)
+        S = plan.alloc(0, fill=0x5A, guard=GUARD)
+        upload_shards(oracle.shard(full_model(os_.model, 71, src.dtype), os_), S, tp=src.tp)
+        D = plan.alloc(1, fill=0xA5, guard=GUARD, alias=S)
+        own = [t for t, d in zip(D.tensors, plan.tensors(1)) if d["alias"] < 0]
+        g = Guard(keep=S.tensors, fills=[(own, 0xA5)] if own else [], label=f"alias {src} -> {dst}")
+        plan.reshard(ws, S.ptrs, D.ptrs)
+        torch.cuda.synchronize()
+        g.check()
+        if not own:
+            assert all(bool((b == 0xA5).all()) for b in D.bufs)
+        check_reshard(plan, S, D, label=f"alias {src.tp}x{src.pp} -> {dst.tp}x{dst.pp}")

@@ -38,7 +38,7 @@ def test_library_exports_every_declared_function():
     assert len(names) >= 14
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.emu_version() == 1
+    assert lib.emu_version() == 2
 
 
 def full_model(model, seed=11, dtype="bf16"):
@@ -223,6 +223,126 @@ def test_error_codes():
     assert lib.emu_set_option(8, 0) == -10 and lib.emu_set_option(emu.OPT_ROW_WRAP, 2) == -11
     for s in range(-11, 1):
         assert lib.emu_status_str(s).startswith(b"EMU_")
+
+
+def _expected_aliases(src, dst):
+    """Brute force from the oracle's per-element coordinates: destination tensor j is a whole copy of
+    source tensor i iff both hold the same logical elements in the same order (no pad rows), in the same
+    element type, and source tensor i is the first holder of every one of its elements (replicated
+    elements are read from their first holder: norms from TP rank 0, replicated KV heads from their
+    first rank)."""
+    from oracle import coords
+
+    if src.dtype != dst.dtype:
+        return None
+    sid = [tuple(ids) for rank in coords.element_ids(o_layout(src)) for ids in rank]
+    owner = {}
+    for i, ids in enumerate(sid):
+        for e in ids:
+            owner.setdefault(e, i)
+    clean = {ids: i for i, ids in enumerate(sid) if all(owner[e] == i for e in ids)}
+    out = []
+    for ids in (tuple(x) for rank in coords.element_ids(o_layout(dst)) for x in rank):
+        out.append(clean.get(ids, -1) if min(ids) >= 0 else -1)
+    return out
+
+
+def check_alias_pair(src, dst, seed=17):
+    """The alias plan against the oracle: alias tensors are exactly the brute-force whole copies, each
+    equals its source tensor in the oracle's reshard (with unequal norm replicas, so a wrong replica
+    shows), the map writes every other destination byte exactly once and nothing of an alias tensor,
+    and the read/write counts drop by the alias bytes."""
+    full_plan = emu.Plan(src, dst)
+    plan = emu.Plan(src, dst, alias=True)
+    descs = plan.tensors(1)
+    got_alias = [d["alias"] for d in descs]
+    assert got_alias == [d["alias"] for d in full_plan.tensors(1)]      # detection does not depend on the flag
+    want_alias = _expected_aliases(src, dst)
+    assert got_alias == (want_alias if want_alias is not None else [-1] * len(descs)), (src, dst)
+    os_, od = o_layout(src), o_layout(dst)
+    src_shards = oracle.shard(full_model(os_.model, seed, src.dtype), os_)
+    for r, specs in enumerate(oracle.rank_inventory(os_)):
+        for j, sp in enumerate(specs):
+            if sp.kind.endswith("norm") and r % os_.tp:
+                src_shards[r][j] = src_shards[r][j] + np.array(1, dtype=src_shards[r][j].dtype)
+    flat_src = [np.ascontiguousarray(a).reshape(-1).view(np.uint8) for rank in src_shards for a in rank]
+    want = [np.ascontiguousarray(a).reshape(-1).view(np.uint8) for rank in oracle.reshard(src_shards, os_, od)
+            for a in rank]
+    got = run_plan(plan.segments(), flat_src, [w.size for w in want])
+    cover = coverage(plan.segments(), [w.size for w in want])
+    nbytes = 0
+    for j, (g, w, a) in enumerate(zip(got, want, got_alias)):
+        if a >= 0:
+            assert np.array_equal(flat_src[a], w), (src, dst, j)
+            assert cover[j] == [], (src, dst, j)
+            nbytes += w.size
+        else:
+            assert np.array_equal(g, w), (src, dst, j)
+    info, full_info = plan.info, full_plan.info
+    assert info["aliased"] == 1 and full_info["aliased"] == 0
+    assert info["n_alias_tensors"] == full_info["n_alias_tensors"] == sum(a >= 0 for a in got_alias)
+    assert info["alias_bytes"] == full_info["alias_bytes"] == nbytes
+    assert info["bytes_written"] == full_info["bytes_written"] - nbytes
+    assert info["bytes_read"] == full_info["bytes_read"] - nbytes
+    return plan
+
+
+@pytest.mark.parametrize("i", range(0, len(MICRO_LAYS), 4))
+def test_alias_plans_match_oracle_micro(i):
+    src = MICRO_LAYS[i]
+    for dst in MICRO_LAYS[::3] + [src, emu.Layout(src.model, src.tp, 1, src.pad, src.dtype, src.qkv, src.mlp)]:
+        check_alias_pair(src, dst)
+
+
+def test_alias_kv_replication_uneven_pp_and_conversion():
+    m = emu.Model(3, 16, 8, 2, 2, 16, 16)
+    for a, b in ((emu.Layout(m, 8, 3), emu.Layout(m, 8, 1)), (emu.Layout(m, 4, 2), emu.Layout(m, 8, 3)),
+                 (emu.Layout(m, 2, 3, 2), emu.Layout(m, 2, 2, 2)), (emu.Layout(m, 2, 1), emu.Layout(m, 2, 1, 0, "fp32"))):
+        check_alias_pair(a, b)
+
+
+def test_alias_counts_8b():
+    """8B: a PP-only change aliases every destination tensor (nothing is copied); TP2 PP2 -> TP4 PP1
+    aliases every norm (each a whole copy of TP rank 0's norm of its layer's stage) and nothing else; a
+    PP-only change that also changes the fused formats aliases the tensors the formats leave alone."""
+    m = emu.Model(*EIGHT_B)
+    pp_only = emu.Plan(emu.Layout(m, 4, 2), emu.Layout(m, 4, 1), alias=True)
+    assert pp_only.info["n_alias_tensors"] == pp_only.info["n_dst_tensors"] == 780
+    assert pp_only.info["bytes_read"] == 0 and pp_only.info["n_tiles"] == 0
+    tp = emu.Plan(emu.Layout(m, 2, 2), emu.Layout(m, 4, 1), alias=True)
+    norms = [d for d in tp.tensors(1) if d["kind"].endswith("norm")]
+    assert tp.info["n_alias_tensors"] == len(norms) == 4 * (2 * 32 + 1)
+    mixed = emu.Plan(emu.Layout(m, 4, 2), emu.Layout(m, 4, 1, qkv="separate", mlp="separate"), alias=True)
+    kinds = {d["kind"] for d in mixed.tensors(1) if d["alias"] >= 0}
+    assert kinds == {"embed", "attn_norm", "o", "mlp_norm", "down", "final_norm", "lm_head"}
+
+
+@pytest.mark.parametrize("B", [2, 30, 4094, 65538, 1 << 20])
+def test_bucket_info_matches_oracle_pack(B):
+    """emu_bucket_info: each bucket's rank, index, stream offset and size equal what oracle.pack makes of
+    each destination rank's tensors; sub-ranges return the same entries; a range past the end fails."""
+    m = emu.Model(*TINY)
+    src, dst = emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 2, 0, "bf16", "separate", "block")
+    plan = emu.Plan(src, dst)
+    od = o_layout(dst)
+    want = []
+    for r, specs in enumerate(oracle.rank_inventory(od)):
+        tensors = [np.zeros(sp.shape, dtype=np.uint16) for sp in specs]
+        off = 0
+        for k, b in enumerate(oracle.pack(tensors, B)):
+            want.append(dict(rank=r, index=k, stream_offset=off, bytes=b.size))
+            off += b.size
+    got = plan.bucket_info(1, B)
+    assert got == want
+    n = len(want)
+    lib = emu.load()
+    arr = (emu.c_bucket_desc * 3)()
+    assert lib.emu_bucket_info(plan._h, 1, B, n - 3, 3, arr) == 0
+    assert [dict(rank=a.rank, index=a.index, stream_offset=a.stream_offset, bytes=a.bytes) for a in arr] == want[-3:]
+    assert lib.emu_bucket_info(plan._h, 1, B, n - 2, 3, arr) == -10
+    assert lib.emu_bucket_info(plan._h, 1, B, n, 0, arr) == 0
+    assert lib.emu_bucket_info(plan._h, 1, 3, 0, 1, arr) == -6
+    assert lib.emu_bucket_info(plan._h, 2, B, 0, 1, arr) == -10
 
 
 def test_noalloc_size_limit_is_checked_before_any_gpu_call():
