@@ -182,8 +182,7 @@ def tiny_latency(emu, iters=200):
 def variant_timings(emu, seed, reps=5):
     """Mean launch time of the layout variants on the 8B decoder (bf16), each on fresh buffers:
     the paper's T_sub route (TP4 PP8 -> TP4 PP2 -> TP8 PP2, section 6.1) against the direct
-    destination-driven TP4 PP8 -> TP8 PP2; KV replication with uneven stages (TP2 PP2 -> TP16 PP3); and
-    a format change to separate q/k/v and gate/up (TP2 PP2 -> TP4 PP1)."""
+    destination-driven TP4 PP8 -> TP8 PP2, and KV replication with uneven stages (TP2 PP2 -> TP16 PP3)."""
     import torch
 
     from synthetic import device_fill
@@ -227,8 +226,7 @@ def variant_timings(emu, seed, reps=5):
         "direct_ms": round(d_ms, 4), "direct_GBps": round(d_b / (d_ms * 1e-3) / 1e9, 1),
         "via_tp4pp2_ms": round(t_ms, 4), "via_tp4pp2_bytes_over_direct": round(t_b / d_b, 3),
         "outputs_equal": same}
-    for name, a, b in (("kv_replication_tp2pp2_to_tp16pp3", L(2, 2), L(16, 3)),
-                       ("formats_fused_tp2pp2_to_separate_tp4pp1", L(2, 2), L(4, 1, qkv="separate", mlp="separate"))):
+    for name, a, b in (("kv_replication_tp2pp2_to_tp16pp3", L(2, 2), L(16, 3)),):
         ms, moved, _, _ = run([(a, b)])
         out[name] = {"ms": round(ms, 4), "GBps": round(moved / (ms * 1e-3) / 1e9, 1)}
     return out
@@ -238,8 +236,9 @@ def bench_other_config(args, emu, torch, cfg):
     """The other workloads, one step each, timed like the default line:
     1 tiny bf16: Split TP1 PP1 -> TP2 PP1 and Merge back (cache-resident: latency);
     2 1B bf16: TP4 PP1 -> TP2 PP1;
-    4 8B fp32 training state (master, Adam m, Adam v): TP4 PP1 -> TP1 PP1, one launch per tensor group,
-      then split back, again one launch per group;
+    4 8B fp32 training state (master, Adam m, Adam v): TP4 PP1 -> TP1 PP1 as one launch over the three
+      tensor groups (emu_reshard_groups), then split back, again one launch; the same two transitions as
+      one launch per group are timed beside it, interleaved, on the same buffers;
     5 8B bf16, vocabulary padded to a multiple of 128 per TP rank: TP8 PP4 -> TP2 PP2, pack into
       2^28-byte buckets, unpack into a receiver set."""
     from synthetic import device_fill
@@ -247,7 +246,11 @@ def bench_other_config(args, emu, torch, cfg):
     def dists(plan, side):
         return ["norm" if d["kind"].endswith("norm") else "weight" for d in plan.tensors(side)]
 
-    calls = []        # (plan, workspace, fn(stream) -> None) in step order, the dominant one first
+    def moved(plan, groups=1):
+        return groups * (plan.info["bytes_read"] + plan.info["bytes_written"])
+
+    calls = []        # (name, algorithmic bytes, fn) in step order, the dominant one first
+    extra = {}
     keep = []
     if cfg in (1, 2):
         shape, a, b = (TINY, (1, 1), (2, 1)) if cfg == 1 else (ONE_B, (4, 1), (2, 1))
@@ -256,12 +259,12 @@ def bench_other_config(args, emu, torch, cfg):
         S, D = fwd.alloc(0), fwd.alloc(1)
         device_fill(S.tensors, args.seed, dists(fwd, 0), "bf16")
         wf = fwd.workspace()
-        calls.append(("reshard", fwd, lambda: fwd.reshard(wf, S.ptrs, D.ptrs)))
+        calls.append(("reshard", moved(fwd), lambda: fwd.reshard(wf, S.ptrs, D.ptrs)))
         if cfg == 1:
             back = emu.Plan(emu.Layout(m, *b), emu.Layout(m, *a))
             wb = back.workspace()
             A2 = back.alloc(1)
-            calls.append(("reshard back", back, lambda: back.reshard(wb, D.ptrs, A2.ptrs)))
+            calls.append(("reshard back", moved(back), lambda: back.reshard(wb, D.ptrs, A2.ptrs)))
             keep.append(A2)
         keep += [S, D]
         workload = ("tiny decoder bf16: Split TP1PP1->TP2PP1, then Merge back" if cfg == 1 else
@@ -272,15 +275,27 @@ def bench_other_config(args, emu, torch, cfg):
         fwd = emu.Plan(emu.Layout(m, 4, 1, 0, "fp32"), emu.Layout(m, 1, 1, 0, "fp32"))
         back = emu.Plan(emu.Layout(m, 1, 1, 0, "fp32"), emu.Layout(m, 4, 1, 0, "fp32"))
         wf, wb = fwd.workspace(), back.workspace()
+        Ss, Ds = [], []
         for gi, dist in enumerate(("weight", "adam_m", "adam_v")):
             S, D = fwd.alloc(0), fwd.alloc(1)
             device_fill(S.tensors, args.seed + gi, [dist] * len(S.tensors), "fp32")
-            keep += [S, D]
-            calls.append((f"group {gi} TP4->TP1", fwd, lambda S=S, D=D: fwd.reshard(wf, S.ptrs, D.ptrs)))
-        for gi in range(3):
-            S, D = keep[2 * gi], keep[2 * gi + 1]
-            calls.append((f"group {gi} TP1->TP4", back, lambda S=S, D=D: back.reshard(wb, D.ptrs, S.ptrs)))
-        workload = "8B training state fp32 (master, Adam m, Adam v): TP4PP1->TP1PP1 and back, one launch per group"
+            Ss.append(S)
+            Ds.append(D)
+        st, dt = emu.group_tables(Ss), emu.group_tables(Ds)
+        keep += Ss + Ds + [st, dt]
+        calls += [("master+m+v TP4->TP1, one launch", moved(fwd, 3), lambda: fwd.reshard_groups(wf, st, dt)),
+                  ("master+m+v TP1->TP4, one launch", moved(back, 3), lambda: back.reshard_groups(wb, dt, st))]
+
+        def per_group(plan, w, xs, ys):
+            def run():
+                for x, y in zip(xs, ys):
+                    plan.reshard(w, x.ptrs, y.ptrs)
+            return run
+
+        extra["per_group_launches"] = (per_group(fwd, wf, Ss, Ds), per_group(back, wb, Ds, Ss),
+                                       lambda: fwd.reshard_groups(wf, st, dt), lambda: back.reshard_groups(wb, dt, st))
+        workload = ("8B training state fp32 (master, Adam m, Adam v): TP4PP1->TP1PP1 and back, each direction one "
+                    "launch over the three tensor groups")
         model_s = "L32 H4096 32x128 heads 8 KV MLP14336 V128256"
     elif cfg == 5:
         m = emu.Model(*EIGHT_B)
@@ -291,39 +306,35 @@ def bench_other_config(args, emu, torch, cfg):
         B = args.bucket_bytes
         bufs, bptrs = plan.alloc_buckets(1, B)
         keep += [S, D, R, bufs]
-        calls += [("reshard", plan, lambda: plan.reshard(ws, S.ptrs, D.ptrs)),
-                  ("pack", plan, lambda: plan.pack(ws, 1, B, D.ptrs, bptrs)),
-                  ("unpack", plan, lambda: plan.unpack(ws, 1, B, bptrs, R.ptrs))]
+        nb = 2 * plan.bucket_layout(1, B, -1)[1]
+        calls += [("reshard", moved(plan), lambda: plan.reshard(ws, S.ptrs, D.ptrs)),
+                  ("pack", nb, lambda: plan.pack(ws, 1, B, D.ptrs, bptrs)),
+                  ("unpack", nb, lambda: plan.unpack(ws, 1, B, bptrs, R.ptrs))]
         workload = "8B decoder bf16, vocab padded to TP*128: reshard TP8PP4->TP2PP2 + pack into 2^28-byte buckets + unpack"
         model_s = "L32 H4096 32x128 heads 8 KV MLP14336 V128256"
     else:
         raise SystemExit(f"unknown config {cfg}")
     torch.cuda.synchronize()
 
-    def nbytes(name, plan):
-        if name in ("pack", "unpack"):
-            return 2 * plan.bucket_layout(1, args.bucket_bytes, -1)[1]
-        return plan.info["bytes_read"] + plan.info["bytes_written"]
-
     for _ in range(args.warmup):
-        for _n, _p, fn in calls:
+        for _n, _b, fn in calls:
             fn()
     torch.cuda.synchronize()
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)] for _ in range(args.steps)]
     t0 = time.perf_counter()
     for k in range(args.steps):
         evs[k][0].record()
-        for j, (_n, _p, fn) in enumerate(calls):
+        for j, (_n, _b, fn) in enumerate(calls):
             fn()
             evs[k][j + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     per = [sorted(e[j].elapsed_time(e[j + 1]) for e in evs) for j in range(len(calls))]
-    step_bytes = sum(nbytes(n, p) for n, p, _ in calls)
+    step_bytes = sum(b for _n, b, _ in calls)
     ms_per_step = wall * 1e3 / args.steps
     r_ms = per[0]
     r_avg = sum(r_ms) / len(r_ms)
-    r_bytes = nbytes(calls[0][0], calls[0][1])
+    r_bytes = calls[0][1]
     achieved = r_bytes / (r_avg * 1e-3) / 1e9
     props = torch.cuda.get_device_properties(0)
     out = {
@@ -337,8 +348,8 @@ def bench_other_config(args, emu, torch, cfg):
         "config": {"workload": workload, "decoder_shape": model_s, "bytes_per_step": step_bytes,
                    "parallelism": "none (1 GPU holds all ranks' shards)", "config_id": cfg},
         "launches": [{"name": n, "mean_ms": round(sum(t) / len(t), 4), "median_ms": round(t[len(t) // 2], 4),
-                      "GBps": round(nbytes(n, p) / (sum(t) / len(t) * 1e-3) / 1e9, 1)}
-                     for (n, p, _), t in zip(calls, per)],
+                      "GBps": round(b / (sum(t) / len(t) * 1e-3) / 1e9, 1)}
+                     for (n, b, _), t in zip(calls, per)],
         "roofline": {"bound": "hbm", "kernel": "k_reshard", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
                      "algorithmic_bytes_per_launch": r_bytes},
@@ -347,6 +358,22 @@ def bench_other_config(args, emu, torch, cfg):
         "seed": args.seed,
         "cpu_baseline": None,
     }
+    if "per_group_launches" in extra:
+        f3, b3, f1, b1 = extra["per_group_launches"]
+        reps = max(3, args.steps // 2)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(reps)]
+        torch.cuda.synchronize()
+        for k in range(reps):
+            for j, fn in enumerate((f3, f1, b3, b1)):
+                ev[k][j].record()
+                fn()
+            ev[k][4].record()
+        torch.cuda.synchronize()
+        med = lambda j: sorted(e[j].elapsed_time(e[j + 1]) for e in ev)[reps // 2]
+        out["one_launch_vs_three"] = {
+            "tp4_to_tp1_three_launches_ms": round(med(0), 4), "tp4_to_tp1_one_launch_ms": round(med(1), 4),
+            "tp1_to_tp4_three_launches_ms": round(med(2), 4), "tp1_to_tp4_one_launch_ms": round(med(3), 4),
+            "note": "interleaved on the same buffers, medians"}
     if cfg == 1:
         out["note"] = "3.95 MB of destination shards: cache-resident and latency-bound; read ms_per_step, not GB/s"
     del keep
@@ -417,24 +444,41 @@ def main():
     dev = torch.device("cuda", 0)
     props = torch.cuda.get_device_properties(dev)
     model = emu.Model(*EIGHT_B)
-    src, dst = emu.Layout(model, 2, 2), emu.Layout(model, 4, 1)
+    L = lambda tp, pp, **kw: emu.Layout(model, tp, pp, **kw)
+    src, dst = L(2, 2), L(4, 1)
     B = args.bucket_bytes
+    Bs = B - 2                       # phase-shifted buckets: every bucket starts at another 16-byte phase
 
     t = time.perf_counter()
     plan = emu.Plan(src, dst)
     plan_ms = (time.perf_counter() - t) * 1e3
     info = plan.info
     log(f"plan: {info['n_segments']} segments, {info['n_tiles']} tiles, {plan_ms:.2f} ms")
+    # plans that share the benchmark's memory pages: the identity plan (same destination layout,
+    # contiguous copies: the copy ceiling), the same transition into separate q/k/v and gate/up tensors,
+    # and the PP-only change TP4 PP2 -> TP4 PP1 with and without aliasing of resident shards
+    ident = emu.Plan(dst, dst)
+    fmt = emu.Plan(src, L(4, 1, qkv="separate", mlp="separate"))
+    pp_copy, pp_alias = emu.Plan(L(4, 2), dst), emu.Plan(L(4, 2), dst, alias=True)
 
-    ws = plan.workspace(dev)
-    S = plan.alloc(0, dev)
-    D = plan.alloc(1, dev)
+    def region(n):
+        return torch.empty(n, dtype=torch.uint8, device=dev)
+
+    src_region = region(max(p.region_bytes(0) for p in (plan, ident, pp_copy)))
+    dst_region = region(max(p.region_bytes(1) for p in (plan, fmt)))
+    bucket_region = region(max(plan.bucket_region_bytes(1, b) for b in (B, Bs)))
+    S, SI, SP = plan.views(0, src_region), ident.views(0, src_region), pp_copy.views(0, src_region)
+    D, DF = plan.views(1, dst_region), fmt.views(1, dst_region)
+    DA = pp_alias.views(1, dst_region, alias=SP)
     R = plan.alloc(1, dev)
-    bufs, bptrs = plan.alloc_buckets(1, B, dev)
+    bufs, bptrs = plan.bucket_views(1, B, bucket_region)
+    sbufs, sbptrs = plan.bucket_views(1, Bs, bucket_region)
+    ws, wsi, wsf = plan.workspace(dev), ident.workspace(dev), fmt.workspace(dev)
+    wpc, wpa = pp_copy.workspace(dev), pp_alias.workspace(dev)
     sdesc = plan.tensors(0)
     device_fill(S.tensors, args.seed, ["norm" if d["kind"].endswith("norm") else "weight" for d in sdesc], "bf16")
     torch.cuda.synchronize()
-    log(f"resident: {(sum(b.numel() for b in S.bufs + D.bufs + R.bufs) + sum(b.numel() for b in bufs)) / 1e9:.1f} GB")
+    log(f"resident: {(src_region.numel() + dst_region.numel() + bucket_region.numel() + sum(b.numel() for b in R.bufs)) / 1e9:.1f} GB")
 
     reshard_bytes = info["bytes_read"] + info["bytes_written"]
     _, stream_bytes = plan.bucket_layout(1, B, -1)
@@ -469,27 +513,53 @@ def main():
     u_ms = sorted(e[2].elapsed_time(e[3]) for e in evs)
     mean = lambda x: sum(x) / len(x)
     med = lambda x: x[len(x) // 2]
-    ok = all(torch.equal(a, b) for a, b in zip(D.bufs, R.bufs))
+    ok = all(torch.equal(a, b) for a, b in zip(D.tensors, R.tensors))
+
+    def interleaved(fns, reps=args.steps):
+        """Median ms of each callable over `reps` rounds, the callables alternating within a round (one
+        stream, HIP events around each launch), so that they share time-varying device state."""
+        for fn in fns:
+            fn()
+        ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+              for _ in fns]
+        torch.cuda.synchronize()
+        for k in range(reps):
+            for j, fn in enumerate(fns):
+                ev[j][k][0].record()
+                fn()
+                ev[j][k][1].record()
+        torch.cuda.synchronize()
+        return [med(sorted(a.elapsed_time(b) for a, b in e)) for e in ev]
+
+    # copy ceiling: the identity plan reads the same source pages and writes the same destination pages
+    id_ms, rs_ms = interleaved([lambda: ident.reshard(wsi, SI.ptrs, D.ptrs), lambda: plan.reshard(ws, S.ptrs, D.ptrs)])
+    id_bytes = ident.info["bytes_read"] + ident.info["bytes_written"]
+    # phase-shifted buckets against aligned ones, on the same bucket pages; the last unpack is checked
+    pk_a, up_a, pk_s, up_s = interleaved([lambda: plan.pack(ws, 1, B, D.ptrs, bptrs),
+                                          lambda: plan.unpack(ws, 1, B, bptrs, R.ptrs),
+                                          lambda: plan.pack(ws, 1, Bs, D.ptrs, sbptrs),
+                                          lambda: plan.unpack(ws, 1, Bs, sbptrs, R.ptrs)])
+    shifted_ok = all(torch.equal(a, b) for a, b in zip(D.tensors, R.tensors))
 
     # fused sender path: source shards straight into the buckets (one pass instead of reshard + pack)
     fused = emu.Plan(src, dst, bucket_bytes=B)
     wf = fused.workspace(dev)
-    for _ in range(args.warmup):
-        fused.reshard(wf, S.ptrs, bptrs)
-    fev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    fev[0].record()
-    for k in range(args.steps):
-        fused.reshard(wf, S.ptrs, bptrs)
-        fev[k + 1].record()
-    torch.cuda.synchronize()
-    f_ms = sorted(fev[k].elapsed_time(fev[k + 1]) for k in range(args.steps))
+    (f_ms,) = interleaved([lambda: fused.reshard(wf, S.ptrs, bptrs)])
     for b in R.bufs:
         b.zero_()
     plan.unpack(ws, 1, B, bptrs, R.ptrs)
     torch.cuda.synchronize()
-    fused_ok = all(torch.equal(a, b) for a, b in zip(D.bufs, R.bufs))
+    fused_ok = all(torch.equal(a, b) for a, b in zip(D.tensors, R.tensors))
     fused_bytes = fused.info["bytes_read"] + fused.info["bytes_written"]
+
+    # format change (training -> generation layout of q/k/v and gate/up) against the same transition
+    # without it, on the same source and destination pages
+    fm_ms, base_ms = interleaved([lambda: fmt.reshard(wsf, S.ptrs, DF.ptrs), lambda: plan.reshard(ws, S.ptrs, D.ptrs)])
+    fmt_bytes = fmt.info["bytes_read"] + fmt.info["bytes_written"]
+    # resident shards aliased: the PP-only change copies nothing when its shards stay where they are
+    pc_ms, pa_ms = interleaved([lambda: pp_copy.reshard(wpc, SP.ptrs, D.ptrs),
+                                lambda: pp_alias.reshard(wpa, SP.ptrs, DA.ptrs)])
+    alias_ok = all(torch.equal(a, b) for a, b in zip(D.tensors, DA.tensors))
 
     # weight sync from a training stage to a generation stage: fp32 TP4 PP1 master -> bf16 TP2 PP2
     # (layout change and round-to-nearest-even conversion in one pass)
@@ -499,36 +569,29 @@ def main():
     device_fill(SY.tensors, args.seed + 1, ["norm" if d["kind"].endswith("norm") else "weight"
                                             for d in sync.tensors(0)], "fp32")
     DY = sync.alloc(1, dev)
-    for _ in range(args.warmup):
-        sync.reshard(wsy, SY.ptrs, DY.ptrs)
-    sev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    torch.cuda.synchronize()
-    sev[0].record()
-    for k in range(args.steps):
-        sync.reshard(wsy, SY.ptrs, DY.ptrs)
-        sev[k + 1].record()
-    torch.cuda.synchronize()
-    sync_ms = sum(sev[k].elapsed_time(sev[k + 1]) for k in range(args.steps)) / args.steps
+    (sync_ms,) = interleaved([lambda: sync.reshard(wsy, SY.ptrs, DY.ptrs)])
     sync_bytes = sync.info["bytes_read"] + sync.info["bytes_written"]
     del SY, DY, wsy
 
-    # plain device copy of the same destination bytes (torch copy_), as a practical ceiling
+    # the runtime's blit copy of the destination bytes (torch copy_), for reference: not a ceiling
+    pairs = [(a, b) for a, b in zip(D.tensors, R.tensors)]
     cev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    for b_src, b_dst in zip(D.bufs, R.bufs):
-        b_dst.copy_(b_src)
+    for a, b in pairs:
+        b.copy_(a)
     cev[0].record()
     reps = 5
     for _ in range(reps):
-        for b_src, b_dst in zip(D.bufs, R.bufs):
-            b_dst.copy_(b_src)
+        for a, b in pairs:
+            b.copy_(a)
     cev[1].record()
     torch.cuda.synchronize()
-    copy_ms = cev[0].elapsed_time(cev[1]) / reps
-    copy_bytes = 2 * sum(b.numel() for b in D.bufs)
+    blit_ms = cev[0].elapsed_time(cev[1]) / reps
+    blit_bytes = 2 * sum(a.numel() for a, _ in pairs)
 
     ms_per_step = wall * 1e3 / args.steps
     reshard_avg = mean(r_ms)
     achieved = reshard_bytes / (reshard_avg * 1e-3) / 1e9
+    gbps = lambda nbytes, ms: round(nbytes / (ms * 1e-3) / 1e9, 1)
     traffic = measured_traffic()
     out = {
         "metric": "reshard HBM GB/s (bytes read+written) and ms per 8B transition, % of HBM peak",
@@ -556,18 +619,39 @@ def main():
         "reshard_pct_of_peak": round(100 * achieved / HBM_PEAK_GBPS, 2),
         "pack_ms": round(mean(p_ms), 4),
         "unpack_ms": round(mean(u_ms), 4),
-        "pack_GBps": round(bucket_bytes_rw / (mean(p_ms) * 1e-3) / 1e9, 1),
-        "unpack_GBps": round(bucket_bytes_rw / (mean(u_ms) * 1e-3) / 1e9, 1),
+        "pack_GBps": gbps(bucket_bytes_rw, mean(p_ms)),
+        "unpack_GBps": gbps(bucket_bytes_rw, mean(u_ms)),
         "transition_ms": round(reshard_avg + mean(p_ms) + mean(u_ms), 4),
-        "fused_reshard_to_buckets_ms": round(mean(f_ms), 4),
-        "fused_reshard_to_buckets_GBps": round(fused_bytes / (mean(f_ms) * 1e-3) / 1e9, 1),
-        "fused_vs_reshard_plus_pack": round((reshard_avg + mean(p_ms)) / mean(f_ms), 3),
+        "identity_copy_ms": round(id_ms, 4),
+        "identity_copy_GBps": gbps(id_bytes, id_ms),
+        "reshard_interleaved_ms": round(rs_ms, 4),
+        "reshard_over_identity": round(rs_ms / id_ms, 4),
+        "phase_shifted_bucket_bytes": Bs,
+        "pack_aligned_interleaved_ms": round(pk_a, 4),
+        "unpack_aligned_interleaved_ms": round(up_a, 4),
+        "pack_phase_shifted_ms": round(pk_s, 4),
+        "unpack_phase_shifted_ms": round(up_s, 4),
+        "pack_phase_shifted_pct_of_peak": round(100 * bucket_bytes_rw / (pk_s * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
+        "unpack_phase_shifted_pct_of_peak": round(100 * bucket_bytes_rw / (up_s * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
+        "pack_aligned_interleaved_pct_of_peak": round(100 * bucket_bytes_rw / (pk_a * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
+        "unpack_aligned_interleaved_pct_of_peak": round(100 * bucket_bytes_rw / (up_a * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
+        "phase_shifted_outputs_consistent": shifted_ok,
+        "fused_reshard_to_buckets_ms": round(f_ms, 4),
+        "fused_reshard_to_buckets_GBps": gbps(fused_bytes, f_ms),
+        "fused_vs_reshard_plus_pack": round((reshard_avg + mean(p_ms)) / f_ms, 3),
         "fused_outputs_consistent": fused_ok,
+        "formats_fused_to_separate_tp2pp2_to_tp4pp1": {
+            "ms": round(fm_ms, 4), "GBps": gbps(fmt_bytes, fm_ms), "same_pages_fused_to_fused_ms": round(base_ms, 4),
+            "ratio": round(fm_ms / base_ms, 4)},
+        "alias_resident_pp_only_tp4pp2_to_tp4pp1": {
+            "copy_ms": round(pc_ms, 4), "copy_GBps": gbps(pp_copy.info["bytes_read"] + pp_copy.info["bytes_written"], pc_ms),
+            "aliased_ms": round(pa_ms, 4), "aliased_bytes_moved": pp_alias.info["bytes_read"] + pp_alias.info["bytes_written"],
+            "alias_tensors": pp_alias.info["n_alias_tensors"], "outputs_equal": alias_ok},
         "weight_sync_fp32_tp4pp1_to_bf16_tp2pp2_ms": round(sync_ms, 4),
-        "weight_sync_GBps": round(sync_bytes / (sync_ms * 1e-3) / 1e9, 1),
+        "weight_sync_GBps": gbps(sync_bytes, sync_ms),
         "plan_compile_ms": round(plan_ms, 3),
         "transition_dag_1024_gpus": dag_planning(emu),
-        "copy_ceiling_GBps": round(copy_bytes / (copy_ms * 1e-3) / 1e9, 1),
+        "blit_copy_GBps": gbps(blit_bytes, blit_ms),
         "roofline": {
             "bound": "hbm",
             "kernel": "k_reshard",
@@ -591,7 +675,7 @@ def main():
         "outputs_consistent": ok,
         "seed": args.seed,
     }
-    del S, D, R, bufs
+    del S, SI, SP, D, DF, DA, R, bufs, sbufs, src_region, dst_region, bucket_region
     torch.cuda.empty_cache()
     out["tiny_transition_latency"] = tiny_latency(emu)
     log("timing the layout variants ...")

@@ -371,6 +371,51 @@ class Plan:
                    for d, o, mine in zip(descs, offs, own)]
         return ShardSet(bufs, tensors, ptr_table(tensors, device))
 
+    def region_bytes(self, side: int) -> int:
+        """Bytes ``views`` needs to lay out one side's tensors back to back (256-byte aligned)."""
+        end = 0
+        for d in self.tensors(side):
+            end = (end + 255) // 256 * 256 + d["bytes"]
+        return end
+
+    def views(self, side: int, region, device=None, alias: ShardSet = None) -> ShardSet:
+        """One side's tensors as 256-byte aligned views laid out back to back in a caller-provided uint8
+        device tensor of at least ``region_bytes(side)`` bytes (several plans may place their tensors in one
+        region, so that their launches touch the same memory pages). alias=S as for ``alloc``."""
+        need = self.region_bytes(side)
+        if region.numel() < need:
+            raise ValueError(f"region of {region.numel()} bytes, the side needs {need}")
+        if alias is not None and (side != 1 or not self.info["aliased"]):
+            raise ValueError("alias= needs the destination side of a plan made with alias=True")
+        tensors, end = [], 0
+        for d in self.tensors(side):
+            if alias is not None and d["alias"] >= 0:
+                tensors.append(alias.tensors[d["alias"]])
+                continue
+            o = (end + 255) // 256 * 256
+            tensors.append(region[o:o + d["bytes"]])
+            end = o + d["bytes"]
+        return ShardSet([region], tensors, ptr_table(tensors, device))
+
+    def bucket_region_bytes(self, side: int, bucket_bytes: int) -> int:
+        """Bytes ``bucket_views`` needs for one side's buckets of size bucket_bytes."""
+        end = 0
+        for b in self.bucket_info(side, bucket_bytes):
+            end = (end + 255) // 256 * 256 + b["bytes"]
+        return end
+
+    def bucket_views(self, side: int, bucket_bytes: int, region, device=None):
+        """One side's buckets of size bucket_bytes as 256-byte aligned views back to back in `region`
+        (as ``views``); returns (buckets, pointer table)."""
+        bufs, end = [], 0
+        for b in self.bucket_info(side, bucket_bytes):
+            o = (end + 255) // 256 * 256
+            if o + b["bytes"] > region.numel():
+                raise ValueError("region too small for the buckets")
+            bufs.append(region[o:o + b["bytes"]])
+            end = o + b["bytes"]
+        return bufs, ptr_table(bufs, device)
+
     def alloc_buckets(self, side: int, bucket_bytes: int, device=None, fill=None, guard: int = 0):
         """Bucket buffers for one side (rank 0's first) and their pointer table. The buckets are
         256-byte aligned views of one backing allocation, separated by at least `guard` bytes (as in
