@@ -534,11 +534,25 @@ def main():
     # copy ceiling: the identity plan reads the same source pages and writes the same destination pages
     id_ms, rs_ms = interleaved([lambda: ident.reshard(wsi, SI.ptrs, D.ptrs), lambda: plan.reshard(ws, S.ptrs, D.ptrs)])
     id_bytes = ident.info["bytes_read"] + ident.info["bytes_written"]
-    # phase-shifted buckets against aligned ones, on the same bucket pages; the last unpack is checked
-    pk_a, up_a, pk_s, up_s = interleaved([lambda: plan.pack(ws, 1, B, D.ptrs, bptrs),
-                                          lambda: plan.unpack(ws, 1, B, bptrs, R.ptrs),
-                                          lambda: plan.pack(ws, 1, Bs, D.ptrs, sbptrs),
-                                          lambda: plan.unpack(ws, 1, Bs, sbptrs, R.ptrs)])
+    def persistent(fn):
+        # the pack/unpack kernel that finds stream offsets with an on-device wave64 scan of each rank's
+        # tensor sizes instead of reading the upload-time chunk map
+        def run():
+            emu.set_option(emu.OPT_BUCKET_TILES, 0)
+            try:
+                fn()
+            finally:
+                emu.set_option(emu.OPT_BUCKET_TILES, 1)
+        return run
+
+    # phase-shifted buckets against aligned ones, and the device-scan kernel, on the same bucket pages;
+    # the last unpack (phase-shifted) is checked
+    pk_a, up_a, pk_d, up_d, pk_s, up_s = interleaved([lambda: plan.pack(ws, 1, B, D.ptrs, bptrs),
+                                                      lambda: plan.unpack(ws, 1, B, bptrs, R.ptrs),
+                                                      persistent(lambda: plan.pack(ws, 1, B, D.ptrs, bptrs)),
+                                                      persistent(lambda: plan.unpack(ws, 1, B, bptrs, R.ptrs)),
+                                                      lambda: plan.pack(ws, 1, Bs, D.ptrs, sbptrs),
+                                                      lambda: plan.unpack(ws, 1, Bs, sbptrs, R.ptrs)])
     shifted_ok = all(torch.equal(a, b) for a, b in zip(D.tensors, R.tensors))
 
     # fused sender path: source shards straight into the buckets (one pass instead of reshard + pack)
@@ -636,6 +650,8 @@ def main():
         "pack_aligned_interleaved_pct_of_peak": round(100 * bucket_bytes_rw / (pk_a * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
         "unpack_aligned_interleaved_pct_of_peak": round(100 * bucket_bytes_rw / (up_a * 1e-3) / 1e9 / HBM_PEAK_GBPS, 2),
         "phase_shifted_outputs_consistent": shifted_ok,
+        "pack_device_scan_ms": round(pk_d, 4),
+        "unpack_device_scan_ms": round(up_d, 4),
         "fused_reshard_to_buckets_ms": round(f_ms, 4),
         "fused_reshard_to_buckets_GBps": gbps(fused_bytes, f_ms),
         "fused_vs_reshard_plus_pack": round((reshard_avg + mean(p_ms)) / f_ms, 3),

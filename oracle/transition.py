@@ -1,18 +1,18 @@
 """Transition DAG between two plans, and its critical-path cost (test infrastructure; see package header).
 
-Paper anchors (section 6.1, decomposition and DAG construction; section 6 introduction for the cost):
-  * For each model-stage, the change between the current and the target EMU collection becomes a local
-    DAG in the fixed order Split -> Destroy -> Extend -> Merge. The engine first finds the largest TP/PP
-    layout T_sub into which both the current and the target units can be split, splits the current units
-    into T_sub units, destroys redundant units, extends replicas onto the target GPUs (a unit with no
-    other replica is destroyed only after an Extend has copied it), and merges the T_sub units into the
-    target layout.
-  * Local DAGs are combined with resource-dependency edges: when an acquisition is blocked by GPUs that
-    another model-stage still holds, the Destroy that releases them is made a predecessor, unless that
-    Destroy depends (directly or transitively) on the blocked acquisition -- then the target plan is
-    infeasible. Resource-releasing primitives are preferred, ties broken in generation -> inference ->
-    training order.
-  * The DAG's critical-path cost L_tran is estimated from bytes, link bandwidth and communicator setup.
+What is implemented, as this module reads section 6.1 (decomposition and DAG construction) and the
+section 6 introduction (cost):
+  * Per model-stage, four phases run in a fixed order: Split, Destroy, Extend, Merge. The common layout
+    T_sub is the largest TP/PP layout that both the current and the target unit layouts divide into;
+    current units are cut into T_sub units, surplus ones are released, missing ones are copied onto target
+    GPUs, and the T_sub units are assembled into target units. A unit that is the only holder of its state
+    is released only after the copy that needs it (an edge from that Extend to that Destroy).
+  * Model-stages hand GPUs to each other through resource edges: an acquisition of GPUs another
+    model-stage still holds waits for the Destroy that frees them. If that Destroy itself waits, directly
+    or through other edges, on the acquisition, the plan has no deadlock-free order and is rejected.
+    Releases are favoured, and equal cases are ordered generation, inference, training.
+  * L_tran, the cost of the DAG's longest path, comes from the bytes moved, link bandwidth and
+    communicator setup.
 
 Readings (the paper gives no algorithm listing):
   * T_sub = (gcd(tp, tp*), gcd(pp, pp*)). Splitting a unit of layout (tp, pp) into T_sub units yields
