@@ -256,8 +256,12 @@ int emu_tensor_info(emu_plan_t plan, int32_t side, int32_t index, emu_tensor_des
 /* Copy `count` segments starting at `first` (in execution order) into out[]. */
 int emu_plan_segments(emu_plan_t plan, int64_t first, int64_t count, emu_segment_t* out);
 
-/* Enqueue the host-to-device copy of the plan's tables into the caller's workspace (at least
- * info.workspace_bytes, 256-byte aligned). The plan must outlive the copy. The source is pageable host
+/* Fill the caller's workspace (at least info.workspace_bytes, 256-byte aligned) with the plan's tables:
+ * enqueue the host-to-device copy of the tables the host computes (the copy map, tensor sizes, each rank's
+ * tensor range and stream length), then two small kernels that derive the bucket kernels' tables from them
+ * on the device (each tensor's offset in its rank's stream, per-rank records, and the map from every 4 KB
+ * chunk of a stream to its rank and tensor). emu_plan_workspace_image gives the resulting bytes. The plan
+ * must outlive the copy. The source is pageable host
  * memory, so the HIP runtime may return only once the stream has reached the copy. The library records that
  * this address now holds this plan's tables: execute calls of the plan accept only a workspace address so
  * recorded (EMU_ERR_WORKSPACE otherwise, before anything is launched), and an upload of another plan to
@@ -265,6 +269,10 @@ int emu_plan_segments(emu_plan_t plan, int64_t first, int64_t count, emu_segment
  * keeps the workspace allocated, and unwritten by anything but emu_plan_upload, while it uses it (a
  * buffer freed and a new one allocated at the same address would pass for the upload). */
 int emu_plan_upload(emu_plan_t plan, void* d_workspace, uint64_t workspace_bytes, void* hip_stream);
+/* The workspace contents emu_plan_upload produces, computed on the host into out[0, info.workspace_bytes)
+ * (bytes smaller than that: EMU_ERR_WORKSPACE), for checking an uploaded workspace byte for byte. Gaps
+ * between the tables are zero here and unspecified in the uploaded workspace. Host only. */
+int emu_plan_workspace_image(emu_plan_t plan, void* out, uint64_t bytes);
 
 /* Execute the reshard (section 5.2 (a)/(b), the local layout change of section 6.2):
  * d_src_ptrs[i] is the device address of source tensor i, d_dst_ptrs[j] of destination tensor j

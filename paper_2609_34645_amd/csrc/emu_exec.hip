@@ -741,6 +741,72 @@ __global__ __launch_bounds__(kBucketTileThreads, EMU_RESHARD_WAVES_PER_EU) void 
 }
 
 // ------------------------------------------------------------------------------------------------
+// upload-time stream tables
+// ------------------------------------------------------------------------------------------------
+// emu_plan_upload copies the host tables (tensor sizes, each rank's tensor range and stream length) and
+// derives the bucket kernel's tables from them on the device. k_stream_tables, one wave64 per rank: the
+// exclusive prefix sum of the rank's tensor sizes (each tensor's stream offset), and the rank's record
+// {first 4 KB chunk, stream bytes, end of its tensor range, 0}, whose first chunk is the sum over earlier
+// ranks of ceil(bytes / 4 KB).
+__global__ __launch_bounds__(64) void k_stream_tables(const uint64_t* __restrict__ sizes,
+                                                      const uint32_t* __restrict__ rank_first,
+                                                      const uint64_t* __restrict__ rank_bytes,
+                                                      uint64_t* __restrict__ stream_off,
+                                                      uint64_t* __restrict__ rank_info) {
+  const uint32_t r = blockIdx.x, lane = threadIdx.x;
+  const uint32_t t0 = rank_first[r], t1 = rank_first[r + 1];
+  uint64_t carry = 0;
+  for (uint32_t base = t0; base < t1; base += 64) {
+    const uint32_t i = base + lane;
+    const uint64_t v = i < t1 ? sizes[i] : 0;
+    const uint64_t incl = wave_incl_scan(v, lane);
+    if (i < t1) stream_off[i] = carry + incl - v;
+    carry += __shfl(incl, 63, 64);
+  }
+  uint64_t acc = 0;
+  for (uint32_t q = lane; q < r; q += 64) acc += (rank_bytes[q] + kTileChunkBytes - 1) / kTileChunkBytes;
+  acc = wave_sum(acc);
+  if (lane == 0) {
+    rank_info[4 * r + 0] = acc;
+    rank_info[4 * r + 1] = rank_bytes[r];
+    rank_info[4 * r + 2] = t1;
+    rank_info[4 * r + 3] = 0;
+  }
+}
+
+// The chunk map, after k_stream_tables: workgroup g < n_tensors gives every chunk of g's rank whose first
+// byte lies in tensor g the entry rank << 20 | g (chunk j of a rank starts in the last tensor whose stream
+// offset is <= j * 4 KB: chunks ceil(offset_g / 4 KB) up to ceil(offset_g+1 / 4 KB), or to the rank's
+// chunk count for its last tensor), and workgroup n_tensors fills the map's padding after the last
+// rank's chunks with kNoSeg.
+__global__ __launch_bounds__(256) void k_chunk_map(const uint32_t* __restrict__ rank_first,
+                                                   const uint64_t* __restrict__ rank_bytes, uint32_t nranks,
+                                                   uint32_t n_tensors, const uint64_t* __restrict__ stream_off,
+                                                   const uint64_t* __restrict__ rank_info,
+                                                   uint32_t* __restrict__ map, uint64_t n_map) {
+  constexpr uint64_t C = kTileChunkBytes;
+  const uint32_t g = blockIdx.x;
+  uint64_t first = 0, j0, j1;
+  uint32_t v = kNoSeg;
+  if (g == n_tensors) {
+    j0 = rank_info[4 * (nranks - 1)] + (rank_bytes[nranks - 1] + C - 1) / C;
+    j1 = n_map;
+  } else {
+    uint32_t lo = 0, hi = nranks;  // the rank r with rank_first[r] <= g < rank_first[r + 1]
+    while (hi - lo > 1) {
+      const uint32_t mid = (lo + hi) >> 1;
+      if (rank_first[mid] <= g) lo = mid; else hi = mid;
+    }
+    const uint32_t t1 = rank_first[lo + 1];
+    first = rank_info[4 * lo];
+    j0 = (stream_off[g] + C - 1) / C;
+    j1 = g + 1 < t1 ? (stream_off[g + 1] + C - 1) / C : (rank_bytes[lo] + C - 1) / C;
+    v = (lo << kMapTensorBits) | g;
+  }
+  for (uint64_t j = j0 + threadIdx.x; j < j1; j += blockDim.x) map[first + j] = v;
+}
+
+// ------------------------------------------------------------------------------------------------
 // launch helpers
 // ------------------------------------------------------------------------------------------------
 
@@ -1023,12 +1089,31 @@ int emu_plan_upload(emu_plan_t plan, void* d_workspace, uint64_t workspace_bytes
   if (!plan_live(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
   if (!d_workspace) return fail(EMU_ERR_NULL, "workspace is NULL");
   if (misaligned(d_workspace, kWsAlign)) return fail(EMU_ERR_WORKSPACE, "workspace not %llu-byte aligned", (unsigned long long)kWsAlign);
-  if (workspace_bytes < P->host_ws.size())
+  if (workspace_bytes < P->ws.total)
     return fail(EMU_ERR_WORKSPACE, "workspace of %llu bytes, plan needs %llu", (unsigned long long)workspace_bytes,
-                (unsigned long long)P->host_ws.size());
-  const hipError_t e = hipMemcpyAsync(d_workspace, P->host_ws.data(), P->host_ws.size(), hipMemcpyHostToDevice,
-                                      static_cast<hipStream_t>(hip_stream));
+                (unsigned long long)P->ws.total);
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  ws_register(d_workspace, nullptr);  // until this upload is enqueued whole, the address holds no plan's tables
+  const hipError_t e = hipMemcpyAsync(d_workspace, P->host_ws.data(), P->host_ws.size(), hipMemcpyHostToDevice, st);
   if (e != hipSuccess) return fail(EMU_ERR_HIP, "workspace upload: %s", hipGetErrorString(e));
+  uint8_t* base = static_cast<uint8_t*>(d_workspace);
+  drop_pending_error();
+  for (int sd = 0; sd < 2; ++sd) {
+    const SideInfo& s = P->side[sd];
+    const SideTables& t = P->ws.side[sd];
+    if (s.nranks <= 0) continue;
+    const uint32_t* rf = reinterpret_cast<const uint32_t*>(base + t.off_rank_first);
+    const uint64_t* rb = reinterpret_cast<const uint64_t*>(base + t.off_rank_bytes);
+    uint64_t* so = reinterpret_cast<uint64_t*>(base + t.off_stream);
+    uint64_t* ri = reinterpret_cast<uint64_t*>(base + t.off_rank_info);
+    hipLaunchKernelGGL(k_stream_tables, dim3(uint32_t(s.nranks)), dim3(64), 0, st,
+                       reinterpret_cast<const uint64_t*>(base + t.off_sizes), rf, rb, so, ri);
+    if (t.n_tiles)  // an encodable side: at most 2^20 tensors
+      hipLaunchKernelGGL(k_chunk_map, dim3(uint32_t(s.tensors.size()) + 1), dim3(256), 0, st, rf, rb,
+                         uint32_t(s.nranks), uint32_t(s.tensors.size()), so, ri,
+                         reinterpret_cast<uint32_t*>(base + t.off_tile_map), t.n_tiles);
+  }
+  if (int rc = hip_check("emu_plan_upload tables")) return rc;
   ws_register(d_workspace, P);
   return EMU_OK;
 }

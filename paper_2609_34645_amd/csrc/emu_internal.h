@@ -73,11 +73,15 @@ struct SideTables {
   uint64_t n_tiles;          // map entries including the padding (0 when the map cannot encode the side)
 };
 
+// Workspace order: segments, tile map, each side's host tables (sizes, rank_first, rank_bytes, chunk_first)
+// -- the first host_bytes, copied by emu_plan_upload -- then each side's device-built tables (stream
+// offsets, rank records, chunk map), which the upload's kernels compute from the host tables.
 struct WsLayout {
   uint64_t off_segs;     // DevSeg[n_segments]
   uint64_t off_tilemap;  // uint32[]  segment index of every tile: copy tiles, then zero-fill tiles, each
                          //           section padded with kNoSeg to a multiple of kXcdCount
   SideTables side[2];
+  uint64_t host_bytes;   // the uploaded prefix
   uint64_t total;
 };
 
@@ -109,7 +113,7 @@ struct Plan {
   uint64_t ntiles_zero = 0;
   emu_plan_info_t info{};
   WsLayout ws{};
-  std::vector<uint8_t> host_ws;     // workspace image uploaded by emu_plan_upload
+  std::vector<uint8_t> host_ws;     // the workspace's first ws.host_bytes, uploaded by emu_plan_upload
   uint64_t reshard_ws_bytes = 0;    // prefix of host_ws that emu_reshard reads (segments and tile map)
 };
 

@@ -451,6 +451,39 @@ static int to_buckets(Plan& P, uint64_t B) {
   return EMU_OK;
 }
 
+// The bucket stream tables of both sides as the upload's kernels build them on the device, written into
+// a workspace image of w.total bytes: per tensor its stream offset (exclusive prefix sum of the rank's
+// tensor sizes), per rank {first 4 KB chunk, stream bytes, end of its tensor range, 0}, and per 4 KB
+// chunk the rank and the global index of the tensor holding its first byte (chunk j of a rank starts in
+// the last tensor whose stream offset is <= j * 4 KB), padded with kNoSeg.
+static void device_tables(const Plan& P, uint8_t* h) {
+  const WsLayout& w = P.ws;
+  for (int sd = 0; sd < 2; ++sd) {
+    const SideInfo& s = P.side[sd];
+    uint64_t* so = reinterpret_cast<uint64_t*>(h + w.side[sd].off_stream);
+    for (size_t i = 0; i < s.tensors.size(); ++i) so[i] = s.tensors[i].stream_offset;
+    uint64_t* ri = reinterpret_cast<uint64_t*>(h + w.side[sd].off_rank_info);
+    uint32_t* cm = reinterpret_cast<uint32_t*>(h + w.side[sd].off_tile_map);
+    uint64_t first = 0;
+    for (int r = 0; r < s.nranks; ++r) {
+      const uint32_t t0 = s.rank_first[r], t1 = s.rank_first[r + 1];
+      const uint64_t nch = (s.rank_bytes[r] + kTileChunkBytes - 1) / kTileChunkBytes;
+      ri[4 * r + 0] = first;
+      ri[4 * r + 1] = s.rank_bytes[r];
+      ri[4 * r + 2] = t1;
+      ri[4 * r + 3] = 0;
+      if (w.side[sd].n_tiles)
+        for (uint32_t g = t0; g < t1; ++g) {
+          const uint64_t j0 = (s.tensors[g].stream_offset + kTileChunkBytes - 1) / kTileChunkBytes;
+          const uint64_t j1 = g + 1 < t1 ? (s.tensors[g + 1].stream_offset + kTileChunkBytes - 1) / kTileChunkBytes : nch;
+          if (j1 > j0) std::fill(cm + first + j0, cm + first + j1, (uint32_t(r) << kMapTensorBits) | g);
+        }
+      first += nch;
+    }
+    if (w.side[sd].n_tiles) std::fill(cm + first, cm + w.side[sd].n_tiles, kNoSeg);
+  }
+}
+
 // Device segments, tiles and the workspace image.
 // Whether a 2D vector segment can run as SEG_VEC_FLAT with tiles of TV vectors: the kernel finds the
 // row of vector n (n below rows * rv) as umulhi(n, ceil(2^32 / rv)), exact while n * rv < 2^32, and
@@ -572,7 +605,9 @@ static int finalize(Plan& P) {
     nchunk[sd] = encodable && n <= 0x7fffff00ull ? (n + kXcdCount - 1) / kXcdCount * kXcdCount : 0;
   }
 
-  // workspace image
+  // workspace image: the tables the host computes come first and are uploaded; the bucket stream tables
+  // of each side (stream offsets, rank records, chunk map) follow and are built on the device by the
+  // upload (device_tables below gives the host's copy of them, for checking)
   auto align = [](uint64_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; };
   WsLayout& w = P.ws;
   uint64_t off = 0;
@@ -584,6 +619,10 @@ static int finalize(Plan& P) {
     w.side[sd].off_rank_first = off; off = align(off + (s.nranks + 1) * 4);
     w.side[sd].off_rank_bytes = off; off = align(off + s.nranks * 8);
     w.side[sd].off_chunk_first = off; off = align(off + (s.nranks + 1) * 8);
+  }
+  w.host_bytes = off;
+  for (int sd = 0; sd < 2; ++sd) {
+    const SideInfo& s = P.side[sd];
     w.side[sd].off_stream = off; off = align(off + s.tensors.size() * 8);
     w.side[sd].off_rank_info = off; off = align(off + size_t(s.nranks) * 4 * 8);
     w.side[sd].off_tile_map = off; off = align(off + nchunk[sd] * 4);
@@ -591,7 +630,7 @@ static int finalize(Plan& P) {
   }
   w.total = off;
   P.reshard_ws_bytes = w.side[0].off_sizes;  // segments and tile map come first
-  P.host_ws.assign(w.total, 0);
+  P.host_ws.assign(w.host_bytes, 0);
   uint8_t* h = P.host_ws.data();
   if (!P.dsegs.empty()) std::memcpy(h + w.off_segs, P.dsegs.data(), P.dsegs.size() * sizeof(DevSeg));
   uint32_t* tm = reinterpret_cast<uint32_t*>(h + w.off_tilemap);
@@ -605,28 +644,6 @@ static int finalize(Plan& P) {
     std::memcpy(h + w.side[sd].off_rank_first, s.rank_first.data(), s.rank_first.size() * 4);
     std::memcpy(h + w.side[sd].off_rank_bytes, s.rank_bytes.data(), s.rank_bytes.size() * 8);
     std::memcpy(h + w.side[sd].off_chunk_first, s.chunk_first.data(), s.chunk_first.size() * 8);
-    uint64_t* so = reinterpret_cast<uint64_t*>(h + w.side[sd].off_stream);
-    for (size_t i = 0; i < s.tensors.size(); ++i) so[i] = s.tensors[i].stream_offset;
-    if (nchunk[sd] == 0) continue;
-    uint64_t* ri = reinterpret_cast<uint64_t*>(h + w.side[sd].off_rank_info);
-    uint32_t* cm = reinterpret_cast<uint32_t*>(h + w.side[sd].off_tile_map);
-    uint64_t first = 0;
-    for (int r = 0; r < s.nranks; ++r) {
-      const uint32_t t0 = s.rank_first[r], t1 = s.rank_first[r + 1];
-      const uint64_t nch = (s.rank_bytes[r] + kTileChunkBytes - 1) / kTileChunkBytes;
-      ri[4 * r + 0] = first;
-      ri[4 * r + 1] = s.rank_bytes[r];
-      ri[4 * r + 2] = t1;
-      // chunk j starts in the last tensor g whose stream offset is <= j * kTileChunkBytes: tensor g
-      // takes chunks [ceil(offset_g / C), ceil(offset_{g+1} / C)), the rank's first tensor from chunk 0
-      for (uint32_t g = t0; g < t1; ++g) {
-        const uint64_t j0 = g == t0 ? 0 : (s.tensors[g].stream_offset + kTileChunkBytes - 1) / kTileChunkBytes;
-        const uint64_t j1 = g + 1 < t1 ? (s.tensors[g + 1].stream_offset + kTileChunkBytes - 1) / kTileChunkBytes : nch;
-        if (j1 > j0) std::fill(cm + first + j0, cm + first + j1, (uint32_t(r) << kMapTensorBits) | g);
-      }
-      first += nch;
-    }
-    std::fill(cm + first, cm + nchunk[sd], kNoSeg);
   }
 
   emu_plan_info_t& I = P.info;
@@ -880,6 +897,21 @@ int emu_plan_info(emu_plan_t plan, emu_plan_info_t* out) {
   if (!plan_live(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
   if (!out) return fail(EMU_ERR_NULL, "out is NULL");
   *out = P->info;
+  return EMU_OK;
+}
+
+int emu_plan_workspace_image(emu_plan_t plan, void* out, uint64_t bytes) {
+  clear_error();
+  const Plan* P = reinterpret_cast<const Plan*>(plan);
+  if (!plan_live(P)) return fail(EMU_ERR_HANDLE, "not a live plan");
+  if (!out) return fail(EMU_ERR_NULL, "out is NULL");
+  if (bytes < P->ws.total)
+    return fail(EMU_ERR_WORKSPACE, "%llu bytes given, the image takes %llu", (unsigned long long)bytes,
+                (unsigned long long)P->ws.total);
+  uint8_t* h = static_cast<uint8_t*>(out);
+  std::memcpy(h, P->host_ws.data(), P->host_ws.size());
+  std::memset(h + P->host_ws.size(), 0, P->ws.total - P->host_ws.size());
+  device_tables(*P, h);
   return EMU_OK;
 }
 

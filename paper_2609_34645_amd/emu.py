@@ -154,6 +154,7 @@ def load(path: str = LIB_PATH):
         "emu_tensor_info": ([P, I32, I32, ctypes.POINTER(c_tensor_desc)], ctypes.c_int),
         "emu_plan_segments": ([P, I64, I64, ctypes.POINTER(c_segment)], ctypes.c_int),
         "emu_plan_upload": ([P, V, U64, V], ctypes.c_int),
+        "emu_plan_workspace_image": ([P, V, U64], ctypes.c_int),
         "emu_reshard": ([P, V, V, V, V], ctypes.c_int),
         "emu_reshard_noalloc": ([P, V, V, V], ctypes.c_int),
         "emu_reshard_groups": ([P, V, I32, V, V, V], ctypes.c_int),
@@ -326,6 +327,13 @@ class Plan:
         arr = (c_bucket_desc * max(1, n))()
         check(load().emu_bucket_info(self._h, side, bucket_bytes, 0, n, arr))
         return [dict(rank=b.rank, index=b.index, stream_offset=b.stream_offset, bytes=b.bytes) for b in arr[:n]]
+
+    def workspace_image(self) -> bytes:
+        """The workspace bytes the upload produces, computed on the host (zero between tables)."""
+        n = self.info["workspace_bytes"]
+        buf = ctypes.create_string_buffer(max(n, 1))
+        check(load().emu_plan_workspace_image(self._h, buf, n))
+        return buf.raw[:n]
 
     # -- device helpers (plumbing) -------------------------------------------------------------
     def workspace(self, device=None, stream=None):

@@ -223,3 +223,19 @@ def check_buckets(plan, side, B, tensor_sets_host, bucket_bufs, label=""):
             k += 1
             off += w.size
     assert k == len(bucket_bufs)
+
+
+def check_upload(plan, label=""):
+    """Upload `plan` into a zeroed workspace and compare it byte for byte with the host's image of it
+    (emu_plan_workspace_image): the tables the upload's kernels derive on the device included."""
+    import torch
+
+    n = plan.info["workspace_bytes"]
+    ws = torch.zeros(max(n, 256), dtype=torch.uint8, device="cuda")
+    plan.upload(ws)
+    torch.cuda.synchronize()
+    got = ws[:n].cpu().numpy()
+    want = np.frombuffer(plan.workspace_image(), np.uint8)
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"{label}: uploaded workspace differs from the host image at {bad.size} bytes, first {bad[0]}"
+    return ws

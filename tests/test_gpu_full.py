@@ -35,7 +35,7 @@ import pytest
 
 import oracle
 from paper_2609_34645_amd import emu
-from tests.gpu_util import Guard, check_reshard, fill_device, host_view, o_layout, say
+from tests.gpu_util import Guard, check_reshard, check_upload, fill_device, host_view, o_layout, say
 from tests.shapes import EIGHT_B, HUGE_VOCAB, ONE_B
 
 pytestmark = pytest.mark.gpu
@@ -117,6 +117,21 @@ def test_8b_tp2pp2_to_tp4pp1(gpu_lib):
     for i, (x, y) in enumerate(zip(S.tensors, A2.tensors)):
         assert torch.equal(x, y), f"round trip differs in source tensor {i}"
     del S, D, A2, ws, wb
+    cleanup()
+
+
+def test_8b_uploaded_workspaces_match_host_image(gpu_lib):
+    """The benchmark plans' workspaces, with the stream tables and 4 KB chunk maps (about 4 million
+    entries per side) derived on the device, equal the host's image byte for byte."""
+    m = emu.Model(*EIGHT_B)
+    for src, dst, B in ((emu.Layout(m, 2, 2), emu.Layout(m, 4, 1), 0),
+                        (emu.Layout(m, 2, 2), emu.Layout(m, 4, 1), (1 << 28) - 2),
+                        (emu.Layout(m, 8, 4, 128), emu.Layout(m, 2, 2, 128), 0)):
+        label = f"TP{src.tp}PP{src.pp}->TP{dst.tp}PP{dst.pp} B={B}"
+        say(f"  upload image {label}")
+        p = emu.Plan(src, dst, bucket_bytes=B)
+        ws = check_upload(p, label)
+        del ws, p
     cleanup()
 
 

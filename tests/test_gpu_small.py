@@ -14,9 +14,9 @@ import pytest
 
 import oracle
 from paper_2609_34645_amd import emu
-from tests.gpu_util import (Guard, check_buckets, check_reshard, full_model, host_view, o_layout, say,
-                             upload_shards)
-from tests.shapes import MICRO, MICRO8, TINY
+from tests.gpu_util import (Guard, check_buckets, check_reshard, check_upload, full_model, host_view, o_layout,
+                             say, upload_shards)
+from tests.shapes import MICRO, MICRO8, MICRO_KV, TINY
 
 pytestmark = pytest.mark.gpu
 
@@ -719,3 +719,19 @@ def test_alias_plans_small(gpu_lib):
         if not own:
             assert all(bool((b == 0xA5).all()) for b in D.bufs)
         check_reshard(plan, S, D, label=f"alias {src.tp}x{src.pp} -> {dst.tp}x{dst.pp}")
+
+
+def test_uploaded_workspace_matches_host_image():
+    """emu_plan_upload derives each side's stream offsets, rank records and 4 KB chunk map on the device:
+    the uploaded workspace equals the host's image byte for byte, for sides that differ in rank and tensor
+    counts, uneven PP with KV replication, and fused plans whose bucket sides hold 30-byte buckets (many
+    tensors inside one chunk) or buckets ending off the chunk grid."""
+    m, mk = emu.Model(*TINY), emu.Model(*MICRO_KV)
+    plans = [emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1)),
+             emu.Plan(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate")),
+             emu.Plan(emu.Layout(m, 2, 1), emu.Layout(m, 1, 2), bucket_bytes=(1 << 16) - 2),
+             emu.Plan(emu.Layout(mk, 8, 3, 2), emu.Layout(mk, 2, 1)),
+             emu.Plan(emu.Layout(mk, 1, 1), emu.Layout(mk, 4, 2), bucket_bytes=30)]
+    for i, p in enumerate(plans):
+        say(f"upload image plan {i}")
+        check_upload(p, label=f"plan {i}")

@@ -23,12 +23,11 @@ import oracle
 from oracle import coords
 from paper_2609_34645_amd import emu
 from tests.gpu_util import Guard, o_layout, say, upload_shards
-from tests.shapes import MICRO
+from tests.shapes import MICRO, MICRO_KV
 
 pytestmark = pytest.mark.gpu
 
 GUARD = 48  # bytes of prefilled guard band around every tensor and bucket view
-MICRO_KV = (3, 16, 8, 2, 2, 16, 16)  # KV replication up to TP8 over 2 KV heads, uneven stages at PP2
 FORMATS = [("interleaved", "block"), ("separate", "separate"), ("interleaved", "separate"), ("separate", "block")]
 TAG = {"bf16": (np.uint16, 0x8000, 0xFFFF), "fp32": (np.uint32, 0x8000_0000, 0xFFFF_FFFF)}
 _CACHE = {}

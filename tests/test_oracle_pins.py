@@ -18,7 +18,7 @@ import pytest
 import oracle
 from oracle import coords
 from synthetic import host_tensor
-from tests.shapes import MICRO, MICRO8, TINY
+from tests.shapes import MICRO, MICRO8, MICRO_KV, TINY
 
 FORMATS = [("interleaved", "block"), ("separate", "separate"), ("interleaved", "separate"),
            ("separate", "block")]
@@ -98,7 +98,6 @@ def expected_tags(lay):
 
 MICRO_LAYOUTS = micro_layouts()
 # KV replication (tp up to 4x the KV heads) and uneven pipeline stages (L = 3)
-MICRO_KV = (3, 16, 8, 2, 2, 16, 16)
 KV_LAYOUTS = micro_layouts(MICRO_KV, tps=(1, 2, 4, 8), pps=(1, 2, 3), pads=(0, 2), dtype="fp32")
 
 

@@ -15,7 +15,7 @@ import oracle
 from paper_2609_34645_amd import emu
 from synthetic import host_tensor
 from tests.plan_interp import coverage, run_plan
-from tests.shapes import EIGHT_B, MICRO, MICRO8, ONE_B, TINY
+from tests.shapes import EIGHT_B, MICRO, MICRO8, MICRO_KV, ONE_B, TINY
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 FMT = {("interleaved", "block"), ("separate", "separate"), ("interleaved", "separate"), ("separate", "block")}
@@ -474,7 +474,6 @@ def test_converting_plan_bytes_8b():
 # KV-head replication (tp > KV heads) and uneven pipeline stages
 # ------------------------------------------------------------------------------------------------
 
-MICRO_KV = (3, 16, 8, 2, 2, 16, 16)
 
 
 def test_kv_replication_and_uneven_pp_match_oracle():
@@ -708,3 +707,70 @@ def test_binding_refuses_tables_the_kernels_would_overrun():
         with pytest.raises(ValueError) as e:
             call()
         assert word in str(e.value), (word, str(e.value))
+
+
+def _ws_tail_tables(plan):
+    """Split the tail of plan.workspace_image() into each side's device-built tables (stream offsets,
+    rank records, 4 KB chunk map), which close the workspace in that order, 256-byte aligned each."""
+    img = plan.workspace_image()
+    assert len(img) == plan.info["workspace_bytes"]
+    a = lambda x: (x + 255) // 256 * 256
+    C = 4096
+    shapes = []
+    for side in (0, 1):
+        descs = plan.tensors(side)
+        nranks = plan.info["n_src_ranks" if side == 0 else "n_dst_ranks"]
+        rank_bytes = [0] * nranks
+        for d in descs:
+            rank_bytes[d["rank"]] += d["bytes"]
+        nch = sum(-(-b // C) for b in rank_bytes)
+        nmap = -(-nch // 8) * 8
+        shapes.append((descs, nranks, rank_bytes, nmap))
+    off = len(img) - sum(a(len(d) * 8) + a(n * 32) + a(m * 4) for d, n, _, m in shapes)
+    assert off > 0
+    out = []
+    for descs, nranks, rank_bytes, nmap in shapes:
+        so = np.frombuffer(img, np.uint64, len(descs), off); off += a(len(descs) * 8)
+        ri = np.frombuffer(img, np.uint64, nranks * 4, off).reshape(nranks, 4); off += a(nranks * 32)
+        cm = np.frombuffer(img, np.uint32, nmap, off); off += a(nmap * 4)
+        out.append((descs, rank_bytes, so, ri, cm))
+    assert off == len(img)
+    return out
+
+
+def _check_stream_tables(plan):
+    C = 4096
+    for descs, rank_bytes, so, ri, cm in _ws_tail_tables(plan):
+        ranks = [d["rank"] for d in descs]
+        assert ranks == sorted(ranks)
+        first_chunk, end = 0, 0
+        for r, rb in enumerate(rank_bytes):
+            idx = [i for i, q in enumerate(ranks) if q == r]
+            end += len(idx)
+            pos = 0
+            for i in idx:  # stream offsets: the tensors of a rank back to back, in global order
+                assert so[i] == pos == descs[i]["stream_offset"]
+                pos += descs[i]["bytes"]
+            assert pos == rb
+            nch = -(-rb // C)
+            assert list(ri[r]) == [first_chunk, rb, end, 0]
+            for j in range(nch):  # chunk j starts in the last tensor of the rank whose offset is <= j*C
+                owner = max(i for i in idx if so[i] <= j * C)
+                assert cm[first_chunk + j] == (r << 20) | owner, (r, j)
+                assert so[owner] <= j * C < (so[owner] + descs[owner]["bytes"] if owner != idx[-1] else rb)
+            first_chunk += nch
+        assert (cm[first_chunk:] == 0xFFFFFFFF).all() and len(cm) - first_chunk < 8
+
+
+def test_workspace_image_stream_tables():
+    """The tables the upload derives on the device, as the host computes them (the GPU tests compare the
+    uploaded workspace with this image byte for byte): stream offsets, rank records and the chunk map,
+    against the tensor inventory. Covers several ranks, uneven PP, KV replication and fused plans'
+    bucket sides, including 30-byte buckets (many tensors start inside one 4 KB chunk)."""
+    m = emu.Model(*TINY)
+    _check_stream_tables(emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1)))
+    _check_stream_tables(emu.Plan(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate")))
+    _check_stream_tables(emu.Plan(emu.Layout(m, 2, 1), emu.Layout(m, 1, 2), bucket_bytes=(1 << 16) - 2))
+    mk = emu.Model(*MICRO_KV)
+    _check_stream_tables(emu.Plan(emu.Layout(mk, 8, 3, 2), emu.Layout(mk, 2, 1)))
+    _check_stream_tables(emu.Plan(emu.Layout(mk, 1, 1), emu.Layout(mk, 4, 2), bucket_bytes=30))
