@@ -39,10 +39,10 @@
  *   - The caller allocates and owns every device buffer (tensors, buckets, pointer tables, workspace)
  *     and every stream. The library allocates host memory for plans only: it never calls hipMalloc or
  *     hipFree and never synchronizes a device or stream itself. Its only device memory is one static
- *     32 MiB array per device, part of its code object, that emu_reshard_noalloc uses as workspace. The one host-to-device copy,
- *     emu_plan_upload, reads the plan's pageable host memory, and the HIP runtime may hold the calling
- *     thread until the stream has reached that copy (it does for workspaces of megabytes): upload once
- *     per plan, before the work it should not wait for.
+ *     32 MiB array per device, part of its code object, that emu_reshard_noalloc uses as workspace. The
+ *     host-to-device copies of emu_plan_upload (and of emu_reshard_noalloc's first call with a plan) read
+ *     the plan's pageable host memory, and the HIP runtime may hold the calling thread until the stream
+ *     has reached them: upload once per plan, before the work it should not wait for.
  *   - Pointer tables are DEVICE arrays of 64-bit device addresses. Every tensor and bucket base must be
  *     16-byte aligned. Source and destination buffers must not overlap (undefined behaviour).
  *   - A pointer table holds exactly the entries the plan indexes: n_src_tensors, n_dst_tensors, or the
@@ -257,12 +257,13 @@ int emu_tensor_info(emu_plan_t plan, int32_t side, int32_t index, emu_tensor_des
 int emu_plan_segments(emu_plan_t plan, int64_t first, int64_t count, emu_segment_t* out);
 
 /* Fill the caller's workspace (at least info.workspace_bytes, 256-byte aligned) with the plan's tables:
- * enqueue the host-to-device copy of the tables the host computes (the copy map, tensor sizes, each rank's
- * tensor range and stream length), then two small kernels that derive the bucket kernels' tables from them
- * on the device (each tensor's offset in its rank's stream, per-rank records, and the map from every 4 KB
- * chunk of a stream to its rank and tensor). emu_plan_workspace_image gives the resulting bytes. The plan
- * must outlive the copy. The source is pageable host
- * memory, so the HIP runtime may return only once the stream has reached the copy. The library records that
+ * enqueue the host-to-device copies of what the host computes (the copy map's segments with their tile
+ * counts; per side the tensor sizes, each rank's tensor range and stream length: about 100 KB for the 8B
+ * transitions), then small kernels that derive the rest on the device (the reshard's tile-to-segment map;
+ * per side each tensor's offset in its rank's stream, per-rank records, and the map from every 4 KB chunk
+ * of a stream to its rank and tensor). emu_plan_workspace_image gives the resulting bytes. The plan must
+ * outlive the copies. Their source is pageable host
+ * memory, so the HIP runtime may return only once the stream has reached them. The library records that
  * this address now holds this plan's tables: execute calls of the plan accept only a workspace address so
  * recorded (EMU_ERR_WORKSPACE otherwise, before anything is launched), and an upload of another plan to
  * the same address replaces the record. The record is of the address, not of the allocation: the caller
@@ -295,9 +296,10 @@ int emu_reshard_groups(emu_plan_t plan, const void* d_workspace, int32_t n_group
  * default tile size fits; a larger one returns EMU_ERR_WORKSPACE before anything is enqueued) live in a
  * static device array of the library, of which every device it runs on holds one copy until the
  * process ends. The call allocates nothing and launches the same kernels as emu_reshard: the first call
- * with a plan on a device enqueues the copy of its tables into that device's array on hip_stream (from
- * the plan's pageable host memory, so the plan must outlive it); later calls with the same plan find
- * the tables there and only launch. Under stream capture a call whose tables are not yet resident
+ * with a plan on a device enqueues, on hip_stream, the copy of its segments into that device's array
+ * (from the plan's pageable host memory, so the plan must outlive it) and the kernel that derives the
+ * tile map there, as emu_plan_upload does; later calls with the same plan find the tables there and
+ * only launch. Under stream capture a call whose tables are not yet resident
  * returns EMU_ERR_ARG: make one call outside capture first.
  * All calls on one device share its array, which holds the tables of the last plan copied in: calls
  * that overlap on one device with different plans (on different streams, or from several threads)

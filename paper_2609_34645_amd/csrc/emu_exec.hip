@@ -741,10 +741,32 @@ __global__ __launch_bounds__(kBucketTileThreads, EMU_RESHARD_WAVES_PER_EU) void 
 }
 
 // ------------------------------------------------------------------------------------------------
-// upload-time stream tables
+// upload-time tables
 // ------------------------------------------------------------------------------------------------
-// emu_plan_upload copies the host tables (tensor sizes, each rank's tensor range and stream length) and
-// derives the bucket kernel's tables from them on the device. k_stream_tables, one wave64 per rank: the
+// emu_plan_upload copies the segments with their tile counts and each side's host tables (tensor sizes,
+// each rank's tensor range and stream length), and derives the rest on the device.
+//
+// k_tile_map: workgroup x < n_seg writes segment x's index into its tiles' map entries, from the
+// segment's first map index on (workgroups y = 0, 1, ... stride through a long segment); workgroup n_seg
+// fills the padding after each section (copy tiles, zero-fill tiles) with kNoSeg.
+__global__ __launch_bounds__(256) void k_tile_map(const DevSeg* __restrict__ segs,
+                                                  const uint32_t* __restrict__ seg_tiles, uint32_t n_seg,
+                                                  uint32_t* __restrict__ map, uint64_t copy_end, uint64_t zero0,
+                                                  uint64_t zero_end, uint64_t n_map) {
+  const uint32_t x = blockIdx.x;
+  if (x == n_seg) {
+    if (blockIdx.y != 0) return;
+    for (uint64_t j = copy_end + threadIdx.x; j < zero0; j += blockDim.x) map[j] = kNoSeg;
+    for (uint64_t j = zero_end + threadIdx.x; j < n_map; j += blockDim.x) map[j] = kNoSeg;
+    return;
+  }
+  const uint64_t t0 = segs[x].tile0;
+  const uint32_t n = seg_tiles[x];
+  for (uint64_t j = uint64_t(blockIdx.y) * blockDim.x + threadIdx.x; j < n; j += uint64_t(gridDim.y) * blockDim.x)
+    map[t0 + j] = x;
+}
+
+// k_stream_tables, one wave64 per rank: the
 // exclusive prefix sum of the rank's tensor sizes (each tensor's stream offset), and the rank's record
 // {first 4 KB chunk, stream bytes, end of its tensor range, 0}, whose first chunk is the sum over earlier
 // ranks of ceil(bytes / 4 KB).
@@ -1030,6 +1052,50 @@ static int launch_plan(const Plan* P, const uint8_t* w, const uint64_t* sp, cons
   return hip_check(what);
 }
 
+// Enqueue on st the plan's tables into device memory at `base` laid out as the workspace: the copies of
+// the host-filled parts, then the kernels that derive the tile map and, with `sides`, each side's stream
+// tables. Without `sides` only the workspace's first ws.reshard_bytes (all emu_reshard reads) are written.
+static int enqueue_tables(const Plan* P, uint8_t* base, bool sides, hipStream_t st, const char* what) {
+  const WsLayout& w = P->ws;
+  const uint64_t head = w.off_tilemap;
+  if (head) {
+    const hipError_t e = hipMemcpyAsync(base, P->host_ws.data(), head, hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return fail(EMU_ERR_HIP, "%s: segment upload: %s", what, hipGetErrorString(e));
+  }
+  if (sides && w.host_end > w.reshard_bytes) {
+    const hipError_t e = hipMemcpyAsync(base + w.reshard_bytes, P->host_ws.data() + head, w.host_end - w.reshard_bytes,
+                                        hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return fail(EMU_ERR_HIP, "%s: table upload: %s", what, hipGetErrorString(e));
+  }
+  drop_pending_error();
+  if (w.n_map) {
+    uint32_t longest = 0;
+    for (uint32_t n : P->seg_tiles) longest = n > longest ? n : longest;
+    const uint32_t gy = uint32_t(std::max<uint64_t>(1, std::min<uint64_t>(64, (uint64_t(longest) + 255) / 256)));
+    hipLaunchKernelGGL(k_tile_map, dim3(uint32_t(P->dsegs.size()) + 1, gy), dim3(256), 0, st,
+                       reinterpret_cast<const DevSeg*>(base + w.off_segs),
+                       reinterpret_cast<const uint32_t*>(base + w.off_seg_tiles), uint32_t(P->dsegs.size()),
+                       reinterpret_cast<uint32_t*>(base + w.off_tilemap), P->ntiles_copy, P->zero_tile0,
+                       P->zero_tile0 + P->ntiles_zero, w.n_map);
+  }
+  for (int sd = 0; sides && sd < 2; ++sd) {
+    const SideInfo& s = P->side[sd];
+    const SideTables& t = w.side[sd];
+    if (s.nranks <= 0) continue;
+    const uint32_t* rf = reinterpret_cast<const uint32_t*>(base + t.off_rank_first);
+    const uint64_t* rb = reinterpret_cast<const uint64_t*>(base + t.off_rank_bytes);
+    uint64_t* so = reinterpret_cast<uint64_t*>(base + t.off_stream);
+    uint64_t* ri = reinterpret_cast<uint64_t*>(base + t.off_rank_info);
+    hipLaunchKernelGGL(k_stream_tables, dim3(uint32_t(s.nranks)), dim3(64), 0, st,
+                       reinterpret_cast<const uint64_t*>(base + t.off_sizes), rf, rb, so, ri);
+    if (t.n_tiles)  // an encodable side: at most 2^20 tensors
+      hipLaunchKernelGGL(k_chunk_map, dim3(uint32_t(s.tensors.size()) + 1), dim3(256), 0, st, rf, rb,
+                         uint32_t(s.nranks), uint32_t(s.tensors.size()), so, ri,
+                         reinterpret_cast<uint32_t*>(base + t.off_tile_map), t.n_tiles);
+  }
+  return hip_check(what);
+}
+
 // ------------------------------------------------------------------------------------------------
 // plan tables without a caller workspace (emu_reshard_noalloc)
 // ------------------------------------------------------------------------------------------------
@@ -1069,8 +1135,7 @@ static int scratch_tables(const Plan* P, hipStream_t st, void** out) {
       return fail(EMU_ERR_ARG, "the static scratch does not hold this plan's tables: make one call outside stream "
                   "capture first");
     sl.resident = 0;
-    const hipError_t e = hipMemcpyAsync(sl.ptr, P->host_ws.data(), P->reshard_ws_bytes, hipMemcpyHostToDevice, st);
-    if (e != hipSuccess) return fail(EMU_ERR_HIP, "scratch upload: %s", hipGetErrorString(e));
+    if (int rc = enqueue_tables(P, static_cast<uint8_t*>(sl.ptr), false, st, "emu_reshard_noalloc tables")) return rc;
     sl.resident = P->id;
   }
   *out = sl.ptr;
@@ -1092,28 +1157,10 @@ int emu_plan_upload(emu_plan_t plan, void* d_workspace, uint64_t workspace_bytes
   if (workspace_bytes < P->ws.total)
     return fail(EMU_ERR_WORKSPACE, "workspace of %llu bytes, plan needs %llu", (unsigned long long)workspace_bytes,
                 (unsigned long long)P->ws.total);
-  hipStream_t st = static_cast<hipStream_t>(hip_stream);
   ws_register(d_workspace, nullptr);  // until this upload is enqueued whole, the address holds no plan's tables
-  const hipError_t e = hipMemcpyAsync(d_workspace, P->host_ws.data(), P->host_ws.size(), hipMemcpyHostToDevice, st);
-  if (e != hipSuccess) return fail(EMU_ERR_HIP, "workspace upload: %s", hipGetErrorString(e));
-  uint8_t* base = static_cast<uint8_t*>(d_workspace);
-  drop_pending_error();
-  for (int sd = 0; sd < 2; ++sd) {
-    const SideInfo& s = P->side[sd];
-    const SideTables& t = P->ws.side[sd];
-    if (s.nranks <= 0) continue;
-    const uint32_t* rf = reinterpret_cast<const uint32_t*>(base + t.off_rank_first);
-    const uint64_t* rb = reinterpret_cast<const uint64_t*>(base + t.off_rank_bytes);
-    uint64_t* so = reinterpret_cast<uint64_t*>(base + t.off_stream);
-    uint64_t* ri = reinterpret_cast<uint64_t*>(base + t.off_rank_info);
-    hipLaunchKernelGGL(k_stream_tables, dim3(uint32_t(s.nranks)), dim3(64), 0, st,
-                       reinterpret_cast<const uint64_t*>(base + t.off_sizes), rf, rb, so, ri);
-    if (t.n_tiles)  // an encodable side: at most 2^20 tensors
-      hipLaunchKernelGGL(k_chunk_map, dim3(uint32_t(s.tensors.size()) + 1), dim3(256), 0, st, rf, rb,
-                         uint32_t(s.nranks), uint32_t(s.tensors.size()), so, ri,
-                         reinterpret_cast<uint32_t*>(base + t.off_tile_map), t.n_tiles);
-  }
-  if (int rc = hip_check("emu_plan_upload tables")) return rc;
+  if (int rc = enqueue_tables(P, static_cast<uint8_t*>(d_workspace), true, static_cast<hipStream_t>(hip_stream),
+                              "emu_plan_upload"))
+    return rc;
   ws_register(d_workspace, P);
   return EMU_OK;
 }
@@ -1158,9 +1205,9 @@ int emu_reshard_noalloc(emu_plan_t plan, const uint64_t* d_src_ptrs, const uint6
   if (!d_src_ptrs || !d_dst_ptrs) return fail(EMU_ERR_NULL, "NULL pointer table");
   if (misaligned(d_src_ptrs, 8) || misaligned(d_dst_ptrs, 8)) return fail(EMU_ERR_ALIGN, "pointer tables must be 8-byte aligned");
   if (P->ntiles == 0) return EMU_OK;
-  if (P->reshard_ws_bytes > kScratchBytes)
+  if (P->ws.reshard_bytes > kScratchBytes)
     return fail(EMU_ERR_WORKSPACE, "the plan's tables take %llu bytes, the static scratch holds %llu: use emu_reshard "
-                "with a workspace", (unsigned long long)P->reshard_ws_bytes, (unsigned long long)kScratchBytes);
+                "with a workspace", (unsigned long long)P->ws.reshard_bytes, (unsigned long long)kScratchBytes);
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
   void* w = nullptr;
   const int rc = scratch_tables(P, st, &w);

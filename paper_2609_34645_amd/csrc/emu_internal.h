@@ -73,15 +73,20 @@ struct SideTables {
   uint64_t n_tiles;          // map entries including the padding (0 when the map cannot encode the side)
 };
 
-// Workspace order: segments, tile map, each side's host tables (sizes, rank_first, rank_bytes, chunk_first)
-// -- the first host_bytes, copied by emu_plan_upload -- then each side's device-built tables (stream
-// offsets, rank records, chunk map), which the upload's kernels compute from the host tables.
+// Workspace order: segments, their tile counts, the tile map, each side's host tables (sizes, rank_first,
+// rank_bytes, chunk_first), then each side's device-built tables (stream offsets, rank records, chunk
+// map). emu_plan_upload copies the segments with their tile counts and the host tables; its kernels
+// derive the tile map and the device-built tables from them. Segments, tile counts and tile map -- all
+// emu_reshard reads -- are the workspace's first reshard_bytes.
 struct WsLayout {
-  uint64_t off_segs;     // DevSeg[n_segments]
-  uint64_t off_tilemap;  // uint32[]  segment index of every tile: copy tiles, then zero-fill tiles, each
-                         //           section padded with kNoSeg to a multiple of kXcdCount
+  uint64_t off_segs;       // DevSeg[n_segments]
+  uint64_t off_seg_tiles;  // uint32[n_segments]  tiles of each segment
+  uint64_t off_tilemap;    // uint32[n_map]  segment index of every tile: copy tiles, then zero-fill tiles,
+                           //                each section padded with kNoSeg to a multiple of kXcdCount
+  uint64_t n_map;
+  uint64_t reshard_bytes;  // end of the tile map: start of the sides' host tables
   SideTables side[2];
-  uint64_t host_bytes;   // the uploaded prefix
+  uint64_t host_end;       // end of the sides' host tables: start of the device-built tables
   uint64_t total;
 };
 
@@ -113,8 +118,10 @@ struct Plan {
   uint64_t ntiles_zero = 0;
   emu_plan_info_t info{};
   WsLayout ws{};
-  std::vector<uint8_t> host_ws;     // the workspace's first ws.host_bytes, uploaded by emu_plan_upload
-  uint64_t reshard_ws_bytes = 0;    // prefix of host_ws that emu_reshard reads (segments and tile map)
+  std::vector<uint32_t> seg_tiles;  // tiles of each segment (dsegs order)
+  // The uploaded bytes: workspace [0, ws.off_tilemap) (segments and their tile counts), then workspace
+  // [ws.reshard_bytes, ws.host_end) (the sides' host tables), back to back.
+  std::vector<uint8_t> host_ws;
 };
 
 uint64_t next_plan_id();

@@ -451,13 +451,17 @@ static int to_buckets(Plan& P, uint64_t B) {
   return EMU_OK;
 }
 
-// The bucket stream tables of both sides as the upload's kernels build them on the device, written into
-// a workspace image of w.total bytes: per tensor its stream offset (exclusive prefix sum of the rank's
+// The tables the upload's kernels build on the device, written into a workspace image of w.total bytes:
+// the tile map (each segment's tiles from its first map index; kNoSeg padding), and per side: per tensor its stream offset (exclusive prefix sum of the rank's
 // tensor sizes), per rank {first 4 KB chunk, stream bytes, end of its tensor range, 0}, and per 4 KB
 // chunk the rank and the global index of the tensor holding its first byte (chunk j of a rank starts in
 // the last tensor whose stream offset is <= j * 4 KB), padded with kNoSeg.
 static void device_tables(const Plan& P, uint8_t* h) {
   const WsLayout& w = P.ws;
+  uint32_t* tm = reinterpret_cast<uint32_t*>(h + w.off_tilemap);
+  for (size_t i = 0; i < P.dsegs.size(); ++i) std::fill_n(tm + P.dsegs[i].tile0, P.seg_tiles[i], uint32_t(i));
+  std::fill(tm + P.ntiles_copy, tm + P.zero_tile0, kNoSeg);  // the two sections' padding
+  std::fill(tm + P.zero_tile0 + P.ntiles_zero, tm + w.n_map, kNoSeg);
   for (int sd = 0; sd < 2; ++sd) {
     const SideInfo& s = P.side[sd];
     uint64_t* so = reinterpret_cast<uint64_t*>(h + w.side[sd].off_stream);
@@ -605,14 +609,18 @@ static int finalize(Plan& P) {
     nchunk[sd] = encodable && n <= 0x7fffff00ull ? (n + kXcdCount - 1) / kXcdCount * kXcdCount : 0;
   }
 
-  // workspace image: the tables the host computes come first and are uploaded; the bucket stream tables
-  // of each side (stream offsets, rank records, chunk map) follow and are built on the device by the
-  // upload (device_tables below gives the host's copy of them, for checking)
+  // workspace image (WsLayout): the host fills the segments, their tile counts and the sides' host
+  // tables; the upload's kernels derive the tile map and the sides' stream tables (device_tables below
+  // gives the host's copy of those, for checking)
   auto align = [](uint64_t x) { return (x + kWsAlign - 1) / kWsAlign * kWsAlign; };
+  P.seg_tiles.assign(segtiles.begin(), segtiles.end());  // each below 2^32: the map has fewer tiles
   WsLayout& w = P.ws;
   uint64_t off = 0;
   w.off_segs = off; off = align(off + P.dsegs.size() * sizeof(DevSeg));
+  w.off_seg_tiles = off; off = align(off + P.dsegs.size() * 4);
   w.off_tilemap = off; off = align(off + nmap * 4);
+  w.n_map = nmap;
+  w.reshard_bytes = off;
   for (int sd = 0; sd < 2; ++sd) {
     const SideInfo& s = P.side[sd];
     w.side[sd].off_sizes = off; off = align(off + s.tensors.size() * 8);
@@ -620,7 +628,7 @@ static int finalize(Plan& P) {
     w.side[sd].off_rank_bytes = off; off = align(off + s.nranks * 8);
     w.side[sd].off_chunk_first = off; off = align(off + (s.nranks + 1) * 8);
   }
-  w.host_bytes = off;
+  w.host_end = off;
   for (int sd = 0; sd < 2; ++sd) {
     const SideInfo& s = P.side[sd];
     w.side[sd].off_stream = off; off = align(off + s.tensors.size() * 8);
@@ -629,21 +637,21 @@ static int finalize(Plan& P) {
     w.side[sd].n_tiles = nchunk[sd];
   }
   w.total = off;
-  P.reshard_ws_bytes = w.side[0].off_sizes;  // segments and tile map come first
-  P.host_ws.assign(w.host_bytes, 0);
+  const uint64_t head = w.off_tilemap;  // host_ws: workspace [0, head), then [reshard_bytes, host_end)
+  P.host_ws.assign(head + (w.host_end - w.reshard_bytes), 0);
   uint8_t* h = P.host_ws.data();
-  if (!P.dsegs.empty()) std::memcpy(h + w.off_segs, P.dsegs.data(), P.dsegs.size() * sizeof(DevSeg));
-  uint32_t* tm = reinterpret_cast<uint32_t*>(h + w.off_tilemap);
-  for (size_t i = 0; i < P.dsegs.size(); ++i) std::fill_n(tm + P.dsegs[i].tile0, segtiles[i], uint32_t(i));
-  std::fill(tm + P.ntiles_copy, tm + P.zero_tile0, kNoSeg);  // the two sections' padding
-  std::fill(tm + P.zero_tile0 + P.ntiles_zero, tm + nmap, kNoSeg);
+  if (!P.dsegs.empty()) {
+    std::memcpy(h + w.off_segs, P.dsegs.data(), P.dsegs.size() * sizeof(DevSeg));
+    std::memcpy(h + w.off_seg_tiles, P.seg_tiles.data(), P.seg_tiles.size() * 4);
+  }
+  uint8_t* hb = h + head - w.reshard_bytes;  // hb + (workspace offset of a side host table)
   for (int sd = 0; sd < 2; ++sd) {
     const SideInfo& s = P.side[sd];
-    uint64_t* sz = reinterpret_cast<uint64_t*>(h + w.side[sd].off_sizes);
+    uint64_t* sz = reinterpret_cast<uint64_t*>(hb + w.side[sd].off_sizes);
     for (size_t i = 0; i < s.tensors.size(); ++i) sz[i] = s.tensors[i].bytes;
-    std::memcpy(h + w.side[sd].off_rank_first, s.rank_first.data(), s.rank_first.size() * 4);
-    std::memcpy(h + w.side[sd].off_rank_bytes, s.rank_bytes.data(), s.rank_bytes.size() * 8);
-    std::memcpy(h + w.side[sd].off_chunk_first, s.chunk_first.data(), s.chunk_first.size() * 8);
+    std::memcpy(hb + w.side[sd].off_rank_first, s.rank_first.data(), s.rank_first.size() * 4);
+    std::memcpy(hb + w.side[sd].off_rank_bytes, s.rank_bytes.data(), s.rank_bytes.size() * 8);
+    std::memcpy(hb + w.side[sd].off_chunk_first, s.chunk_first.data(), s.chunk_first.size() * 8);
   }
 
   emu_plan_info_t& I = P.info;
@@ -908,9 +916,11 @@ int emu_plan_workspace_image(emu_plan_t plan, void* out, uint64_t bytes) {
   if (bytes < P->ws.total)
     return fail(EMU_ERR_WORKSPACE, "%llu bytes given, the image takes %llu", (unsigned long long)bytes,
                 (unsigned long long)P->ws.total);
+  const WsLayout& w = P->ws;
   uint8_t* h = static_cast<uint8_t*>(out);
-  std::memcpy(h, P->host_ws.data(), P->host_ws.size());
-  std::memset(h + P->host_ws.size(), 0, P->ws.total - P->host_ws.size());
+  std::memset(h, 0, w.total);
+  std::memcpy(h, P->host_ws.data(), w.off_tilemap);
+  std::memcpy(h + w.reshard_bytes, P->host_ws.data() + w.off_tilemap, w.host_end - w.reshard_bytes);
   device_tables(*P, h);
   return EMU_OK;
 }

@@ -121,12 +121,14 @@ def test_8b_tp2pp2_to_tp4pp1(gpu_lib):
 
 
 def test_8b_uploaded_workspaces_match_host_image(gpu_lib):
-    """The benchmark plans' workspaces, with the stream tables and 4 KB chunk maps (about 4 million
-    entries per side) derived on the device, equal the host's image byte for byte."""
+    """The benchmark plans' workspaces, with the tile map (about 4 million entries), the stream tables
+    and 4 KB chunk maps (about 4 million entries per side) derived on the device, equal the host's image
+    byte for byte; the last plan zero-fills padded vocabulary rows."""
     m = emu.Model(*EIGHT_B)
     for src, dst, B in ((emu.Layout(m, 2, 2), emu.Layout(m, 4, 1), 0),
                         (emu.Layout(m, 2, 2), emu.Layout(m, 4, 1), (1 << 28) - 2),
-                        (emu.Layout(m, 8, 4, 128), emu.Layout(m, 2, 2, 128), 0)):
+                        (emu.Layout(m, 8, 4, 128), emu.Layout(m, 2, 2, 128), 0),
+                        (emu.Layout(m, 4, 1), emu.Layout(m, 8, 4, 128), 0)):
         label = f"TP{src.tp}PP{src.pp}->TP{dst.tp}PP{dst.pp} B={B}"
         say(f"  upload image {label}")
         p = emu.Plan(src, dst, bucket_bytes=B)

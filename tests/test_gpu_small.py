@@ -722,13 +722,15 @@ def test_alias_plans_small(gpu_lib):
 
 
 def test_uploaded_workspace_matches_host_image():
-    """emu_plan_upload derives each side's stream offsets, rank records and 4 KB chunk map on the device:
-    the uploaded workspace equals the host's image byte for byte, for sides that differ in rank and tensor
-    counts, uneven PP with KV replication, and fused plans whose bucket sides hold 30-byte buckets (many
-    tensors inside one chunk) or buckets ending off the chunk grid."""
+    """emu_plan_upload derives the reshard's tile map and each side's stream offsets, rank records and
+    4 KB chunk map on the device: the uploaded workspace equals the host's image byte for byte, for sides
+    that differ in rank and tensor counts, zero-filled pad rows (a second tile-map section), uneven PP with
+    KV replication, and fused plans whose bucket sides hold 30-byte buckets (many tensors inside one chunk)
+    or buckets ending off the chunk grid."""
     m, mk = emu.Model(*TINY), emu.Model(*MICRO_KV)
     plans = [emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1)),
              emu.Plan(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate")),
+             emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 2, 384)),
              emu.Plan(emu.Layout(m, 2, 1), emu.Layout(m, 1, 2), bucket_bytes=(1 << 16) - 2),
              emu.Plan(emu.Layout(mk, 8, 3, 2), emu.Layout(mk, 2, 1)),
              emu.Plan(emu.Layout(mk, 1, 1), emu.Layout(mk, 4, 2), bucket_bytes=30)]

@@ -774,3 +774,37 @@ def test_workspace_image_stream_tables():
     mk = emu.Model(*MICRO_KV)
     _check_stream_tables(emu.Plan(emu.Layout(mk, 8, 3, 2), emu.Layout(mk, 2, 1)))
     _check_stream_tables(emu.Plan(emu.Layout(mk, 1, 1), emu.Layout(mk, 4, 2), bucket_bytes=30))
+
+
+def test_workspace_image_tile_map():
+    """The head of the workspace image: the segment records (80 bytes each, the first map index of the
+    segment's tiles in the last 8), their tile counts, and the tile map the upload derives on the device
+    -- each segment's index on its own tiles, copy segments' tiles first, each section padded with
+    0xFFFFFFFF to a multiple of 8 entries, and every tile of the plan on the map exactly once."""
+    a = lambda x: (x + 255) // 256 * 256
+    m = emu.Model(*TINY)
+    for plan in (emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1)),
+                 emu.Plan(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate")),
+                 emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 2, 384)),  # zero-filled pad rows
+                 emu.Plan(emu.Layout(m, 2, 1), emu.Layout(m, 1, 2), bucket_bytes=(1 << 16) - 2)):
+        img = plan.workspace_image()
+        n = plan.info["n_segments"]
+        segs = plan.segments()
+        tile0 = np.frombuffer(img, np.uint64, n * 10).reshape(n, 10)[:, 9]
+        counts = np.frombuffer(img, np.uint32, n, a(n * 80))
+        assert counts.sum() == plan.info["n_tiles"]
+        zero = np.array([s["src_tensor"] < 0 for s in segs])
+        n_copy, n_zero = int(counts[~zero].sum()), int(counts[zero].sum())
+        z0 = -(-n_copy // 8) * 8
+        n_map = z0 + -(-n_zero // 8) * 8
+        tm = np.frombuffer(img, np.uint32, n_map, a(n * 80) + a(n * 4))
+        want = np.full(n_map, 0xFFFFFFFF, np.uint32)
+        nxt = [0, z0]
+        assert n_zero > 0 or plan.info["zero_fill_bytes"] == 0
+        for i in range(n):  # tiles in segment order within each section
+            sec = int(zero[i])
+            assert tile0[i] == nxt[sec]
+            want[nxt[sec]:nxt[sec] + counts[i]] = i
+            nxt[sec] += int(counts[i])
+        assert nxt == [n_copy, z0 + n_zero]
+        assert np.array_equal(tm, want)
