@@ -169,14 +169,43 @@ def tiny_latency(emu, iters=200):
         return e0.elapsed_time(e1) * 1e3 / iters
 
     eager = timed(step)
+    cap = torch.cuda.Stream()
     graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
+    with torch.cuda.graph(graph, stream=cap):
         step()
     replay = timed(graph.replay)
+    # ten steps in one graph: the graph launch's host cost spread over ten steps, close to the device
+    # time of a step (three dependent kernels and the gaps between them)
+    graph10 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph10, stream=cap):
+        for _ in range(10):
+            step()
+    replay10 = timed(graph10.replay) / 10
     ok = all(torch.equal(x, y) for x, y in zip(D.tensors, R.tensors))
+    # the transport path proper: the sender reshards straight into its buckets (fused plan), the
+    # receiver unpacks them; two kernels instead of three
+    fused = emu.Plan(plan.src, plan.dst, bucket_bytes=B)
+    wf = fused.workspace()
+    fbufs, fbptrs = plan.alloc_buckets(1, B)
+    R2 = plan.alloc(1)
+
+    def fstep():
+        fused.reshard(wf, S.ptrs, fbptrs)
+        plan.unpack(ws, 1, B, fbptrs, R2.ptrs)
+
+    f_eager = timed(fstep)
+    fgraph10 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(fgraph10, stream=cap):
+        for _ in range(10):
+            fstep()
+    f_replay10 = timed(fgraph10.replay) / 10
+    ok = ok and all(torch.equal(x, y) for x, y in zip(D.tensors, R2.tensors))
     return {"workload": "tiny decoder bf16 TP1PP1->TP2PP1 + pack/unpack at 64 KiB buckets",
             "destination_bytes": plan.info["bytes_written"], "eager_us_per_step": round(eager, 2),
-            "graph_us_per_step": round(replay, 2), "outputs_consistent": ok}
+            "graph_us_per_step": round(replay, 2), "graph_of_10_steps_us_per_step": round(replay10, 2),
+            "fused_to_buckets_then_unpack": {"eager_us_per_step": round(f_eager, 2),
+                                             "graph_of_10_steps_us_per_step": round(f_replay10, 2)},
+            "outputs_consistent": ok}
 
 
 def variant_timings(emu, seed, reps=5):

@@ -289,6 +289,8 @@ class Plan:
         check(lib.emu_plan_info(h, ctypes.byref(info)))
         self.info = {f: getattr(info, f) for f, _ in c_plan_info._fields_}
         self._descs = [None, None]
+        self._n = (self.info["n_src_tensors"], self.info["n_dst_tensors"])
+        self._nbuckets = {}  # (side, bucket_bytes) -> bucket count of the side (a plan never changes)
 
     # -- host queries ------------------------------------------------------------------------
     def tensors(self, side: int) -> list:
@@ -444,8 +446,7 @@ class Plan:
 
     # -- execution -----------------------------------------------------------------------------
     def reshard(self, ws, src_ptrs, dst_ptrs, stream=None):
-        self._tables(ws, (src_ptrs, self.info["n_src_tensors"], "src_ptrs"),
-                     (dst_ptrs, self.info["n_dst_tensors"], "dst_ptrs"))
+        self._tables(ws, (src_ptrs, self._n[0], "src_ptrs"), (dst_ptrs, self._n[1], "dst_ptrs"))
         check(load().emu_reshard(self._h, ctypes.c_void_p(ws.data_ptr()), ctypes.c_void_p(src_ptrs.data_ptr()),
                                  ctypes.c_void_p(dst_ptrs.data_ptr()), _stream_handle(stream)))
 
@@ -472,29 +473,31 @@ class Plan:
         """Refuse, before any library call, pointer tables the kernels would read past the end of:
         each must be an int64 device tensor with exactly the entries the plan indexes."""
         for t, n, what in tables:
-            if getattr(t, "dtype", None) is None or str(t.dtype) != "torch.int64":
+            if str(getattr(t, "dtype", None)) != "torch.int64":
                 raise ValueError(f"{what} must be an int64 tensor (emu.ptr_table), not {type(t).__name__}")
             if t.numel() != n or (n and not t.is_contiguous()):
                 raise ValueError(f"{what} has {t.numel()} entries, the plan needs {n} (contiguous)")
         for t, _, what in tables:
             if not t.is_cuda:
                 raise ValueError(f"{what} must be a device tensor")
-        if ws is not None and not getattr(ws, "is_cuda", False):
-            raise ValueError("the workspace must be a device tensor")
-        if ws is not None and self._uploads.get(ws.data_ptr()) is None:
-            raise EmuError(-5, f"workspace at {ws.data_ptr():#x} holds no upload of this plan (Plan.upload)")
+        if ws is not None:
+            if not getattr(ws, "is_cuda", False):
+                raise ValueError("the workspace must be a device tensor")
+            if ws.data_ptr() not in self._uploads:
+                raise EmuError(-5, f"workspace at {ws.data_ptr():#x} holds no upload of this plan (Plan.upload)")
 
     def _bucket_tables(self, ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs):
         if side not in (0, 1):
             raise ValueError("side must be 0 or 1")
         if bucket_bytes < 0:
             raise ValueError("bucket_bytes must be positive")
-        es = ESIZE[DTYPES[(self.src if side == 0 else self.dst).dtype]]
-        if bucket_bytes == 0 or bucket_bytes % es:
-            return  # the library refuses the size (EMU_ERR_BUCKET) before launching anything
-        n_t = self.info["n_src_tensors" if side == 0 else "n_dst_tensors"]
-        self._tables(ws, (tensor_ptrs, n_t, "tensor_ptrs"),
-                     (bucket_ptrs, self.bucket_layout(side, bucket_bytes, -1)[0], "bucket_ptrs"))
+        nb = self._nbuckets.get((side, bucket_bytes))
+        if nb is None:
+            es = ESIZE[DTYPES[(self.src if side == 0 else self.dst).dtype]]
+            if bucket_bytes == 0 or bucket_bytes % es:
+                return  # the library refuses the size (EMU_ERR_BUCKET) before launching anything
+            nb = self._nbuckets[(side, bucket_bytes)] = self.bucket_layout(side, bucket_bytes, -1)[0]
+        self._tables(ws, (tensor_ptrs, self._n[side], "tensor_ptrs"), (bucket_ptrs, nb, "bucket_ptrs"))
 
     def pack(self, ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs, stream=None):
         self._bucket_tables(ws, side, bucket_bytes, tensor_ptrs, bucket_ptrs)
