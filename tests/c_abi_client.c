@@ -76,6 +76,17 @@ int main(void) {
     printf("bucket_range %s\n", emu_status_str(emu_bucket_info(plan, 1, 1ull << 28, nb, 1, bk)));
     free(bk);
   }
+  {
+    /* the workspace image: refused for a buffer one byte short, filled for a whole one */
+    uint8_t* img = (uint8_t*)malloc((size_t)info.workspace_bytes);
+    uint64_t k, nz = 0;
+    if (!img) return 1;
+    printf("image_short %s\n", emu_status_str(emu_plan_workspace_image(plan, img, info.workspace_bytes - 1)));
+    CHECK(emu_plan_workspace_image(plan, img, info.workspace_bytes));
+    for (k = 0; k < info.workspace_bytes; ++k) nz += img[k] != 0;
+    printf("image_nonzero %d\n", nz > 0);
+    free(img);
+  }
   CHECK(emu_plan_free(plan));
   printf("freed_again %s\n", emu_status_str(emu_plan_free(plan)));
 

@@ -113,7 +113,19 @@ int main(int argc, char** argv) {
   HIPCHECK(hipMalloc(&ws, info.workspace_bytes));
   HIPCHECK(hipMalloc(&ws2, info.workspace_bytes));
   printf("not_uploaded %s\n", emu_status_str(emu_reshard(plan, ws2, d_sp, d_dp, NULL)));
+  HIPCHECK(hipMemset(ws, 0, info.workspace_bytes));
   EMUCHECK(emu_plan_upload(plan, ws, info.workspace_bytes, NULL));
+  {
+    /* the uploaded workspace, tables built on the device included, against the host's image of it */
+    uint8_t* want = malloc((size_t)info.workspace_bytes);
+    uint8_t* got = malloc((size_t)info.workspace_bytes);
+    if (!want || !got) return 1;
+    EMUCHECK(emu_plan_workspace_image(plan, want, info.workspace_bytes));
+    HIPCHECK(hipMemcpy(got, ws, info.workspace_bytes, hipMemcpyDeviceToHost));
+    printf("upload_image_equal %d\n", memcmp(want, got, (size_t)info.workspace_bytes) == 0);
+    free(want);
+    free(got);
+  }
   EMUCHECK(emu_reshard(plan, ws, d_sp, d_dp, NULL));
 
   /* buckets of every destination rank, rank 0 first, sized as the library reports them */

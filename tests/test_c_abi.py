@@ -50,6 +50,7 @@ def test_header_compiles_as_c99_and_host_calls_work(client):
     # TP4 PP2 -> TP4 PP1 aliased: every destination tensor is a whole source tensor, nothing is read
     n_dst41 = sum(len(r) for r in oracle.rank_inventory(oracle.Layout(om, 4, 1)))
     assert client["alias"] == f"{n_dst41} 1 {dst_bytes} 0 0"
+    assert client["image_short"] == "EMU_ERR_WORKSPACE" and client["image_nonzero"] == "1"
     assert client["freed_again"] == "EMU_ERR_HANDLE"
     n_nodes, n_edges, l_tran = client["dag"].split()
     py = emu.dag_plan([dict(kind=2, tp=4, pp=8, dp=1, gpus=list(range(32)), tgt_tp=8, tgt_pp=2, tgt_dp=1,

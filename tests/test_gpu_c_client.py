@@ -53,6 +53,7 @@ def test_c_client_reshard_and_buckets(gpu_lib, tmp_path):
     assert res.returncode == 0, res.stderr
     facts = dict(line.split(" ", 1) for line in res.stdout.strip().splitlines())
     assert facts["not_uploaded"] == "EMU_ERR_WORKSPACE"
+    assert facts["upload_image_equal"] == "1"
     assert facts["unpack_equal"] == "1" and facts["done"] == "1"
     om = oracle.Model(*TINY)
     src, dst = oracle.Layout(om, 1, 1), oracle.Layout(om, 2, 1)
