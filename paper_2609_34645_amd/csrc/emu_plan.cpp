@@ -488,7 +488,7 @@ static void device_tables(const Plan& P, uint8_t* h) {
   }
 }
 
-// Device segments, tiles and the workspace image.
+// Device segments, tiles and the workspace layout.
 // Whether a 2D vector segment can run as SEG_VEC_FLAT with tiles of TV vectors: the kernel finds the
 // row of vector n (n below rows * rv) as umulhi(n, ceil(2^32 / rv)), exact while n * rv < 2^32, and
 // keeps in-tile byte offsets in 31 bits: a tile spans at most 2 + TV / rv rows.
@@ -572,8 +572,8 @@ static int finalize(Plan& P) {
   // Tile map: the copy segments' tiles, then the zero-fill segments' tiles, which run on their own
   // kernel instance. Each section is padded with kNoSeg to a whole number of XCD groups, so that every
   // workgroup of a grid (a multiple of kXcdCount) reads an entry of its own section and the kernel
-  // needs no bounds check before its first load. Here each segment gets its first map index; the map
-  // is written straight into the workspace image below.
+  // needs no bounds check before its first load. Here each segment gets its first map index; the
+  // upload's k_tile_map writes the map on the device from those indices and the tile counts.
   uint64_t nmap = 0;
   for (int pass = 0; pass < 2; ++pass) {
     if (pass == 1) P.zero_tile0 = nmap;
