@@ -47,6 +47,7 @@ bool walk(emu_plan_t p) {
   if (!expect(emu_plan_info(p, &info), EMU_OK, "info")) return false;
   emu_tensor_desc_t d;
   std::vector<uint64_t> ptrs[2];
+  std::vector<int> written;  // destination tensors the map writes (all but an alias plan's aliases)
   for (int side = 0; side < 2; ++side) {
     const int n = side ? info.n_dst_tensors : info.n_src_tensors;
     uint64_t a = (1ull << 36) * uint64_t(side + 1);
@@ -54,20 +55,32 @@ bool walk(emu_plan_t p) {
       if (!expect(emu_tensor_info(p, side, i, &d), EMU_OK, "tensor_info")) return false;
       ptrs[side].push_back(a);
       a = (a + d.bytes + 255) / 256 * 256;
+      if (side == 1 && !(info.aliased && d.alias >= 0)) written.push_back(i);
     }
     if (!expect(emu_tensor_info(p, side, n, &d), EMU_ERR_RANGE, "tensor_info past the end")) return false;
     uint64_t nb = 0, sb = 0;
-    for (uint64_t B : {4ull, 28ull, 4096ull, 1ull << 28})  // multiples of either element size
+    for (uint64_t B : {4ull, 28ull, 4096ull, 1ull << 28}) {  // multiples of either element size
       if (!expect(emu_bucket_layout(p, side, B, -1, &nb, &sb), EMU_OK, "bucket_layout")) return false;
+      if (nb > (1u << 16)) continue;  // small buckets of the 8B plans: billions of them
+      std::vector<emu_bucket_desc_t> bk(size_t(nb) + 1);
+      if (!expect(emu_bucket_info(p, side, B, 0, nb, bk.data()), EMU_OK, "bucket_info") ||
+          !expect(emu_bucket_info(p, side, B, nb, 1, bk.data()), EMU_ERR_RANGE, "bucket_info past the end"))
+        return false;
+    }
   }
+  // the workspace image: the host's copy of the tables the upload builds on the device
+  std::vector<uint8_t> img(size_t(info.workspace_bytes) + 1);
+  if (!expect(emu_plan_workspace_image(p, img.data(), info.workspace_bytes), EMU_OK, "workspace_image") ||
+      !expect(emu_plan_workspace_image(p, img.data(), info.workspace_bytes - 1), EMU_ERR_WORKSPACE, "short image"))
+    return false;
   std::vector<emu_segment_t> segs(size_t(info.n_segments) + 1);
   if (!expect(emu_plan_segments(p, 0, info.n_segments, segs.data()), EMU_OK, "segments")) return false;
   if (!expect(emu_plan_segments(p, 0, info.n_segments + 1, segs.data()), EMU_ERR_RANGE, "segments past the end"))
     return false;
   if (!expect(emu_check_tables(p, ptrs[0].data(), ptrs[1].data()), EMU_OK, "check_tables")) return false;
-  if (info.n_dst_tensors > 1) {
+  if (written.size() > 1) {
     std::vector<uint64_t> bad = ptrs[1];
-    bad[1] = bad[0];
+    bad[size_t(written[1])] = bad[size_t(written[0])];
     if (!expect(emu_check_tables(p, ptrs[0].data(), bad.data()), EMU_ERR_OVERLAP, "overlap")) return false;
   }
   return expect(emu_plan_free(p), EMU_OK, "free") && expect(emu_plan_free(p), EMU_ERR_HANDLE, "double free");
@@ -89,6 +102,7 @@ bool plans() {
       const emu_layout_t& b = lays[rnd(uint32_t(lays.size()))];
       emu_plan_t p = nullptr;
       if (!expect(emu_plan(&a, &b, &p), EMU_OK, "micro plan") || !walk(p)) return false;
+      if (!expect(emu_plan_ex(&a, &b, EMU_PLAN_ALIAS_RESIDENT, &p), EMU_OK, "micro alias plan") || !walk(p)) return false;
       if (a.dtype == b.dtype) {
         const uint64_t B = (a.dtype == EMU_FP32 ? 4u : 2u) * (1 + rnd(40));
         if (!expect(emu_plan_to_buckets(&a, &b, B, &p), EMU_OK, "micro fused plan") || !walk(p)) return false;
