@@ -1,5 +1,6 @@
 // Device side of the EMU reshard library for CDNA4 (gfx950): the reshard kernel that executes a
-// compiled copy map, the bucket pack/unpack kernel, and the C ABI entry points that launch them.
+// compiled copy map, the bucket pack/unpack kernel, the small kernels that build a plan's tile map and
+// bucket stream tables in its workspace at upload, and the C ABI entry points that launch them.
 //
 // Both kernels are pure HBM streams: no arithmetic on the data (fp32 <-> bf16 conversion aside),
 // integer address math only. Every thread moves 16-byte vectors (global_load/store_dwordx4), a tile is
