@@ -737,3 +737,11 @@ def test_uploaded_workspace_matches_host_image():
     for i, p in enumerate(plans):
         say(f"upload image plan {i}")
         check_upload(p, label=f"plan {i}")
+
+
+def test_graft_entry_smoke(capsys):
+    """The repository's smoke entry point (tiny decoder: reshard, pack and unpack against the oracle)."""
+    import __graft_entry__
+
+    __graft_entry__.smoke()
+    assert "smoke ok" in capsys.readouterr().out
