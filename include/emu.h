@@ -262,8 +262,8 @@ int emu_plan_segments(emu_plan_t plan, int64_t first, int64_t count, emu_segment
  * transitions), then small kernels that derive the rest on the device (the reshard's tile-to-segment map;
  * per side each tensor's offset in its rank's stream, per-rank records, and the map from every 4 KB chunk
  * of a stream to its rank and tensor). emu_plan_workspace_image gives the resulting bytes. The plan must
- * outlive the copies. Their source is pageable host
- * memory, so the HIP runtime may return only once the stream has reached them. The library records that
+ * outlive the copies. Their source is pageable host memory, so the HIP runtime may return only once the
+ * stream has reached them. The library records that
  * this address now holds this plan's tables: execute calls of the plan accept only a workspace address so
  * recorded (EMU_ERR_WORKSPACE otherwise, before anything is launched), and an upload of another plan to
  * the same address replaces the record. The record is of the address, not of the allocation: the caller
@@ -322,10 +322,10 @@ int emu_bucket_info(emu_plan_t plan, int32_t side, uint64_t bucket_bytes, uint64
  * buffer, after the local layout change): bucket k of rank r receives bytes [k*B, (k+1)*B) of r's
  * stream. d_tensor_ptrs lists that side's tensors (as for emu_reshard); d_bucket_ptrs lists all
  * buckets, rank 0 first (emu_bucket_layout(..., -1, ...) of them). Tensor stream offsets (exclusive
- * prefix sums of the ragged tensor sizes) come from the uploaded workspace; each rank's first bucket
- * index depends on bucket_bytes and is formed per call (on the host for the first 128 ranks, by a
- * wave64 reduction on the device beyond; the persistent fallback kernel scans the tensor sizes on the
- * device). bucket_bytes must be a positive multiple of the element size. */
+ * prefix sums of the ragged tensor sizes, a wave64 scan per rank at upload) come from the workspace;
+ * each rank's first bucket index depends on bucket_bytes and is formed per call (on the host for the
+ * first 128 ranks, by a wave64 reduction on the device beyond; the persistent fallback kernel scans the
+ * tensor sizes on the device). bucket_bytes must be a positive multiple of the element size. */
 int emu_pack_buckets(emu_plan_t plan, const void* d_workspace, int32_t side, uint64_t bucket_bytes,
                      const uint64_t* d_tensor_ptrs, const uint64_t* d_bucket_ptrs, void* hip_stream);
 /* The inverse of emu_pack_buckets on the receiver side (section 6.2: the receiver restores its shards
