@@ -96,6 +96,46 @@ def test_1b_tp4_to_tp2(gpu_lib):
     cleanup()
 
 
+def _l1b(tp, pp, pad=0, dtype="bf16", qkv="interleaved", mlp="block"):
+    return emu.Layout(emu.Model(*ONE_B), tp, pp, pad, dtype, qkv, mlp)
+
+
+# 1B layout pairs beyond the benchmark's: TP16 replicates each of the 8 KV heads on two ranks, PP3 splits
+# the 16 layers 6/5/5, pad 128 pads the vocabulary (zero-filled destination rows, unread source rows),
+# every format combination, and both element conversions.
+LAYOUTS_1B = [
+    (_l1b(8, 4, 128, qkv="separate", mlp="separate"), _l1b(1, 1, mlp="separate")),
+    (_l1b(2, 2, dtype="fp32"), _l1b(4, 4, mlp="separate")),
+    (_l1b(16, 3), _l1b(8, 2, 128, qkv="separate")),
+    (_l1b(1, 4, qkv="separate"), _l1b(16, 1)),
+    (_l1b(8, 3, mlp="separate"), _l1b(2, 1, 128, dtype="fp32", mlp="separate")),
+    (_l1b(4, 1, 128, dtype="fp32"), _l1b(16, 3, 128, dtype="fp32", qkv="separate", mlp="separate")),
+]
+
+
+@pytest.mark.parametrize("k", range(len(LAYOUTS_1B)))
+def test_1b_layout_pairs(gpu_lib, k):
+    """Full-size reshards of the 1B decoder between the layouts above, every byte against the oracle with
+    the write footprint checked; the even cases also pack and unpack the destination at a bucket size
+    that is not a multiple of 16 bytes."""
+    src, dst = LAYOUTS_1B[k]
+    label = (f"1B {src.dtype} TP{src.tp}PP{src.pp} pad{src.pad} {src.qkv}/{src.mlp} -> "
+             f"{dst.dtype} TP{dst.tp}PP{dst.pp} pad{dst.pad} {dst.qkv}/{dst.mlp}")
+    say(f"  {label}")
+    p = emu.Plan(src, dst)
+    ws = p.workspace()
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
+    fill_device(p, 0, S, seed=300 + k, dtype=src.dtype)  # source pad rows hold random values too
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], label)
+    check_reshard(p, S, D, label=label)
+    if k % 2 == 0:
+        es = 4 if dst.dtype == "fp32" else 2
+        _pack_check(p, ws, D, (1 << 26) - es, f"{label}: buckets 2^26 - {es}")
+    del S, D, ws
+    cleanup()
+
+
 def test_8b_tp2pp2_to_tp4pp1(gpu_lib):
     import torch
 
