@@ -14,8 +14,8 @@ import pytest
 
 import oracle
 from paper_2609_34645_amd import emu
-from tests.gpu_util import (Guard, check_buckets, check_reshard, check_upload, full_model, host_view, o_layout,
-                             say, upload_shards)
+from tests.gpu_util import (Guard, check_buckets, check_reshard, check_upload, fill_device, full_model, host_view,
+                             o_layout, say, upload_shards)
 from tests.shapes import MICRO, MICRO8, MICRO_KV, TINY
 
 pytestmark = pytest.mark.gpu
@@ -745,3 +745,40 @@ def test_graft_entry_smoke(capsys):
 
     __graft_entry__.smoke()
     assert "smoke ok" in capsys.readouterr().out
+
+
+@pytest.mark.parametrize("dtype,fmt", [("bf16", ("interleaved", "block")), ("fp32", ("separate", "separate"))])
+def test_same_layout_is_a_copy(dtype, fmt):
+    """The identity plan (source layout == destination layout) is a plain copy. Shards of one full model
+    hold equal replicas (norms on every TP rank, KV heads at TP4 over 2 KV heads), as real state does:
+    every destination tensor then equals its source tensor byte for byte, except that with vocabulary
+    padding the pad rows come out zero while the source's hold garbage that must never be read."""
+    import torch
+
+    m = emu.Model(*TINY)
+    for tp, pp, pad in ((2, 2, 0), (4, 1, 0), (2, 2, 384)):
+        lay = emu.Layout(m, tp, pp, pad, dtype, *fmt)
+        plan = emu.Plan(lay, lay)
+        assert plan.info["bytes_written"] == plan.info["dst_bytes"] == plan.info["src_bytes"]
+        ol = o_layout(lay)
+        ws = plan.workspace()
+        S = plan.alloc(0, fill=0x5A, guard=GUARD)
+        upload_shards(oracle.shard(full_model(ol.model, 29, dtype), ol), S, tweak_replicas=False)
+        descs = plan.tensors(1)
+        real = {}
+        for i, d in enumerate(descs):  # garbage in the source pad rows
+            if d["kind"] in ("embed", "lm_head"):
+                rows, cols = d["shape"]
+                n = max(0, min(rows, m.vocab - d["rank"] % tp * rows)) * (d["bytes"] // rows)
+                real[i] = n
+                S.tensors[i][n:] = 0x77
+        D = plan.alloc(1, fill=0xA5, guard=GUARD)
+        g = Guard(keep=S.tensors, fills=[(D.tensors, 0xA5)], label=f"identity TP{tp}PP{pp} pad {pad}")
+        plan.reshard(ws, S.ptrs, D.ptrs)
+        torch.cuda.synchronize()
+        g.check()
+        for i, (d, s_, t) in enumerate(zip(descs, S.tensors, D.tensors)):
+            n = real.get(i, d["bytes"])
+            assert torch.equal(t[:n], s_[:n]), (tp, pp, pad, d)
+            assert int(t[n:].count_nonzero()) == 0, (tp, pp, pad, d)
+        assert (pad == 0) == all(n == descs[i]["bytes"] for i, n in real.items())
