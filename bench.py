@@ -495,7 +495,7 @@ def main():
 
     src_region = region(max(p.region_bytes(0) for p in (plan, ident, pp_copy)))
     dst_region = region(max(p.region_bytes(1) for p in (plan, fmt)))
-    bucket_region = region(max(plan.bucket_region_bytes(1, b) for b in (B, Bs)))
+    bucket_region = region(max([plan.bucket_region_bytes(1, b) for b in (B, Bs)] + [plan.bucket_region_bytes(0, B)]))
     S, SI, SP = plan.views(0, src_region), ident.views(0, src_region), pp_copy.views(0, src_region)
     D, DF = plan.views(1, dst_region), fmt.views(1, dst_region)
     DA = pp_alias.views(1, dst_region, alias=SP)
@@ -606,6 +606,17 @@ def main():
     fused_ok = all(torch.equal(a, b) for a, b in zip(D.tensors, R.tensors))
     fused_bytes = fused.info["bytes_read"] + fused.info["bytes_written"]
 
+    # receiver path: the source ranks' TP2 PP2 streams, packed into 2^28-byte buckets (on the bucket
+    # region's pages), resharded straight into TP4 PP1 tensors in one pass
+    recv = emu.Plan(src, dst, src_bucket_bytes=B)
+    wr = recv.workspace(dev)
+    s0bufs, s0ptrs = plan.bucket_views(0, B, bucket_region)
+    plan.pack(ws, 0, B, S.ptrs, s0ptrs)
+    (rv_ms,) = interleaved([lambda: recv.reshard(wr, s0ptrs, R.ptrs)])
+    recv_ok = all(torch.equal(a, b) for a, b in zip(D.tensors, R.tensors))
+    recv_bytes = recv.info["bytes_read"] + recv.info["bytes_written"]
+    del s0bufs, s0ptrs, wr
+
     # format change (training -> generation layout of q/k/v and gate/up) against the same transition
     # without it, on the same source and destination pages
     fm_ms, base_ms = interleaved([lambda: fmt.reshard(wsf, S.ptrs, DF.ptrs), lambda: plan.reshard(ws, S.ptrs, D.ptrs)])
@@ -696,6 +707,9 @@ def main():
         "fused_reshard_to_buckets_GBps": gbps(fused_bytes, f_ms),
         "fused_vs_reshard_plus_pack": round((reshard_avg + mean(p_ms)) / f_ms, 3),
         "fused_outputs_consistent": fused_ok,
+        "receiver_reshard_from_buckets_ms": round(rv_ms, 4),
+        "receiver_reshard_from_buckets_GBps": gbps(recv_bytes, rv_ms),
+        "receiver_outputs_consistent": recv_ok,
         "formats_fused_to_separate_tp2pp2_to_tp4pp1": {
             "ms": round(fm_ms, 4), "GBps": gbps(fmt_bytes, fm_ms), "same_pages_fused_to_fused_ms": round(base_ms, 4),
             "ratio": round(fm_ms / base_ms, 4)},

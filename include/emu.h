@@ -248,6 +248,16 @@ int emu_plan_ex(const emu_layout_t* src, const emu_layout_t* dst, uint32_t flags
  * emu_pack_buckets applied to the emu_reshard result. bucket_bytes must be a positive multiple of the
  * element size (EMU_ERR_BUCKET). Host only. */
 int emu_plan_to_buckets(const emu_layout_t* src, const emu_layout_t* dst, uint64_t bucket_bytes, emu_plan_t* out);
+/* The receiver's side of the same transport: a plan that reads the transfer buckets of layout *src's
+ * ranks (bucket k of rank r = bytes [k*B, (k+1)*B) of r's stream) and writes layout *dst's tensors,
+ * restoring the shards from the contiguous buffers (section 6.2, transport and resharding-transport
+ * interplay) and, when dst differs from src, resharding them in the same pass. The plan's source side
+ * (side 0) is the bucket list, rank 0's first, so it is executed with emu_reshard(plan, ws,
+ * d_bucket_ptrs, d_dst_ptrs, stream). With dst == src it is emu_unpack_buckets for a bucket size fixed
+ * at plan time, run by the reshard kernel; the tensors equal emu_unpack_buckets's (and, for dst != src,
+ * emu_reshard's of the unpacked tensors). bucket_bytes must be a positive multiple of the source
+ * element size (EMU_ERR_BUCKET). Host only. */
+int emu_plan_from_buckets(const emu_layout_t* src, const emu_layout_t* dst, uint64_t bucket_bytes, emu_plan_t* out);
 /* Free a plan. Work enqueued with it must have completed. */
 int emu_plan_free(emu_plan_t plan);
 int emu_plan_info(emu_plan_t plan, emu_plan_info_t* out);

@@ -358,6 +358,40 @@ static void find_aliases(Plan& P, bool drop) {
                  P.segs.end());
 }
 
+// The bucket list of one side for bucket size B: per rank its stream cut every B bytes, each bucket a
+// 1D tensor whose stream offset is k * B.
+static SideInfo bucket_side(const SideInfo& X, uint64_t B) {
+  const uint64_t es = uint64_t(elem_size(X.lay.dtype));
+  SideInfo bk;
+  bk.lay = X.lay;
+  bk.vp = X.vp;
+  bk.nranks = X.nranks;
+  bk.total_bytes = X.total_bytes;
+  bk.offsets_grid = B % kTileChunkBytes == 0 || X.nranks == 0;
+  bk.rank_first.assign(X.nranks + 1, 0);
+  bk.rank_bytes = X.rank_bytes;
+  bk.chunk_first.assign(X.nranks + 1, 0);
+  for (int r = 0; r < X.nranks; ++r) {
+    bk.rank_first[r] = uint32_t(bk.tensors.size());
+    for (uint64_t k = 0; k * B < X.rank_bytes[r]; ++k) {
+      emu_tensor_desc_t d{};
+      d.rank = r;
+      d.kind = EMU_T_BUCKET;
+      d.layer = -1;
+      d.ndim = 1;
+      d.bytes = std::min<uint64_t>(B, X.rank_bytes[r] - k * B);
+      d.alias = -1;
+      d.rows = 1;
+      d.cols = int64_t(d.bytes / es);
+      d.stream_offset = k * B;
+      bk.tensors.push_back(d);
+    }
+    bk.chunk_first[r + 1] = bk.chunk_first[r] + (X.rank_bytes[r] + kChunkBytes - 1) / kChunkBytes;
+  }
+  bk.rank_first[X.nranks] = uint32_t(bk.tensors.size());
+  return bk;
+}
+
 // Rewrite a destination-driven copy map so that it writes the destination ranks' bucket streams
 // instead of the destination tensors: tensor j's byte o lands at stream position
 // stream_offset(j) + o of its rank, i.e. in bucket (pos / B) at offset (pos % B). Rows that stay inside
@@ -419,35 +453,78 @@ static int to_buckets(Plan& P, uint64_t B) {
     }
   }
   P.segs.swap(out);
-  // the destination side is now the bucket list
-  SideInfo bk;
-  bk.lay = D.lay;
-  bk.vp = D.vp;
-  bk.nranks = D.nranks;
-  bk.total_bytes = D.total_bytes;
-  bk.offsets_grid = B % kTileChunkBytes == 0 || D.nranks == 0;
-  bk.rank_first.assign(D.nranks + 1, 0);
-  bk.rank_bytes = D.rank_bytes;
-  bk.chunk_first.assign(D.nranks + 1, 0);
-  for (int r = 0; r < D.nranks; ++r) {
-    bk.rank_first[r] = uint32_t(bk.tensors.size());
-    for (uint64_t k = 0; k * B < D.rank_bytes[r]; ++k) {
-      emu_tensor_desc_t d{};
-      d.rank = r;
-      d.kind = EMU_T_BUCKET;
-      d.layer = -1;
-      d.ndim = 1;
-      d.bytes = std::min<uint64_t>(B, D.rank_bytes[r] - k * B);
-      d.alias = -1;
-      d.rows = 1;
-      d.cols = int64_t(d.bytes / es);
-      d.stream_offset = k * B;
-      bk.tensors.push_back(d);
+  P.side[1] = bucket_side(D, B);  // the destination side is now the bucket list
+  return EMU_OK;
+}
+
+// Rewrite a copy map so that it reads the source ranks' bucket streams instead of the source tensors:
+// source tensor i's byte o sits at stream position stream_offset(i) + o of its rank, in bucket (pos / B)
+// at offset (pos % B). Rows whose source bytes stay inside one bucket keep their 2D shape; a row whose
+// source bytes cross a bucket boundary is cut there, on an element boundary (B and every stream offset
+// are multiples of the source element size), and its destination bytes with it. The source side
+// becomes the list of buckets (rank 0's first), so that the receiver of a transfer restores -- or
+// reshards -- its tensors straight from the contiguous buffers on the ordinary reshard kernel.
+static int from_buckets(Plan& P, uint64_t B) {
+  SideInfo& S = P.side[0];
+  const uint64_t ess = uint64_t(elem_size(S.lay.dtype));          // source bytes per element
+  const uint64_t esd = uint64_t(elem_size(P.side[1].lay.dtype));  // destination bytes per element
+  if (B == 0 || B % ess)
+    return fail(EMU_ERR_BUCKET, "bucket size %llu is not a positive multiple of %llu", (unsigned long long)B,
+                (unsigned long long)ess);
+  std::vector<uint64_t> base(S.nranks + 1, 0);
+  for (int r = 0; r < S.nranks; ++r) base[r + 1] = base[r] + (S.rank_bytes[r] + B - 1) / B;
+  if (base[S.nranks] > 0x7fffffffull) return fail(EMU_ERR_UNSUPPORTED, "too many buckets");
+  std::vector<emu_segment_t> out;
+  out.reserve(P.segs.size() + 64);
+  auto emit = [&](const emu_segment_t& g, int64_t bucket, uint64_t src_off, uint64_t dst_off, uint64_t rows,
+                  uint64_t run, uint64_t src_run, bool one_d) {
+    emu_segment_t s = g;
+    s.src_tensor = int32_t(bucket);
+    s.src_offset = src_off;
+    s.dst_offset = dst_off;
+    s.rows = rows;
+    s.run = run;
+    s.src_run = src_run;
+    if (one_d) {
+      s.src_stride = src_run;
+      s.dst_stride = run;
     }
-    bk.chunk_first[r + 1] = bk.chunk_first[r] + (D.rank_bytes[r] + kChunkBytes - 1) / kChunkBytes;
+    push_segment(out, s);
+  };
+  for (const emu_segment_t& g : P.segs) {
+    if (g.src_tensor < 0) {  // zero fill: no source bytes
+      push_segment(out, g);
+      continue;
+    }
+    const emu_tensor_desc_t& t = S.tensors[g.src_tensor];
+    const uint64_t s0 = t.stream_offset + g.src_offset;
+    uint64_t i = 0;
+    while (i < g.rows) {
+      const uint64_t si = s0 + i * g.src_stride;
+      const uint64_t k = si / B, bend = (k + 1) * B;
+      const uint64_t di = g.dst_offset + i * g.dst_stride;
+      if (si + g.src_run <= bend) {
+        // rows i .. i+n-1 read inside bucket k
+        uint64_t n = 1;
+        if (g.rows > 1)
+          n = g.src_stride ? std::min<uint64_t>(g.rows - i, (bend - si - g.src_run) / g.src_stride + 1) : g.rows - i;
+        emit(g, int64_t(base[t.rank] + k), si - k * B, di, n, g.run, g.src_run, g.rows == 1);
+        i += n;
+      } else {
+        // row i's source bytes cross at least one bucket boundary: cut them there
+        for (uint64_t pos = 0; pos < g.src_run;) {
+          const uint64_t sp = si + pos, kk = sp / B;
+          const uint64_t e = std::min<uint64_t>(g.src_run, (kk + 1) * B - si);
+          emit(g, int64_t(base[t.rank] + kk), sp - kk * B, di + pos / ess * esd, 1, (e - pos) / ess * esd, e - pos,
+               true);
+          pos = e;
+        }
+        i += 1;
+      }
+    }
   }
-  bk.rank_first[D.nranks] = uint32_t(bk.tensors.size());
-  P.side[1] = std::move(bk);
+  P.segs.swap(out);
+  P.side[0] = bucket_side(S, B);  // the source side is now the bucket list
   return EMU_OK;
 }
 
@@ -855,7 +932,10 @@ int emu_plan_ex(const emu_layout_t* src, const emu_layout_t* dst, uint32_t flags
   return EMU_OK;
 }
 
-int emu_plan_to_buckets(const emu_layout_t* src, const emu_layout_t* dst, uint64_t bucket_bytes, emu_plan_t* out) {
+// emu_plan_to_buckets / emu_plan_from_buckets: the plan of (src, dst) with one side rewritten into
+// bucket space, then finalized again.
+static int bucket_plan(const emu_layout_t* src, const emu_layout_t* dst, uint64_t bucket_bytes, int side,
+                       emu_plan_t* out) {
   clear_error();
   if (!src || !dst || !out) return fail(EMU_ERR_NULL, "NULL argument");
   *out = nullptr;
@@ -868,7 +948,7 @@ int emu_plan_to_buckets(const emu_layout_t* src, const emu_layout_t* dst, uint64
     g_plans.erase(P);
   }
   try {
-    rc = to_buckets(*P, bucket_bytes);
+    rc = side == 1 ? to_buckets(*P, bucket_bytes) : from_buckets(*P, bucket_bytes);
     if (!rc) rc = finalize(*P);
   } catch (const std::bad_alloc&) {
     rc = fail(EMU_ERR_ARG, "out of host memory");
@@ -883,6 +963,14 @@ int emu_plan_to_buckets(const emu_layout_t* src, const emu_layout_t* dst, uint64
   }
   *out = base;
   return EMU_OK;
+}
+
+int emu_plan_to_buckets(const emu_layout_t* src, const emu_layout_t* dst, uint64_t bucket_bytes, emu_plan_t* out) {
+  return bucket_plan(src, dst, bucket_bytes, 1, out);
+}
+
+int emu_plan_from_buckets(const emu_layout_t* src, const emu_layout_t* dst, uint64_t bucket_bytes, emu_plan_t* out) {
+  return bucket_plan(src, dst, bucket_bytes, 0, out);
 }
 
 int emu_plan_free(emu_plan_t plan) {

@@ -149,6 +149,8 @@ def load(path: str = LIB_PATH):
                         ctypes.c_int),
         "emu_plan_to_buckets": ([ctypes.POINTER(c_layout), ctypes.POINTER(c_layout), U64, ctypes.POINTER(P)],
                                 ctypes.c_int),
+        "emu_plan_from_buckets": ([ctypes.POINTER(c_layout), ctypes.POINTER(c_layout), U64, ctypes.POINTER(P)],
+                                  ctypes.c_int),
         "emu_plan_free": ([P], ctypes.c_int),
         "emu_plan_info": ([P, ctypes.POINTER(c_plan_info)], ctypes.c_int),
         "emu_tensor_info": ([P, I32, I32, ctypes.POINTER(c_tensor_desc)], ctypes.c_int),
@@ -268,20 +270,27 @@ class ShardSet:
 class Plan:
     """A compiled copy map between two layouts (``emu_plan``)."""
 
-    def __init__(self, src: Layout, dst: Layout, bucket_bytes: int = 0, alias: bool = False):
+    def __init__(self, src: Layout, dst: Layout, bucket_bytes: int = 0, alias: bool = False,
+                 src_bucket_bytes: int = 0):
         """bucket_bytes > 0 compiles the fused map (``emu_plan_to_buckets``): its destination side is
-        the destination ranks' buckets of that size. alias=True leaves destination tensors that are byte
-        copies of a whole source tensor out of the map (``emu_plan_ex`` with EMU_PLAN_ALIAS_RESIDENT);
-        ``alloc(1, alias=S)`` makes them views of the source set S."""
+        the destination ranks' buckets of that size. src_bucket_bytes > 0 compiles the receiver's map
+        (``emu_plan_from_buckets``): its source side is the source ranks' buckets of that size. alias=True
+        leaves destination tensors that are byte copies of a whole source tensor out of the map
+        (``emu_plan_ex`` with EMU_PLAN_ALIAS_RESIDENT); ``alloc(1, alias=S)`` makes them views of the
+        source set S."""
         lib = load()
-        self.src, self.dst, self.bucket_bytes = src, dst, bucket_bytes
+        self.src, self.dst, self.bucket_bytes, self.src_bucket_bytes = src, dst, bucket_bytes, src_bucket_bytes
         self._uploads = {}  # data_ptr -> workspace tensor this plan uploaded to (kept alive)
         cs, cd = src.c(), dst.c()
         h = ctypes.c_void_p()
+        if (bucket_bytes or src_bucket_bytes) and alias:
+            raise ValueError("a bucket plan has buckets on one side: nothing to alias")
+        if bucket_bytes and src_bucket_bytes:
+            raise ValueError("give bucket_bytes (destination buckets) or src_bucket_bytes (source buckets), not both")
         if bucket_bytes:
-            if alias:
-                raise ValueError("a fused plan's destination is its buckets: nothing to alias")
             check(lib.emu_plan_to_buckets(ctypes.byref(cs), ctypes.byref(cd), bucket_bytes, ctypes.byref(h)))
+        elif src_bucket_bytes:
+            check(lib.emu_plan_from_buckets(ctypes.byref(cs), ctypes.byref(cd), src_bucket_bytes, ctypes.byref(h)))
         else:
             check(lib.emu_plan_ex(ctypes.byref(cs), ctypes.byref(cd), 1 if alias else 0, ctypes.byref(h)))
         self._h = h

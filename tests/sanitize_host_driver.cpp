@@ -107,6 +107,8 @@ bool plans() {
         const uint64_t B = (a.dtype == EMU_FP32 ? 4u : 2u) * (1 + rnd(40));
         if (!expect(emu_plan_to_buckets(&a, &b, B, &p), EMU_OK, "micro fused plan") || !walk(p)) return false;
       }
+      const uint64_t Bs = (a.dtype == EMU_FP32 ? 4u : 2u) * (1 + rnd(40));  // whole source elements
+      if (!expect(emu_plan_from_buckets(&a, &b, Bs, &p), EMU_OK, "micro receiver plan") || !walk(p)) return false;
     }
   const emu_model_t m8 = {32, 4096, 32, 8, 128, 14336, 128256};
   const emu_layout_t pairs[][2] = {
@@ -121,6 +123,8 @@ bool plans() {
     if (pr[0].dtype == pr[1].dtype)
       for (uint64_t B : {1ull << 28, (1ull << 28) - 2})
         if (!expect(emu_plan_to_buckets(&pr[0], &pr[1], B, &p), EMU_OK, "8B fused plan") || !walk(p)) return false;
+    for (uint64_t B : {1ull << 28, (1ull << 28) - 4})
+      if (!expect(emu_plan_from_buckets(&pr[0], &pr[1], B, &p), EMU_OK, "8B receiver plan") || !walk(p)) return false;
   }
   return true;
 }

@@ -177,6 +177,48 @@ def test_8b_uploaded_workspaces_match_host_image(gpu_lib):
     cleanup()
 
 
+def test_8b_receiver_plans_from_buckets(gpu_lib):
+    """Receiver plans (emu_plan_from_buckets) on the benchmark transition: the TP4PP1 destination set
+    packed into 2^28- and 2^28-2-byte buckets and restored by TP4PP1 -> TP4PP1 plans reading those
+    buckets equals the destination set; the TP2PP2 source set packed into 2^28-byte buckets and resharded
+    straight into TP4PP1 tensors equals emu_reshard's result, which is checked against the oracle."""
+    import torch
+
+    m = emu.Model(*EIGHT_B)
+    src, dst = emu.Layout(m, 2, 2), emu.Layout(m, 4, 1)
+    p = emu.Plan(src, dst)
+    ws = p.workspace()
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
+    fill_device(p, 0, S, seed=91)
+    make_consistent_replicas(p, 0, S)  # buckets carry every replica; a consistent state holds equal ones
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], "8B reshard")
+    check_reshard(p, S, D, label="8B TP2PP2->TP4PP1 (reference for the receiver plans)")
+    for B in (1 << 28, (1 << 28) - 2):
+        bufs, bptrs = p.alloc_buckets(1, B, fill=0x77, guard=GUARD)
+        guarded(lambda: p.pack(ws, 1, B, D.ptrs, bptrs), D.tensors, [(bufs, 0x77)], f"pack B={B}")
+        u = emu.Plan(dst, dst, src_bucket_bytes=B)
+        wu = u.workspace()
+        R = u.alloc(1, fill=0x11, guard=GUARD)
+        guarded(lambda: u.reshard(wu, bptrs, R.ptrs), bufs, [(R.tensors, 0x11)], f"receiver unpack B={B}")
+        for i, (x, y) in enumerate(zip(D.tensors, R.tensors)):
+            assert torch.equal(x, y), f"receiver unpack B={B}: tensor {i} differs"
+        say(f"  receiver unpack B={B}: {len(R.tensors)} tensors equal the destination set")
+        del bufs, bptrs, R, wu, u
+        cleanup()
+    B = 1 << 28
+    sbufs, sbptrs = p.alloc_buckets(0, B, fill=0x33, guard=GUARD)
+    guarded(lambda: p.pack(ws, 0, B, S.ptrs, sbptrs), S.tensors, [(sbufs, 0x33)], "pack source B=2^28")
+    f = emu.Plan(src, dst, src_bucket_bytes=B)
+    wf = f.workspace()
+    R2 = f.alloc(1, fill=0x22, guard=GUARD)
+    guarded(lambda: f.reshard(wf, sbptrs, R2.ptrs), sbufs, [(R2.tensors, 0x22)], "receiver reshard from buckets")
+    for i, (x, y) in enumerate(zip(D.tensors, R2.tensors)):
+        assert torch.equal(x, y), f"receiver reshard: tensor {i} differs"
+    del S, D, sbufs, sbptrs, R2, ws, wf
+    cleanup()
+
+
 def _pack_check(p, ws, D, B, label, S=None, pack_too=False):
     """Fill buckets of size B -- with emu_pack_buckets from D, or, when the source set S is given, with
     the fused source -> bucket plan (and with emu_pack_buckets as well when pack_too) -- and compare every

@@ -782,3 +782,41 @@ def test_same_layout_is_a_copy(dtype, fmt):
             assert torch.equal(t[:n], s_[:n]), (tp, pp, pad, d)
             assert int(t[n:].count_nonzero()) == 0, (tp, pp, pad, d)
         assert (pad == 0) == all(n == descs[i]["bytes"] for i, n in real.items())
+
+
+@pytest.mark.parametrize("B", [30, 4096, (1 << 16) - 2])
+def test_from_buckets_plans_small(B):
+    """Receiver-side plans (emu_plan_from_buckets): source shards packed by the oracle into buckets of B
+    bytes are restored -- or resharded into another layout -- by the reshard kernel in one pass, every
+    byte against oracle.reshard, with the write footprint checked: unpack (same layout), a TP/PP change,
+    format change with padded source rows, zero-filled destination pad rows, and the fp32 -> bf16 and
+    bf16 -> fp32 conversions where B holds whole source elements."""
+    import torch
+
+    m = emu.Model(*TINY)
+    L = lambda *a: emu.Layout(m, *a)
+    pairs = [(L(2, 1), L(2, 1)), (L(1, 1), L(2, 1)),
+             (L(2, 2, 128), L(1, 1, 0, "bf16", "separate", "separate")), (L(1, 1, 128), L(2, 2, 384)),
+             (L(2, 1, 0, "fp32"), L(1, 2, 0, "bf16")), (L(1, 2, 0, "bf16"), L(2, 1, 0, "fp32"))]
+    for src, dst in pairs:
+        if B % (4 if src.dtype == "fp32" else 2):
+            continue
+        os_, od = o_layout(src), o_layout(dst)
+        shards = oracle.shard(full_model(os_.model, 41, src.dtype), os_)
+        plan = emu.Plan(src, dst, src_bucket_bytes=B)
+        ws = plan.workspace()
+        K = plan.alloc(0, fill=0x5A, guard=GUARD)  # the source side is the bucket list
+        packed = [b for rank in shards for b in oracle.pack(rank, B)]
+        assert len(packed) == len(K.tensors)
+        for t, b in zip(K.tensors, packed):
+            t.copy_(torch.from_numpy(np.ascontiguousarray(b).reshape(-1).view(np.uint8).copy()))
+        D = plan.alloc(1, fill=0xA5, guard=GUARD)
+        label = f"from buckets B={B} {src.dtype} TP{src.tp}PP{src.pp} -> {dst.dtype} TP{dst.tp}PP{dst.pp}"
+        g = Guard(keep=K.tensors, fills=[(D.tensors, 0xA5)], label=label)
+        plan.reshard(ws, K.ptrs, D.ptrs)
+        torch.cuda.synchronize()
+        g.check()
+        want = [np.ascontiguousarray(a).reshape(-1).view(np.uint8) for rank in oracle.reshard(shards, os_, od)
+                for a in rank]
+        for i, (t, w) in enumerate(zip(D.tensors, want)):
+            assert np.array_equal(t.cpu().numpy(), w), f"{label}: tensor {i}"

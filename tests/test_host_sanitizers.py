@@ -1,7 +1,7 @@
 """The host half of the library (plan compiler and transition-DAG planner) built with g++ under
 AddressSanitizer, UndefinedBehaviorSanitizer and LeakSanitizer, driven through the C ABI by
 tests/sanitize_host_driver.cpp: every micro layout pair sampled in both element types, fused,
-converting and alias plans, the 8B plans, bucket geometry and per-bucket records, the workspace image
+converting, alias and receiver (from-buckets) plans, the 8B plans, bucket geometry and per-bucket records, the workspace image
 (the host's copy of the tile and chunk maps the upload builds on the device), table checks, the DAG
 planner on random and malformed scenarios, and the error paths. Any report, or any unexpected status,
 fails the run."""

@@ -439,6 +439,85 @@ def test_fused_plan_errors():
     assert lib.emu_pack_buckets(p._h, fake, 1, 64, fake, fake, None) == -4
 
 
+def check_from_buckets(src, dst, B, full=None, seed=13):
+    """The receiver's plan (source side: the source ranks' buckets of size B) against the oracle: the
+    source shards packed by oracle.pack, run through the plan's segment table, must give
+    oracle.reshard of the shards. Replicas past their first holder are perturbed, so that reading
+    one shows."""
+    plan = emu.Plan(src, dst, src_bucket_bytes=B)
+    os_, od = o_layout(src), o_layout(dst)
+    if full is None:
+        full = full_model(os_.model, seed, src.dtype)
+    src_shards = oracle.shard(full, os_)
+    for r, specs in enumerate(oracle.rank_inventory(os_)):
+        for j, sp in enumerate(specs):
+            if sp.kind.endswith("norm") and r % os_.tp:
+                src_shards[r][j] = src_shards[r][j] + np.array(1, dtype=src_shards[r][j].dtype)
+    buckets = [b for rank in src_shards for b in oracle.pack(rank, B)]
+    descs = plan.tensors(0)
+    assert [d["kind"] for d in descs] == ["bucket"] * len(buckets)
+    assert [d["bytes"] for d in descs] == [b.size for b in buckets]
+    want = [np.ascontiguousarray(a).reshape(-1).view(np.uint8) for rank in oracle.reshard(src_shards, os_, od)
+            for a in rank]
+    got = run_plan(plan.segments(), buckets, [w.size for w in want])
+    for i, (g, w) in enumerate(zip(got, want)):
+        assert np.array_equal(g, w), (src, dst, B, i)
+    return plan
+
+
+@pytest.mark.parametrize("B", [8, 30, 64, 1000, 4094, 1 << 20])
+def test_from_buckets_plan_matches_oracle_micro(B):
+    lays = MICRO_LAYS[::5]
+    full = full_model(o_layout(lays[0]).model)
+    for i, src in enumerate(lays):
+        for dst in lays[i % 3::3] + [src]:  # dst == src: the plan is an unpack
+            check_from_buckets(src, dst, B, full)
+
+
+def test_from_buckets_plan_matches_oracle_tiny_kv_and_conversion():
+    m = emu.Model(*TINY)
+    for B in (1 << 16, (1 << 16) - 2, 12345 * 2):
+        check_from_buckets(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1), B)
+        check_from_buckets(emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 1, 0, "bf16", "separate", "separate"), B)
+        check_from_buckets(emu.Layout(m, 1, 1, 128), emu.Layout(m, 2, 2, 384), B)  # zero-filled pad rows
+    check_from_buckets(emu.Layout(m, 2, 1, 0, "fp32"), emu.Layout(m, 1, 2, 0, "bf16"), 4 * 1001)
+    check_from_buckets(emu.Layout(m, 2, 1, 0, "bf16"), emu.Layout(m, 4, 2, 0, "fp32"), 2 * 1001)
+    mk = emu.Model(*MICRO_KV)
+    full = full_model(o_layout(emu.Layout(mk, 1, 1)).model, 23)
+    for B in (6, 40, 4096):
+        check_from_buckets(emu.Layout(mk, 8, 3, 2), emu.Layout(mk, 2, 1), B, full)
+        check_from_buckets(emu.Layout(mk, 1, 2), emu.Layout(mk, 8, 3, 2), B, full)
+
+
+@pytest.mark.parametrize("B", [1 << 28, (1 << 28) - 2, 256 * 10**6])
+def test_from_buckets_plan_exact_cover_8b(B):
+    m = emu.Model(*EIGHT_B)
+    for src, dst in ((emu.Layout(m, 4, 1), emu.Layout(m, 4, 1)), (emu.Layout(m, 2, 2), emu.Layout(m, 4, 1))):
+        plan = emu.Plan(src, dst, src_bucket_bytes=B)
+        base = emu.Plan(src, dst)
+        nb, sb = base.bucket_layout(0, B, -1)
+        assert plan.info["n_src_tensors"] == nb
+        assert plan.info["bytes_read"] == base.info["bytes_read"] and plan.info["bytes_written"] == base.info["bytes_written"]
+        exact_cover(plan)
+        if B % 16 == 0:
+            assert plan.info["n_general_segments"] == 0
+
+
+def test_from_buckets_plan_errors():
+    m = emu.Model(*TINY)
+    lib = emu.load()
+    a, b, h = emu.Layout(m, 1, 1).c(), emu.Layout(m, 2, 1).c(), ctypes.c_void_p()
+    f, fb = emu.Layout(m, 1, 1, 0, "fp32").c(), emu.Layout(m, 2, 1, 0, "bf16").c()
+    assert lib.emu_plan_from_buckets(ctypes.byref(a), ctypes.byref(b), 0, ctypes.byref(h)) == -6
+    assert lib.emu_plan_from_buckets(ctypes.byref(a), ctypes.byref(b), 3, ctypes.byref(h)) == -6
+    assert lib.emu_plan_from_buckets(ctypes.byref(f), ctypes.byref(fb), 6, ctypes.byref(h)) == -6  # fp32 source
+    assert lib.emu_plan_from_buckets(ctypes.byref(f), ctypes.byref(fb), 8, ctypes.byref(h)) == 0
+    assert lib.emu_plan_free(h) == 0
+    assert lib.emu_plan_from_buckets(None, ctypes.byref(b), 64, ctypes.byref(h)) == -1
+    with pytest.raises(ValueError):
+        emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1), bucket_bytes=64, src_bucket_bytes=64)
+
+
 # ------------------------------------------------------------------------------------------------
 # element-converting reshard (fp32 training state <-> bf16 generation weights)
 # ------------------------------------------------------------------------------------------------
