@@ -77,6 +77,19 @@ int main(void) {
     free(bk);
   }
   {
+    /* the receiver's plan: its source side is the source ranks' 2^28-byte buckets */
+    emu_plan_t rp = NULL;
+    emu_plan_info_t ri;
+    uint64_t nb = 0, sb = 0;
+    CHECK(emu_plan_from_buckets(&src, &dst, 1ull << 28, &rp));
+    CHECK(emu_plan_info(rp, &ri));
+    CHECK(emu_bucket_layout(plan, 0, 1ull << 28, -1, &nb, &sb));
+    printf("receiver %d %d %llu %d\n", ri.n_src_tensors, ri.n_dst_tensors, (unsigned long long)nb,
+           ri.bytes_written == info.bytes_written);
+    CHECK(emu_plan_free(rp));
+    printf("receiver_odd %s\n", emu_status_str(emu_plan_from_buckets(&src, &dst, 3, &rp)));
+  }
+  {
     /* the workspace image: refused for a buffer one byte short, filled for a whole one */
     uint8_t* img = (uint8_t*)malloc((size_t)info.workspace_bytes);
     uint64_t k, nz = 0;

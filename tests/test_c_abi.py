@@ -51,6 +51,10 @@ def test_header_compiles_as_c99_and_host_calls_work(client):
     n_dst41 = sum(len(r) for r in oracle.rank_inventory(oracle.Layout(om, 4, 1)))
     assert client["alias"] == f"{n_dst41} 1 {dst_bytes} 0 0"
     assert client["image_short"] == "EMU_ERR_WORKSPACE" and client["image_nonzero"] == "1"
+    src_streams = [sum(s.numel * 2 for s in r) for r in oracle.rank_inventory(src)]
+    n_src_buckets = sum(-(-n // (1 << 28)) for n in src_streams)
+    assert client["receiver"] == f"{n_src_buckets} {n_dst} {n_src_buckets} 1"
+    assert client["receiver_odd"] == "EMU_ERR_BUCKET"
     assert client["freed_again"] == "EMU_ERR_HANDLE"
     n_nodes, n_edges, l_tran = client["dag"].split()
     py = emu.dag_plan([dict(kind=2, tp=4, pp=8, dp=1, gpus=list(range(32)), tgt_tp=8, tgt_pp=2, tgt_dp=1,
