@@ -200,11 +200,29 @@ def tiny_latency(emu, iters=200):
             fstep()
     f_replay10 = timed(fgraph10.replay) / 10
     ok = ok and all(torch.equal(x, y) for x, y in zip(D.tensors, R2.tensors))
+    # the same path with the receiver's own plan (buckets -> tensors on the reshard kernel)
+    recv = emu.Plan(plan.dst, plan.dst, src_bucket_bytes=B)
+    wr = recv.workspace()
+    R3 = plan.alloc(1)
+
+    def rstep():
+        fused.reshard(wf, S.ptrs, fbptrs)
+        recv.reshard(wr, fbptrs, R3.ptrs)
+
+    r_eager = timed(rstep)
+    rgraph10 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(rgraph10, stream=cap):
+        for _ in range(10):
+            rstep()
+    r_replay10 = timed(rgraph10.replay) / 10
+    ok = ok and all(torch.equal(x, y) for x, y in zip(D.tensors, R3.tensors))
     return {"workload": "tiny decoder bf16 TP1PP1->TP2PP1 + pack/unpack at 64 KiB buckets",
             "destination_bytes": plan.info["bytes_written"], "eager_us_per_step": round(eager, 2),
             "graph_us_per_step": round(replay, 2), "graph_of_10_steps_us_per_step": round(replay10, 2),
             "fused_to_buckets_then_unpack": {"eager_us_per_step": round(f_eager, 2),
                                              "graph_of_10_steps_us_per_step": round(f_replay10, 2)},
+            "fused_to_buckets_then_receiver_plan": {"eager_us_per_step": round(r_eager, 2),
+                                                    "graph_of_10_steps_us_per_step": round(r_replay10, 2)},
             "outputs_consistent": ok}
 
 
