@@ -26,9 +26,11 @@ FORMATS = [("interleaved", "block"), ("separate", "separate"), ("interleaved", "
 GUARD = 48  # bytes of prefilled guard band around every tensor and bucket view
 
 
-def run_pair(src, dst, seed=5, options=None, bucket_sizes=(), fused=False):
-    """Reshard (and pack / unpack / fused plan) one layout pair on seeded oracle shards; every output
-    byte against the oracle, and every call's write footprint checked (Guard)."""
+def run_pair(src, dst, seed=5, options=None, bucket_sizes=(), fused=False, receiver_bucket=0):
+    """Reshard (and pack / unpack / fused plan / receiver plan) one layout pair on seeded oracle shards;
+    every output byte against the oracle, and every call's write footprint checked (Guard). With
+    receiver_bucket, the source set is packed into buckets of that size and the receiver plan
+    (emu_plan_from_buckets) must rebuild the destination set from them."""
     import torch
 
     for k, v in (options or {}).items():
@@ -76,6 +78,23 @@ def run_pair(src, dst, seed=5, options=None, bucket_sizes=(), fused=False):
             g.check()
             for k, (a, b) in enumerate(zip(bufs, fbufs)):
                 assert torch.equal(a, b), f"fused bucket {k} differs (B={B})"
+    if receiver_bucket:
+        Bs = receiver_bucket
+        sbufs, sbptrs = plan.alloc_buckets(0, Bs, fill=0x44, guard=GUARD)
+        g = Guard(keep=S.tensors, fills=[(sbufs, 0x44)], label=f"pack source Bs={Bs} {label}")
+        plan.pack(ws, 0, Bs, S.ptrs, sbptrs)
+        torch.cuda.synchronize()
+        g.check()
+        rp = emu.Plan(src, dst, src_bucket_bytes=Bs)
+        rws = rp.workspace()
+        R2 = rp.alloc(1, fill=0x66, guard=GUARD)
+        rp.check_tables(sbptrs, R2.ptrs)
+        g = Guard(keep=sbufs, fills=[(R2.tensors, 0x66)], label=f"receiver Bs={Bs} {label}")
+        rp.reshard(rws, sbptrs, R2.ptrs)
+        torch.cuda.synchronize()
+        g.check()
+        for i, (a, b) in enumerate(zip(D.tensors, R2.tensors)):
+            assert torch.equal(a, b), f"receiver plan (Bs={Bs}): tensor {i} differs"
     return plan
 
 
@@ -109,8 +128,9 @@ def random_valid_layout(rng, model, dtype):
 @pytest.mark.parametrize("row_wrap", [1, 0], ids=["row_wrap", "whole_rows"])
 def test_random_layout_pairs(gpu_lib, row_wrap):
     """400 random valid layout pairs on random small models, each with a random bucket size: reshard,
-    pack and unpack bit-exact against the oracle, and the fused source -> bucket plan giving the same
-    buckets. Of the 400: 206 have byte-granular segments (odd widths
+    pack and unpack bit-exact against the oracle, the fused source -> bucket plan giving the same
+    buckets, and the receiver plan rebuilding the destination set from the source set's buckets (of
+    another size). Of the 400: 206 have byte-granular segments (odd widths
     put runs at every 16-byte phase), 203 convert between fp32 and bf16, 133 zero-fill pad rows, 177
     replicate KV heads and 141 have uneven pipeline stages. Run once with row-wrapping tiles for 2D
     segments (the default) and once with whole-row tiles and row slices."""
@@ -134,7 +154,9 @@ def _random_pairs(rng):
         src = random_valid_layout(rng, model, rng.choice(["bf16", "fp32"]))
         dst = random_valid_layout(rng, model, rng.choice(["bf16", "fp32"]))
         es = 2 if dst.dtype == "bf16" else 4
-        run_pair(src, dst, seed=n, bucket_sizes=(es * rng.randint(1, 700),), fused=True)
+        ess = 2 if src.dtype == "bf16" else 4  # the receiver's bucket size, from the pair index: same pairs
+        run_pair(src, dst, seed=n, bucket_sizes=(es * rng.randint(1, 700),), fused=True,
+                 receiver_bucket=ess * (1 + n * 7919 % 700))
         n += 1
     say(f"  {n} random layout pairs bit-exact")
 
