@@ -12,6 +12,8 @@ and N written), which calibrates FETCH_SIZE / WRITE_SIZE. Workloads (--workload)
            unpack B - 2 per round.
   formats  8B TP2 PP2 -> TP4 PP1 into fused q/k/v and gate/up tensors, then into separate ones, on the
            same source and destination pages, --repeat times each, alternating.
+  receiver 8B TP2 PP2 source set packed into 2^28-byte buckets (emu_pack_buckets, source side), then
+           the receiver plan (emu_plan_from_buckets) resharding those buckets into TP4 PP1 tensors.
 
 Example (from /tmp with TMPDIR=/tmp):
 
@@ -123,9 +125,31 @@ def formats_workload(torch, emu, device_fill, repeat):
           f"on shared pages; calibration copies {n} B", flush=True)
 
 
+def receiver_workload(torch, emu, device_fill):
+    m = emu.Model(*EIGHT_B)
+    src, dst = emu.Layout(m, 2, 2), emu.Layout(m, 4, 1)
+    plan = emu.Plan(src, dst)
+    ws = plan.workspace()
+    B = 1 << 28
+    recv = emu.Plan(src, dst, src_bucket_bytes=B)
+    wr = recv.workspace()
+    S, R = plan.alloc(0), plan.alloc(1)
+    bufs, bptrs = plan.alloc_buckets(0, B)
+    device_fill(S.tensors, 1, ["weight"] * len(S.tensors))
+    for b in R.bufs:
+        b.zero_()
+    torch.cuda.synchronize()
+    n = calibrate(torch, S.bufs, R.bufs)
+    plan.pack(ws, 0, B, S.ptrs, bptrs)
+    recv.reshard(wr, bptrs, R.ptrs)
+    torch.cuda.synchronize()
+    print(f"profile_once: receiver {recv.info['bytes_read']} B read + {recv.info['bytes_written']} B written; "
+          f"calibration copies {n} B", flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--workload", choices=["main", "shifted", "formats"], default="main")
+    ap.add_argument("--workload", choices=["main", "shifted", "formats", "receiver"], default="main")
     ap.add_argument("--repeat", type=int, default=1)
     args = ap.parse_args()
     import torch
@@ -138,6 +162,8 @@ def main():
         main_workload(torch, emu, device_fill)
     elif args.workload == "shifted":
         shifted_workload(torch, emu, device_fill, args.repeat)
+    elif args.workload == "receiver":
+        receiver_workload(torch, emu, device_fill)
     else:
         formats_workload(torch, emu, device_fill, args.repeat)
 
