@@ -219,6 +219,36 @@ def test_8b_receiver_plans_from_buckets(gpu_lib):
     cleanup()
 
 
+def test_8b_padded_receiver_plan_phase_shifted(gpu_lib):
+    """The padded workload's receiver side: the TP8PP4 (vocabulary padded to TP*128) source set packed
+    into 2^28-2-byte buckets, every bucket at another 16-byte phase, and resharded from them straight
+    into TP2PP2 tensors (the byte-granular path at full size) equals emu_reshard's result, which is
+    checked against the oracle; source pad rows hold random values and must not be read."""
+    import torch
+
+    m = emu.Model(*EIGHT_B)
+    src, dst = emu.Layout(m, 8, 4, 128), emu.Layout(m, 2, 2, 128)
+    p = emu.Plan(src, dst)
+    ws = p.workspace()
+    S = p.alloc(0, fill=0x5A, guard=GUARD)
+    fill_device(p, 0, S, seed=57)
+    D = p.alloc(1, fill=0xA5, guard=GUARD)
+    guarded(lambda: p.reshard(ws, S.ptrs, D.ptrs), S.tensors, [(D.tensors, 0xA5)], "8B padded reshard")
+    check_reshard(p, S, D, label="8B TP8PP4(pad)->TP2PP2 (reference for the receiver plan)")
+    B = (1 << 28) - 2
+    sbufs, sbptrs = p.alloc_buckets(0, B, fill=0x33, guard=GUARD)
+    guarded(lambda: p.pack(ws, 0, B, S.ptrs, sbptrs), S.tensors, [(sbufs, 0x33)], "pack source B=2^28-2")
+    f = emu.Plan(src, dst, src_bucket_bytes=B)
+    assert f.info["n_general_segments"] > 0
+    wf = f.workspace()
+    R = f.alloc(1, fill=0x22, guard=GUARD)
+    guarded(lambda: f.reshard(wf, sbptrs, R.ptrs), sbufs, [(R.tensors, 0x22)], "receiver reshard B=2^28-2")
+    for i, (x, y) in enumerate(zip(D.tensors, R.tensors)):
+        assert torch.equal(x, y), f"receiver reshard B=2^28-2: tensor {i} differs"
+    del S, D, sbufs, sbptrs, R, ws, wf
+    cleanup()
+
+
 def _pack_check(p, ws, D, B, label, S=None, pack_too=False):
     """Fill buckets of size B -- with emu_pack_buckets from D, or, when the source set S is given, with
     the fused source -> bucket plan (and with emu_pack_buckets as well when pack_too) -- and compare every
