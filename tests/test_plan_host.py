@@ -887,3 +887,29 @@ def test_workspace_image_tile_map():
             nxt[sec] += int(counts[i])
         assert nxt == [n_copy, z0 + n_zero]
         assert np.array_equal(tm, want)
+
+
+def test_sender_and_receiver_plans_compose():
+    """The transport end to end on the host: a sender's fused plan L -> L' into buckets of B, then a
+    receiver plan L' -> L'' out of those buckets, gives the oracle's direct reshard L -> L'' (the
+    composition through an intermediate layout, section 6.1's T_sub route, with the contiguous transfer
+    of section 6.2 between the two halves)."""
+    m = emu.Model(*MICRO)
+    lays = [emu.Layout(m, tp, pp, pad, "bf16", q, g) for tp, pp, pad, (q, g) in
+            ((1, 1, 0, ("interleaved", "block")), (2, 2, 2, ("separate", "separate")), (4, 1, 0, ("interleaved", "separate")),
+             (2, 4, 2, ("separate", "block")))]
+    full = full_model(o_layout(lays[0]).model, 31)
+    for a, b, c in itertools.permutations(lays, 3):
+        oa, oc = o_layout(a), o_layout(c)
+        shards = oracle.shard(full, oa)
+        flat = [np.ascontiguousarray(x).reshape(-1).view(np.uint8) for rank in shards for x in rank]
+        for B in (6, 64, 1000):
+            send = emu.Plan(a, b, bucket_bytes=B)
+            buckets = run_plan(send.segments(), flat, [d["bytes"] for d in send.tensors(1)])
+            recv = emu.Plan(b, c, src_bucket_bytes=B)
+            assert [d["bytes"] for d in recv.tensors(0)] == [x.size for x in buckets]
+            got = run_plan(recv.segments(), buckets, [d["bytes"] for d in recv.tensors(1)])
+            want = [np.ascontiguousarray(x).reshape(-1).view(np.uint8) for rank in oracle.reshard(shards, oa, oc)
+                    for x in rank]
+            for i, (g, w) in enumerate(zip(got, want)):
+                assert np.array_equal(g, w), (a, b, c, B, i)
