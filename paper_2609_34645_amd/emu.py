@@ -454,6 +454,31 @@ class Plan:
         return bufs, ptr_table(bufs, device)
 
     # -- execution -----------------------------------------------------------------------------
+    def shard_set(self, side: int, tensors, device=None) -> ShardSet:
+        """A ShardSet over the caller's own tensors of one side, in the plan's global order (rank 0's
+        first, canonical order within a rank; ``tensors(side)`` lists them). Each must be a contiguous
+        device tensor of exactly the plan's byte size for it, 16-byte aligned: the kernels trust the
+        pointer table, so a tensor of the wrong size would be written past its end. Raises ValueError
+        (EmuError -7 for alignment) before anything reaches the library."""
+        descs = self.tensors(side)
+        tensors = list(tensors)
+        if len(tensors) != len(descs):
+            raise ValueError(f"side {side} has {len(descs)} tensors, {len(tensors)} given")
+        _check_buffers(tensors, [d["bytes"] for d in descs], lambda i: f"{descs[i]['kind']} (rank {descs[i]['rank']})")
+        views = [t.view(-1).view(_uint8()) for t in tensors]
+        return ShardSet(tensors, views, ptr_table(tensors, device))
+
+    def bucket_set(self, side: int, bucket_bytes: int, buffers, device=None):
+        """(views, pointer table) over the caller's own bucket buffers of one side for bucket size
+        bucket_bytes, in pointer-table order (``bucket_info``): each a contiguous device tensor of exactly
+        its bucket's bytes, 16-byte aligned; checked as in ``shard_set``."""
+        info = self.bucket_info(side, bucket_bytes)
+        buffers = list(buffers)
+        if len(buffers) != len(info):
+            raise ValueError(f"side {side} has {len(info)} buckets of {bucket_bytes} bytes, {len(buffers)} given")
+        _check_buffers(buffers, [b["bytes"] for b in info], lambda i: f"bucket {info[i]['index']} of rank {info[i]['rank']}")
+        return [b.view(-1).view(_uint8()) for b in buffers], ptr_table(buffers, device)
+
     def reshard(self, ws, src_ptrs, dst_ptrs, stream=None):
         self._tables(ws, (src_ptrs, self._n[0], "src_ptrs"), (dst_ptrs, self._n[1], "dst_ptrs"))
         check(load().emu_reshard(self._h, ctypes.c_void_p(ws.data_ptr()), ctypes.c_void_p(src_ptrs.data_ptr()),
@@ -548,6 +573,28 @@ def _u64_array(ptrs):
         ptrs = ptrs.cpu().tolist()
     vals = [int(x) & 0xFFFFFFFFFFFFFFFF for x in ptrs]
     return (ctypes.c_uint64 * max(1, len(vals)))(*vals)
+
+
+def _uint8():
+    import torch
+
+    return torch.uint8
+
+
+def _check_buffers(bufs, sizes, name):
+    """Each buffer contiguous, of exactly its size in bytes, 16-byte aligned, on the device (in that
+    order, so that the host-side conditions are checked before the device one)."""
+    for i, (t, n) in enumerate(zip(bufs, sizes)):
+        nbytes = t.numel() * t.element_size()
+        if nbytes != n:
+            raise ValueError(f"{name(i)}: {nbytes} bytes, the plan needs {n}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name(i)}: not contiguous")
+        if t.data_ptr() % 16:
+            raise EmuError(-7, f"{name(i)}: address {t.data_ptr():#x} is not 16-byte aligned")
+    for i, t in enumerate(bufs):
+        if not t.is_cuda:
+            raise ValueError(f"{name(i)}: not a device tensor")
 
 
 def group_tables(sets, device=None):

@@ -842,3 +842,37 @@ def test_from_buckets_plans_small(B):
                 for a in rank]
         for i, (t, w) in enumerate(zip(D.tensors, want)):
             assert np.array_equal(t.cpu().numpy(), w), f"{label}: tensor {i}"
+
+
+def test_callers_own_tensors_and_buckets():
+    """A caller's own torch tensors (allocated one by one, in the plan's shapes and element type) and
+    bucket buffers, wrapped by Plan.shard_set / Plan.bucket_set: reshard and pack match the oracle."""
+    import torch
+
+    m = emu.Model(*TINY)
+    src, dst = emu.Layout(m, 2, 2, 128), emu.Layout(m, 1, 2, 0, "bf16", "separate", "separate")
+    plan = emu.Plan(src, dst)
+    ws = plan.workspace()
+    os_, od = o_layout(src), o_layout(dst)
+    shards = oracle.shard(full_model(os_.model, 43), os_)
+    mine_s = [torch.from_numpy(np.ascontiguousarray(a).view(np.int16).copy()).view(torch.bfloat16).cuda()
+              for rank in shards for a in rank]
+    mine_d = [torch.empty(tuple(d["shape"]), dtype=torch.bfloat16, device="cuda") for d in plan.tensors(1)]
+    S, D = plan.shard_set(0, mine_s), plan.shard_set(1, mine_d)
+    plan.check_tables(S.ptrs, D.ptrs)
+    plan.reshard(ws, S.ptrs, D.ptrs)
+    B = 1000
+    bufs = [torch.empty(b["bytes"], dtype=torch.uint8, device="cuda") for b in plan.bucket_info(1, B)]
+    views, bptrs = plan.bucket_set(1, B, bufs)
+    plan.pack(ws, 1, B, D.ptrs, bptrs)
+    torch.cuda.synchronize()
+    want = oracle.reshard(shards, os_, od)
+    flat = [np.ascontiguousarray(a) for rank in want for a in rank]
+    for i, (t, w) in enumerate(zip(mine_d, flat)):
+        assert np.array_equal(t.view(torch.int16).cpu().numpy().reshape(-1), w.view(np.int16).reshape(-1)), i
+    k = 0
+    for rank in want:
+        for b in oracle.pack(rank, B):
+            assert np.array_equal(views[k].cpu().numpy(), b), k
+            k += 1
+    assert k == len(bufs)

@@ -913,3 +913,42 @@ def test_sender_and_receiver_plans_compose():
                     for x in rank]
             for i, (g, w) in enumerate(zip(got, want)):
                 assert np.array_equal(g, w), (a, b, c, B, i)
+
+
+def test_shard_set_and_bucket_set_refuse_wrong_buffers():
+    """The binding's checks on a caller's own tensors and buckets, before any library call: count, byte
+    size, contiguity and 16-byte alignment (on host tensors, so that the device check comes last)."""
+    import torch
+
+    m = emu.Model(*TINY)
+    plan = emu.Plan(emu.Layout(m, 1, 1), emu.Layout(m, 2, 1))
+    descs = plan.tensors(1)
+    good = [torch.empty(d["bytes"] // 2, dtype=torch.bfloat16) for d in descs]
+    with pytest.raises(ValueError, match="tensors"):
+        plan.shard_set(1, good[:-1])
+    bad = list(good)
+    bad[3] = torch.empty(descs[3]["bytes"] // 2 + 1, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="bytes, the plan needs"):
+        plan.shard_set(1, bad)
+    bad = list(good)
+    bad[2] = torch.empty(2, descs[2]["bytes"] // 2, dtype=torch.bfloat16)[:, : descs[2]["bytes"] // 4].t()
+    with pytest.raises(ValueError):  # a strided view: wrong size or not contiguous
+        plan.shard_set(1, bad)
+    raw = torch.empty(descs[0]["bytes"] + 64, dtype=torch.uint8)
+    off = (16 - raw.data_ptr() % 16) % 16 + 2
+    bad = list(good)
+    bad[0] = raw[off:off + descs[0]["bytes"]]
+    with pytest.raises(emu.EmuError):
+        plan.shard_set(1, bad)
+    with pytest.raises(ValueError, match="device"):
+        plan.shard_set(1, good)
+    info = plan.bucket_info(1, 1 << 16)
+    bufs = [torch.empty(b["bytes"], dtype=torch.uint8) for b in info]
+    with pytest.raises(ValueError, match="buckets"):
+        plan.bucket_set(1, 1 << 16, bufs[1:])
+    bad = list(bufs)
+    bad[-1] = torch.empty(info[-1]["bytes"] + 2, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="bytes, the plan needs"):
+        plan.bucket_set(1, 1 << 16, bad)
+    with pytest.raises(ValueError, match="device"):
+        plan.bucket_set(1, 1 << 16, bufs)
