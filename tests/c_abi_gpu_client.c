@@ -160,6 +160,34 @@ int main(int argc, char** argv) {
   printf("tensors %d %d\n", ns, nd);
   printf("buckets %llu\n", (unsigned long long)nb);
   printf("unpack_equal %d\n", equal);
+  {
+    /* the receiver's own plan over the same buckets: destination layout to itself, read from buckets */
+    emu_plan_t rp = NULL;
+    emu_plan_info_t ri;
+    void* wsr;
+    int requal = 1;
+    EMUCHECK(emu_plan_from_buckets(&b, &b, B, &rp));
+    EMUCHECK(emu_plan_info(rp, &ri));
+    if ((uint64_t)ri.n_src_tensors != nb || ri.n_dst_tensors != nd) return 1;
+    HIPCHECK(hipMalloc(&wsr, ri.workspace_bytes));
+    EMUCHECK(emu_plan_upload(rp, wsr, ri.workspace_bytes, NULL));
+    for (i = 0; i < nd; ++i) HIPCHECK(hipMemset(R[i], 0x11, dsz[i]));
+    EMUCHECK(emu_reshard(rp, wsr, d_kp, d_rp, NULL));
+    HIPCHECK(hipDeviceSynchronize());
+    for (i = 0; i < nd && requal; ++i) {
+      void* x = malloc(dsz[i]);
+      void* y = malloc(dsz[i]);
+      if (!x || !y) return 1;
+      HIPCHECK(hipMemcpy(x, D[i], dsz[i], hipMemcpyDeviceToHost));
+      HIPCHECK(hipMemcpy(y, R[i], dsz[i], hipMemcpyDeviceToHost));
+      requal = memcmp(x, y, dsz[i]) == 0;
+      free(x);
+      free(y);
+    }
+    printf("receiver_equal %d\n", requal);
+    HIPCHECK(hipFree(wsr));
+    EMUCHECK(emu_plan_free(rp));
+  }
 
   for (i = 0; i < ns; ++i) HIPCHECK(hipFree(S[i]));
   for (i = 0; i < nd; ++i) {

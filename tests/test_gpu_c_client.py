@@ -55,6 +55,7 @@ def test_c_client_reshard_and_buckets(gpu_lib, tmp_path):
     assert facts["not_uploaded"] == "EMU_ERR_WORKSPACE"
     assert facts["upload_image_equal"] == "1"
     assert facts["unpack_equal"] == "1" and facts["done"] == "1"
+    assert facts["receiver_equal"] == "1"
     om = oracle.Model(*TINY)
     src, dst = oracle.Layout(om, 1, 1), oracle.Layout(om, 2, 1)
     want = oracle.reshard(source_shards(src), src, dst)
