@@ -525,6 +525,7 @@ static int from_buckets(Plan& P, uint64_t B) {
   }
   P.segs.swap(out);
   P.side[0] = bucket_side(S, B);  // the source side is now the bucket list
+  for (emu_tensor_desc_t& d : P.side[1].tensors) d.alias = -1;  // no destination tensor is a source tensor
   return EMU_OK;
 }
 

@@ -503,6 +503,17 @@ def test_from_buckets_plan_exact_cover_8b(B):
             assert plan.info["n_general_segments"] == 0
 
 
+def test_from_buckets_plan_reports_no_aliases():
+    """A receiver plan's source side is the bucket list: no destination tensor is a byte copy of a source
+    tensor any more, so none is reported as one (the plain plan of the same layouts reports 30)."""
+    m = emu.Model(*TINY)
+    a, b = emu.Layout(m, 2, 2), emu.Layout(m, 2, 1)
+    assert emu.Plan(a, b).info["n_alias_tensors"] == 30
+    p = emu.Plan(a, b, src_bucket_bytes=1 << 16)
+    assert p.info["n_alias_tensors"] == 0 and p.info["alias_bytes"] == 0 and p.info["aliased"] == 0
+    assert all(d["alias"] == -1 for d in p.tensors(1))
+
+
 def test_from_buckets_plan_errors():
     m = emu.Model(*TINY)
     lib = emu.load()
